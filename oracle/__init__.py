@@ -1,0 +1,114 @@
+"""Ember CPU oracle: test infrastructure only.
+
+A plain, slow, float64 C implementation of one step of Algorithm 1 ("Ember",
+Token Geometry, Section 2) and its ctypes binding.  Only the tests, the smoke
+check and the benchmark's CPU-baseline leg may import it; the product library
+never does, and the two share no code.  Arrays are numpy: fp32 data as
+``float32``, bf16 data as its raw ``uint16`` bit patterns.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "ember_oracle.c")
+_LIB = os.path.join(_HERE, "libember_oracle.so")
+
+F32 = 0
+BF16 = 1
+OK = 0
+BAD_ARG = -1
+BAD_INDEX = -6
+
+_lib = None
+
+
+def build() -> str:
+    """Compile the oracle with gcc (no fast-math, no FMA contraction)."""
+    cmd = ["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math",
+           "-fPIC", "-shared", _SRC, "-o", _LIB + ".tmp", "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(_LIB + ".tmp", _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB):
+        build()
+    lib = ctypes.CDLL(_LIB)
+    vp, i64, f32, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_float, ctypes.c_int
+    lib.ember_oracle_step.argtypes = [vp, i32, i64, vp, i32, i64, vp, i64,
+                                      vp, vp, i64, i64, i64, f32, f32, f32, i32]
+    lib.ember_oracle_step.restype = i32
+    lib.ember_oracle_bf16_to_f64.argtypes = [ctypes.c_uint16]
+    lib.ember_oracle_bf16_to_f64.restype = ctypes.c_double
+    lib.ember_oracle_f64_to_bf16.argtypes = [ctypes.c_double]
+    lib.ember_oracle_f64_to_bf16.restype = ctypes.c_uint16
+    lib.ember_oracle_state_bytes.argtypes = [i64, i64]
+    lib.ember_oracle_state_bytes.restype = i64
+    _lib = lib
+    return lib
+
+
+def _dtype_code(a: np.ndarray) -> int:
+    if a.dtype == np.float32:
+        return F32
+    if a.dtype == np.uint16:
+        return BF16
+    raise TypeError(f"oracle arrays are float32 or uint16 (bf16 bits), got {a.dtype}")
+
+
+def _ld(a: np.ndarray) -> int:
+    if a.ndim != 2 or a.strides[1] != a.itemsize or a.strides[0] % a.itemsize:
+        raise ValueError("2-D arrays with unit column stride expected")
+    return a.strides[0] // a.itemsize
+
+
+def step(W: np.ndarray, G: np.ndarray, r: np.ndarray, c: np.ndarray, t: int,
+         lr: float = 1e-3, beta2: float = 0.999, eps: float = 1e-8,
+         maximize: bool = False, idx: np.ndarray | None = None) -> int:
+    """One Ember step, in place on W, r and c.  Returns the oracle's status.
+
+    ``idx`` (int64) selects the sparse-row form: G then holds ``len(idx)``
+    rows, row k being the gradient of W's row ``idx[k]``.
+    """
+    lib = _load()
+    V, D = W.shape
+    if r.dtype != np.float32 or c.dtype != np.float32 or r.shape != (V,) or c.shape != (D,):
+        raise ValueError("r must be float32[V] and c float32[D]")
+    if not (r.flags.c_contiguous and c.flags.c_contiguous):
+        raise ValueError("r and c must be contiguous")
+    if idx is None:
+        if G.shape != (V, D):
+            raise ValueError("dense G must have W's shape")
+        idx_ptr, n_idx = None, 0
+    else:
+        idx = np.ascontiguousarray(idx, dtype=np.int64)
+        if G.shape != (idx.shape[0], D):
+            raise ValueError("sparse G must be [len(idx), D]")
+        idx_ptr, n_idx = idx.ctypes.data, idx.shape[0]
+    g_ptr = G.ctypes.data if G.size else None
+    g_ld = _ld(G) if G.shape[0] > 0 else D
+    return lib.ember_oracle_step(W.ctypes.data, _dtype_code(W), _ld(W),
+                                 g_ptr, _dtype_code(G), g_ld, idx_ptr, n_idx,
+                                 r.ctypes.data, c.ctypes.data, V, D, int(t),
+                                 float(lr), float(beta2), float(eps), int(bool(maximize)))
+
+
+def bf16_to_f64(bits: int) -> float:
+    return _load().ember_oracle_bf16_to_f64(int(bits))
+
+
+def f64_to_bf16(x: float) -> int:
+    return _load().ember_oracle_f64_to_bf16(float(x))
+
+
+def state_bytes(V: int, D: int) -> int:
+    return _load().ember_oracle_state_bytes(int(V), int(D))
