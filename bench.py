@@ -1,0 +1,255 @@
+#!/usr/bin/env python3
+"""Benchmark of the Ember step on one MI355X.
+
+Workload (one "step"): the Ember update of the two untied token tables of a
+model with a 128256-token vocabulary and width 4096, both bf16 with fp32
+state: the LM head takes a dense step (gradient with Zipf(1.1) per-row
+scales), the input embedding a sparse-row step (8 x 2048 Zipf(1.1) token ids
+per step, ~4650 distinct rows).  All inputs are synthetic, made before the
+timed region and resident in HBM.
+
+Prints one JSON line: whole-step throughput in algorithmic GB/s (the bytes
+the method must move, see paper_2607_01455_amd.workloads.algorithmic_bytes),
+ms per step, per-part times, the roofline of the dominant kernel (the dense
+apply pass, timed with HIP events around each launch), a plain device copy as
+a practical bandwidth ceiling, and the CPU oracle timed on a sample.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "Ember step ms + achieved HBM GB/s (% of peak) at V=128256, D=4096"
+PEAK_GBPS = 8000.0
+V, D = 128256, 4096
+KERNEL_SRC = os.path.join(ROOT, "paper_2607_01455_amd", "csrc", "ember_kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ember_apply_lmhead128k_traffic.json")
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=10)
+    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-rows", type=int, default=16384, help="rows of the oracle's sample")
+    return p.parse_args()
+
+
+def kernel_source_hash() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def traffic_for_current_kernel():
+    """HBM bytes per dense apply launch from committed PMC counters, if they were
+    taken on the current kernel source (else None)."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(rows: int, steps: int = 2):
+    """The oracle on the first `rows` rows of the LM-head table (dense, bf16)."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from paper_2607_01455_amd import workloads as wl
+
+    cfg = wl.Config("cpu_sample", rows, D, torch.bfloat16, torch.bfloat16, steps, "zipf_rows")
+    W = wl.make_weights(cfg, seed=21, device="cpu").contiguous().view(torch.int16).numpy().view(np.uint16).copy()
+    scales = (wl.zipf_probs(V) * V).float()[:rows]
+    r = np.zeros(rows, np.float32)
+    c = np.zeros(D, np.float32)
+    times = []
+    for t in range(1, steps + 1):
+        G = wl.make_dense_grad(cfg, t, seed=21, device="cpu", scales=scales)
+        G = G.contiguous().view(torch.int16).numpy().view(np.uint16)
+        t0 = time.perf_counter()
+        assert oracle.step(W, G, r, c, t) == 0
+        times.append(time.perf_counter() - t0)
+    sec = sum(times) / len(times)
+    gbps = wl.algorithmic_bytes(rows, D, 2, 2) / sec / 1e9
+    return {"value": round(gbps, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"dense bf16 step on the first {rows} of {V} LM-head rows x {D}, "
+                      f"{steps} steps, float64 C oracle, single thread; {sec * 1e3:.0f} ms/step"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the Ember step here runs on a single MI355X "
+              "(no sharding or collectives are built); run it with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2607_01455_amd import ember
+    from paper_2607_01455_amd import workloads as wl
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    K, Wm = args.steps, args.warmup
+    head_cfg = wl.CONFIGS["lmhead128k"]
+    emb_cfg = wl.CONFIGS["embed128k"]
+
+    # --- inputs, resident before timing -----------------------------------
+    W_head = wl.make_weights(head_cfg, seed=31, device=dev)
+    W_emb = wl.make_weights(emb_cfg, seed=32, device=dev)
+    scales = wl.row_scales(head_cfg, 31, dev)
+    n_grads = 4  # distinct dense gradients, reused round-robin (1 GiB each)
+    grads = [wl.make_dense_grad(head_cfg, t + 1, seed=31, device=dev, scales=scales) for t in range(n_grads)]
+    batches = [wl.make_sparse_batch(emb_cfg, t + 1, seed=32, device=dev) for t in range(K + Wm)]
+    head = ember.EmberTable(V, D, device=dev)
+    emb = ember.EmberTable(V, D, device=dev)
+    torch.cuda.synchronize()
+
+    def step(k):
+        head.step(W_head, grads[k % n_grads])
+        idx, Gr = batches[k]
+        emb.step_sparse_rows(W_emb, Gr, idx)
+
+    for k in range(Wm):
+        step(k)
+    torch.cuda.synchronize()
+    if ember.ember_get_error(emb.ws) != ember.EMBER_OK:
+        raise RuntimeError("sparse step reported an index error")
+
+    stream = torch.cuda.current_stream()
+
+    # --- timed region A: whole steps, with a marker between the two tables --
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    t_start.record(stream)
+    for k in range(K):
+        ev[k][0].record(stream)
+        head.step(W_head, grads[(Wm + k) % n_grads])
+        ev[k][1].record(stream)
+        idx, Gr = batches[Wm + k]
+        emb.step_sparse_rows(W_emb, Gr, idx)
+        ev[k][2].record(stream)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = t_start.elapsed_time(t_end)
+    ms_step = total_ms / K
+    dense_ms = sorted(e[0].elapsed_time(e[1]) for e in ev)[K // 2]
+    sparse_ms = sorted(e[1].elapsed_time(e[2]) for e in ev)[K // 2]
+    if ember.ember_get_error(emb.ws) != ember.EMBER_OK:
+        raise RuntimeError("sparse step reported an index error")
+
+    dense_bytes = wl.algorithmic_bytes(V, D, 2, 2)
+    n_rows = [int(b[0].numel()) for b in batches[Wm:Wm + K]]
+    sparse_bytes = [wl.algorithmic_bytes(V, D, 2, 2, rows=n) for n in n_rows]
+    step_bytes = dense_bytes + sum(sparse_bytes) / K
+    value = step_bytes / (ms_step * 1e-3) / 1e9
+
+    # --- timed region B: the same steps with HIP events around every kernel --
+    ember.ember_profile_enable(True)
+    torch.cuda.synchronize()
+    tb0 = torch.cuda.Event(enable_timing=True)
+    tb1 = torch.cuda.Event(enable_timing=True)
+    tb0.record(stream)
+    for k in range(K):
+        head.step(W_head, grads[(Wm + K + k) % n_grads])
+        idx, Gr = batches[Wm + k]
+        emb.step_sparse_rows(W_emb, Gr, idx)
+    tb1.record(stream)
+    torch.cuda.synchronize()
+    ember.ember_profile_enable(False)
+    kstats = ember.ember_profile_collect()
+    ms_step_with_kernel_events = tb0.elapsed_time(tb1) / K
+
+    # the dense apply pass: one launch per dense step and one per sparse step
+    # carry the same name; split them by launch order is not possible from the
+    # totals, so region C times the dense apply alone.
+    ember.ember_profile_enable(True)
+    for k in range(K):
+        head.step(W_head, grads[k % n_grads])
+    torch.cuda.synchronize()
+    ember.ember_profile_enable(False)
+    dstats = ember.ember_profile_collect()
+    apply_launches, apply_ms = dstats["ember_apply"]
+    apply_avg_ms = apply_ms / apply_launches
+    apply_bytes = V * D * (2 + 2 * 2) + 4 * (V + D)
+    apply_gbps = apply_bytes / (apply_avg_ms * 1e-3) / 1e9
+
+    # --- plain device copy over a W-sized buffer: practical ceiling ----------
+    src = torch.empty(V * D, dtype=torch.bfloat16, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        dst.copy_(src)
+    c0 = torch.cuda.Event(enable_timing=True)
+    c1 = torch.cuda.Event(enable_timing=True)
+    c0.record(stream)
+    for _ in range(10):
+        dst.copy_(src)
+    c1.record(stream)
+    torch.cuda.synchronize()
+    copy_gbps = 2 * src.numel() * 2 / (c0.elapsed_time(c1) / 10 * 1e-3) / 1e9
+    del src, dst
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": Wm,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": "Ember step of both untied token tables, V=128256 x D=4096: "
+                        "LM head dense (Zipf(1.1) row-scaled gradient) + input embedding "
+                        "sparse rows (8x2048 Zipf(1.1) ids per step)",
+            "V": V, "D": D, "storage": "bf16 W and G, fp32 r and c",
+            "sparse_rows_per_step": round(sum(n_rows) / K, 1),
+            "algorithmic_bytes_per_step": int(step_bytes),
+        },
+        "pct_of_peak": round(100.0 * value / PEAK_GBPS, 2),
+        "parts": {
+            "dense_lmhead": {"ms": round(dense_ms, 4), "bytes": dense_bytes,
+                             "GBps": round(dense_bytes / (dense_ms * 1e-3) / 1e9, 1),
+                             "pct_of_peak": round(100.0 * dense_bytes / (dense_ms * 1e-3) / 1e9 / PEAK_GBPS, 2)},
+            "sparse_embedding": {"ms": round(sparse_ms, 4), "bytes": int(sum(sparse_bytes) / K),
+                                 "GBps": round(sum(sparse_bytes) / K / (sparse_ms * 1e-3) / 1e9, 1)},
+        },
+        "kernels_ms_avg": {k: round(v[1] / v[0], 5) for k, v in kstats.items()},
+        "ms_per_step_with_kernel_events": round(ms_step_with_kernel_events, 4),
+        "roofline": {
+            "kernel": "ember_apply (dense LM-head step)",
+            "bound": "hbm",
+            "achieved": round(apply_gbps, 1),
+            "peak": PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(apply_gbps / PEAK_GBPS, 4),
+            "traffic": traffic_for_current_kernel(),
+            "avg_launch_ms": round(apply_avg_ms, 5),
+            "algorithmic_bytes_per_launch": apply_bytes,
+        },
+        "copy_ceiling_GBps": round(copy_gbps, 1),
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(args.cpu_rows)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,163 @@
+/*
+ * ember.h: C ABI of the Ember token-table optimizer step for AMD MI355X (gfx950).
+ *
+ * Ember (Token Geometry, Algorithm 1 in Section 2) updates a V x D
+ * token-interface matrix W (embedding table or LM head) from its gradient G
+ * with O(V + D) state: a row second-moment vector r (V floats) and a column
+ * second-moment vector c (D floats).  One step t >= 1 computes
+ *
+ *   r <- beta2 r + (1 - beta2) mean_j G_ij^2          (row statistic)
+ *   c <- beta2 c + (1 - beta2) mean_i G_ij^2          (column statistic)
+ *   rhat = r / (1 - beta2^t),  chat = c / (1 - beta2^t)
+ *   s = sqrt(mean(rhat) mean(chat))
+ *   W_ij <- W_ij -/+ lr G_ij / (sqrt(rhat_i chat_j / s) + eps)
+ *
+ * The V x D preconditioner rhat chat^T / s is never stored: the update is
+ * applied as a row scaling times a column scaling (section "Distributed
+ * Ember", paragraph on the preconditioner).  All reductions use a fixed
+ * order, with no floating-point atomics, so a given input produces the same
+ * bits on every run (same section, on the fused deterministic reduction).
+ *
+ * Conventions shared by every entry point:
+ *  - Memory: every pointer argument except the scalars is DEVICE memory owned
+ *    by the caller.  The library never allocates, frees or synchronises,
+ *    except ember_get_error (which synchronises the stream it is given).
+ *  - Layout: W and G are row-major, row i starting at element i * ld.  Both
+ *    base pointers must be 16-byte aligned and ld * element_size must be a
+ *    multiple of 16 bytes, so every row starts on a 16-byte boundary.  Only
+ *    the first D elements of each row are read or written.  W must not
+ *    overlap G, r, c or the workspace.
+ *  - dtypes: W and G are EMBER_F32 or EMBER_BF16, independently.  r and c are
+ *    always fp32 (the paper keeps optimizer state in fp32).  Arithmetic is
+ *    fp32; W is written with round-to-nearest-even; an element whose
+ *    gradient is exactly zero keeps its bits.
+ *  - Streams: all work is enqueued on `stream` (0 = the null stream) in
+ *    order; calls return before the work runs.  One (r, c, workspace) set
+ *    must not be used by two streams at once.
+ *  - Errors: every argument check below happens on the host before anything
+ *    is enqueued; on a negative return nothing was enqueued and no memory was
+ *    touched.  EMBER_ERR_HIP means a launch failed after validation.
+ *  - Step counter: t is owned by the caller: it starts at 0 and the caller
+ *    passes t = 1, 2, ... (Algorithm 1 increments t before each update).
+ *  - Sign: maximize = 0 descends a loss (W -= ...); maximize = 1 is the
+ *    paper's literal ascent of a reward (W += ...).
+ */
+#ifndef EMBER_H
+#define EMBER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { EMBER_F32 = 0, EMBER_BF16 = 1 } ember_dtype;
+
+typedef enum {
+    EMBER_OK = 0,
+    EMBER_ERR_ARG = -1,       /* null pointer, or a scalar out of range */
+    EMBER_ERR_SHAPE = -2,     /* V or D < 1 or too large, ld < D, n_idx > V */
+    EMBER_ERR_ALIGN = -3,     /* W/G not 16-byte aligned, ld*size not a multiple of 16,
+                                 r/c not 4-byte aligned, workspace not 256-byte aligned */
+    EMBER_ERR_DTYPE = -4,     /* dtype is not EMBER_F32 or EMBER_BF16 */
+    EMBER_ERR_WORKSPACE = -5, /* ws_bytes smaller than ember_workspace_bytes(V, D) */
+    EMBER_ERR_INDEX = -6,     /* sparse step: idx holds a value outside [0, V) or a
+                                 repeated value (reported by ember_get_error) */
+    EMBER_ERR_HIP = -7        /* a HIP runtime call failed */
+} ember_status;
+
+/* Largest supported V (row indices are kept in 31 bits) and D. */
+#define EMBER_MAX_V ((int64_t)0x7FFFFFFE)
+#define EMBER_MAX_D ((int64_t)(1 << 24))
+
+/*
+ * Workspace size for a V x D table, valid for both the dense and the sparse
+ * step.  The workspace holds the per-block partial sums of the fixed-order
+ * reductions, a V-entry row-slot table used by the sparse step, and a status
+ * word.  It is caller-allocated device memory, 256-byte aligned, and must be
+ * initialised once by ember_init_state before its first step.
+ * Returns EMBER_OK and sets *bytes, or EMBER_ERR_SHAPE / EMBER_ERR_ARG.
+ */
+int ember_workspace_bytes(int64_t V, int64_t D, size_t* bytes);
+
+/*
+ * Ember state initialisation (Algorithm 1: r_0 = 0 in R^V, c_0 = 0 in R^D,
+ * t = 0).  Enqueues zero fills of r (V floats), c (D floats) and the parts
+ * of the workspace that must start at zero.  The caller sets t = 0.
+ */
+int ember_init_state(float* r, float* c, int64_t V, int64_t D,
+                     void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * One dense Ember step (Algorithm 1, one pass of its loop body) on W (V x D,
+ * row stride ldw, dtype w_dtype) with gradient G (V x D, row stride ldg,
+ * dtype g_dtype).  r (V) and c (D) are updated in place, then W.
+ * Scalars: t >= 1; lr >= 0 and finite; 0 <= beta2 < 1; eps >= 0 and finite
+ * (the paper's defaults: lr = 1e-3, beta2 = 0.999, eps = 1e-8).  beta2 is
+ * used as the fp32 value passed.
+ */
+int ember_step_dense(void* W, int w_dtype, int64_t ldw,
+                     const void* G, int g_dtype, int64_t ldg,
+                     float* r, float* c, int64_t V, int64_t D, int64_t t,
+                     float lr, float beta2, float eps, int maximize,
+                     void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * One sparse-row Ember step: the gradient is zero except on the n_idx rows
+ * listed in idx (the embedding-table case of Section 2.2, where only the
+ * tokens of the batch receive gradient).  G_rows is n_idx x D (row stride
+ * ldg, compact: row k is the gradient of W's row idx[k]).  idx is a device
+ * array of n_idx int64 values, unique and in [0, V), in any order;
+ * n_idx = 0 is allowed (then G_rows and idx may be NULL).
+ *
+ * The result is the dense step on the gradient that is zero outside idx:
+ * every row's r decays by beta2 (touched rows also add their statistic), the
+ * column mean still divides by V, s uses all V rows, and W rows outside idx
+ * are not touched.
+ *
+ * Index errors (a value outside [0, V), or a repeated value) are detected on
+ * the device: the step then leaves W, r and c unchanged, and the next
+ * ember_get_error on this workspace reports EMBER_ERR_INDEX.  The caller
+ * should then not advance t.
+ */
+int ember_step_sparse_rows(void* W, int w_dtype, int64_t ldw,
+                           const void* G_rows, int g_dtype, int64_t ldg,
+                           const int64_t* idx, int64_t n_idx,
+                           float* r, float* c, int64_t V, int64_t D, int64_t t,
+                           float lr, float beta2, float eps, int maximize,
+                           void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Device status of the most recent step enqueued with this workspace.
+ * Synchronises `stream`, then sets *device_status to EMBER_OK or
+ * EMBER_ERR_INDEX.  Returns EMBER_OK, EMBER_ERR_ARG or EMBER_ERR_HIP.
+ */
+int ember_get_error(const void* ws, hipStream_t stream, int* device_status);
+
+/* Static description of a status code (never NULL). */
+const char* ember_strerror(int status);
+
+/*
+ * Kernel timing (diagnostics).  While enabled, each kernel the library
+ * launches is bracketed by two HIP events recorded on its stream.
+ * ember_profile_collect waits for those events, writes per-kernel totals
+ * (name, launch count, summed duration in milliseconds) for up to
+ * max_entries kernels, sets *n_entries, and clears the record.
+ */
+typedef struct {
+    const char* name;
+    int64_t launches;
+    double total_ms;
+} ember_kernel_stat;
+
+int ember_profile_enable(int enable);
+int ember_profile_collect(ember_kernel_stat* out, int max_entries, int* n_entries);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EMBER_H */

@@ -45,7 +45,7 @@ def _load():
     lib = ctypes.CDLL(_LIB)
     vp, i64, f32, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_float, ctypes.c_int
     lib.ember_oracle_step.argtypes = [vp, i32, i64, vp, i32, i64, vp, i64,
-                                      vp, vp, i64, i64, i64, f32, f32, f32, i32]
+                                      vp, vp, i64, i64, i64, f32, f32, f32, i32, vp, i64]
     lib.ember_oracle_step.restype = i32
     lib.ember_oracle_bf16_to_f64.argtypes = [ctypes.c_uint16]
     lib.ember_oracle_bf16_to_f64.restype = ctypes.c_double
@@ -73,11 +73,14 @@ def _ld(a: np.ndarray) -> int:
 
 def step(W: np.ndarray, G: np.ndarray, r: np.ndarray, c: np.ndarray, t: int,
          lr: float = 1e-3, beta2: float = 0.999, eps: float = 1e-8,
-         maximize: bool = False, idx: np.ndarray | None = None) -> int:
+         maximize: bool = False, idx: np.ndarray | None = None,
+         w_rows: np.ndarray | None = None) -> int:
     """One Ember step, in place on W, r and c.  Returns the oracle's status.
 
     ``idx`` (int64) selects the sparse-row form: G then holds ``len(idx)``
-    rows, row k being the gradient of W's row ``idx[k]``.
+    rows, row k being the gradient of W's row ``idx[k]``.  ``w_rows``
+    (strictly increasing int64) restricts which rows of W are written; the
+    state is always updated in full.
     """
     lib = _load()
     V, D = W.shape
@@ -94,12 +97,18 @@ def step(W: np.ndarray, G: np.ndarray, r: np.ndarray, c: np.ndarray, t: int,
         if G.shape != (idx.shape[0], D):
             raise ValueError("sparse G must be [len(idx), D]")
         idx_ptr, n_idx = idx.ctypes.data, idx.shape[0]
+    if w_rows is None:
+        wr_ptr, n_wr = None, 0
+    else:
+        w_rows = np.ascontiguousarray(w_rows, dtype=np.int64)
+        wr_ptr, n_wr = w_rows.ctypes.data, w_rows.shape[0]
     g_ptr = G.ctypes.data if G.size else None
     g_ld = _ld(G) if G.shape[0] > 0 else D
     return lib.ember_oracle_step(W.ctypes.data, _dtype_code(W), _ld(W),
                                  g_ptr, _dtype_code(G), g_ld, idx_ptr, n_idx,
                                  r.ctypes.data, c.ctypes.data, V, D, int(t),
-                                 float(lr), float(beta2), float(eps), int(bool(maximize)))
+                                 float(lr), float(beta2), float(eps), int(bool(maximize)),
+                                 wr_ptr, n_wr)
 
 
 def bf16_to_f64(bits: int) -> float:

@@ -116,14 +116,18 @@ static void store_elem(void* base, int dtype, int64_t off, double v)
  *   idx != NULL : G holds n_idx rows (stride ldg); row k is the gradient of
  *                 W's row idx[k]; all other rows of the gradient are zero.
  * r (V floats) and c (D floats) are read and updated in place; t >= 1 is the
- * step being taken.  W is updated in place.  Returns 0, or a negative code
- * with nothing modified.
+ * step being taken.  W is updated in place.
+ * w_rows (optional, n_w_rows entries, strictly increasing): when given, only
+ * these rows of W are written (a sample for checks at large sizes); the state
+ * update is always complete.
+ * Returns 0, or a negative code with nothing modified.
  */
 int ember_oracle_step(void* W, int w_dtype, int64_t ldw,
                       const void* G, int g_dtype, int64_t ldg,
                       const int64_t* idx, int64_t n_idx,
                       float* r, float* c, int64_t V, int64_t D, int64_t t,
-                      float lr, float beta2, float eps, int maximize)
+                      float lr, float beta2, float eps, int maximize,
+                      const int64_t* w_rows, int64_t n_w_rows)
 {
     if (V < 1 || D < 1 || ldw < D || ldg < D || t < 1)
         return ORACLE_BAD_ARG;
@@ -136,6 +140,11 @@ int ember_oracle_step(void* W, int w_dtype, int64_t ldw,
         return ORACLE_BAD_ARG;
     if (idx != NULL && n_idx < 0)
         return ORACLE_BAD_ARG;
+    if (w_rows != NULL) {
+        for (int64_t k = 0; k < n_w_rows; ++k)
+            if (w_rows[k] < 0 || w_rows[k] >= V || (k > 0 && w_rows[k] <= w_rows[k - 1]))
+                return ORACLE_BAD_ARG;
+    }
 
     /* grow[i]: row of G holding gradient row i, or -1 for a zero row. */
     int64_t* grow = (int64_t*)malloc((size_t)V * sizeof(int64_t));
@@ -207,7 +216,9 @@ int ember_oracle_step(void* W, int w_dtype, int64_t ldw,
     /* Update with the factored preconditioner vtil_ij = rhat_i chat_j / s. */
     const double alpha = (double)lr;
     const double e = (double)eps;
-    for (int64_t i = 0; i < V; ++i) {
+    const int64_t n_out = (w_rows != NULL) ? n_w_rows : V;
+    for (int64_t k = 0; k < n_out; ++k) {
+        const int64_t i = (w_rows != NULL) ? w_rows[k] : k;
         if (grow[i] < 0)
             continue; /* zero gradient row: every update is exactly zero */
         const double rhat = (double)r[i] / bias;

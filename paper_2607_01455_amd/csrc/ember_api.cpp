@@ -1,0 +1,257 @@
+// Host side of the Ember C ABI (include/ember.h): argument validation, scalar
+// preparation in float64, workspace layout and the launch sequence of one step.
+// Every check runs before anything is enqueued.
+
+#include "ember.h"
+
+#include <cmath>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "ember_launch.h"
+
+namespace {
+
+using ember::StepArgs;
+using ember::WsLayout;
+
+bool dtype_ok(int d) { return d == EMBER_F32 || d == EMBER_BF16; }
+size_t dtype_size(int d) { return d == EMBER_F32 ? 4 : 2; }
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+int check_shape(int64_t V, int64_t D) {
+    if (V < 1 || D < 1 || V > EMBER_MAX_V || D > EMBER_MAX_D) return EMBER_ERR_SHAPE;
+    return EMBER_OK;
+}
+
+int check_matrix(const void* p, int dtype, int64_t ld, int64_t D, bool may_be_null) {
+    if (!dtype_ok(dtype)) return EMBER_ERR_DTYPE;
+    if (ld < D) return EMBER_ERR_SHAPE;
+    if (p == nullptr) return may_be_null ? EMBER_OK : EMBER_ERR_ARG;
+    if (!aligned(p, 16) || ((ld * (int64_t)dtype_size(dtype)) % 16) != 0) return EMBER_ERR_ALIGN;
+    return EMBER_OK;
+}
+
+int check_scalars(int64_t t, float lr, float beta2, float eps) {
+    if (t < 1) return EMBER_ERR_ARG;
+    if (!(beta2 >= 0.0f && beta2 < 1.0f)) return EMBER_ERR_ARG;
+    if (!(lr >= 0.0f) || !std::isfinite(lr)) return EMBER_ERR_ARG;
+    if (!(eps >= 0.0f) || !std::isfinite(eps)) return EMBER_ERR_ARG;
+    return EMBER_OK;
+}
+
+int check_state(const float* r, const float* c, const void* ws, size_t ws_bytes, int64_t V, int64_t D) {
+    if (r == nullptr || c == nullptr || ws == nullptr) return EMBER_ERR_ARG;
+    if (!aligned(r, 4) || !aligned(c, 4) || !aligned(ws, 256)) return EMBER_ERR_ALIGN;
+    if (ws_bytes < ember::ws_layout(V, D).total) return EMBER_ERR_WORKSPACE;
+    return EMBER_OK;
+}
+
+// ---------------------------------------------------------------------------
+// optional kernel timing
+// ---------------------------------------------------------------------------
+
+struct Record {
+    const char* name;
+    hipEvent_t start;
+    hipEvent_t stop;
+};
+
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+std::vector<Record> g_records;
+std::vector<hipEvent_t> g_free_events;
+
+hipEvent_t take_event() {
+    if (!g_free_events.empty()) {
+        hipEvent_t e = g_free_events.back();
+        g_free_events.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+template <typename F>
+hipError_t timed(const char* name, hipStream_t s, F&& launch) {
+    if (!g_prof_on) return launch();
+    std::lock_guard<std::mutex> lock(g_prof_mu);
+    Record rec{name, take_event(), take_event()};
+    if (rec.start) (void)hipEventRecord(rec.start, s);
+    hipError_t err = launch();
+    if (rec.stop) (void)hipEventRecord(rec.stop, s);
+    if (rec.start && rec.stop) g_records.push_back(rec);
+    return err;
+}
+
+// ---------------------------------------------------------------------------
+// one step
+// ---------------------------------------------------------------------------
+
+int run_step(StepArgs& a, float lr, float beta2, float eps, int64_t t, int maximize, hipStream_t s) {
+    const double b2 = (double)beta2;
+    a.beta2 = beta2;
+    a.one_minus_beta2 = (float)(1.0 - b2);
+    a.inv_bias = 1.0 / (1.0 - std::pow(b2, (double)t));
+    const double alpha_s = maximize ? (double)lr : -(double)lr;
+    a.inv_alpha = lr > 0.0f ? 1.0 / alpha_s : 0.0;
+    a.eps_over_alpha = lr > 0.0f ? (float)((double)eps / alpha_s) : 0.0f;
+
+    hipError_t e = timed("ember_stats", s, [&] { return ember::launch_stats(a, s); });
+    if (e == hipSuccess) e = timed("ember_finalize_rows", s, [&] { return ember::launch_finalize_rows(a, s); });
+    if (e == hipSuccess) e = timed("ember_finalize_cols", s, [&] { return ember::launch_finalize_cols(a, s); });
+    // lr == 0 leaves every weight bit unchanged, so the dense step skips the
+    // apply pass; the sparse apply pass also clears the index-error flag for the
+    // next step, so it always runs (and returns before the row loop when lr == 0).
+    if (e == hipSuccess && (lr > 0.0f || a.sparse))
+        e = timed("ember_apply", s, [&] { return ember::launch_apply(a, s); });
+    return e == hipSuccess ? EMBER_OK : EMBER_ERR_HIP;
+}
+
+} // namespace
+
+extern "C" {
+
+int ember_workspace_bytes(int64_t V, int64_t D, size_t* bytes) {
+    if (bytes == nullptr) return EMBER_ERR_ARG;
+    int st = check_shape(V, D);
+    if (st != EMBER_OK) return st;
+    *bytes = ember::ws_layout(V, D).total;
+    return EMBER_OK;
+}
+
+int ember_init_state(float* r, float* c, int64_t V, int64_t D, void* ws, size_t ws_bytes, hipStream_t stream) {
+    int st = check_shape(V, D);
+    if (st != EMBER_OK) return st;
+    st = check_state(r, c, ws, ws_bytes, V, D);
+    if (st != EMBER_OK) return st;
+    const WsLayout L = ember::ws_layout(V, D);
+    hipError_t e = ember::launch_zero(r, (size_t)V * 4, stream);
+    if (e == hipSuccess) e = ember::launch_zero(c, (size_t)D * 4, stream);
+    if (e == hipSuccess) e = ember::launch_zero(ws, L.zero_end, stream);
+    return e == hipSuccess ? EMBER_OK : EMBER_ERR_HIP;
+}
+
+int ember_step_dense(void* W, int w_dtype, int64_t ldw, const void* G, int g_dtype, int64_t ldg,
+                     float* r, float* c, int64_t V, int64_t D, int64_t t,
+                     float lr, float beta2, float eps, int maximize,
+                     void* ws, size_t ws_bytes, hipStream_t stream) {
+    int st = check_shape(V, D);
+    if (st == EMBER_OK) st = check_matrix(W, w_dtype, ldw, D, false);
+    if (st == EMBER_OK) st = check_matrix(G, g_dtype, ldg, D, false);
+    if (st == EMBER_OK) st = check_state(r, c, ws, ws_bytes, V, D);
+    if (st == EMBER_OK) st = check_scalars(t, lr, beta2, eps);
+    if (st != EMBER_OK) return st;
+    StepArgs a{};
+    a.sparse = false;
+    a.W = W;
+    a.w_dtype = w_dtype;
+    a.ldw = ldw;
+    a.G = G;
+    a.g_dtype = g_dtype;
+    a.ldg = ldg;
+    a.idx = nullptr;
+    a.rows = V;
+    a.r = r;
+    a.c = c;
+    a.V = V;
+    a.D = D;
+    a.ws = static_cast<char*>(ws);
+    return run_step(a, lr, beta2, eps, t, maximize, stream);
+}
+
+int ember_step_sparse_rows(void* W, int w_dtype, int64_t ldw, const void* G_rows, int g_dtype, int64_t ldg,
+                           const int64_t* idx, int64_t n_idx,
+                           float* r, float* c, int64_t V, int64_t D, int64_t t,
+                           float lr, float beta2, float eps, int maximize,
+                           void* ws, size_t ws_bytes, hipStream_t stream) {
+    int st = check_shape(V, D);
+    if (st == EMBER_OK && (n_idx < 0 || n_idx > V)) st = EMBER_ERR_SHAPE;
+    if (st == EMBER_OK) st = check_matrix(W, w_dtype, ldw, D, false);
+    if (st == EMBER_OK) st = check_matrix(G_rows, g_dtype, ldg, D, n_idx == 0);
+    if (st == EMBER_OK && n_idx > 0 && idx == nullptr) st = EMBER_ERR_ARG;
+    if (st == EMBER_OK && idx != nullptr && !aligned(idx, 8)) st = EMBER_ERR_ALIGN;
+    if (st == EMBER_OK) st = check_state(r, c, ws, ws_bytes, V, D);
+    if (st == EMBER_OK) st = check_scalars(t, lr, beta2, eps);
+    if (st != EMBER_OK) return st;
+    StepArgs a{};
+    a.sparse = true;
+    a.W = W;
+    a.w_dtype = w_dtype;
+    a.ldw = ldw;
+    a.G = G_rows;
+    a.g_dtype = g_dtype;
+    a.ldg = ldg;
+    a.idx = idx;
+    a.rows = n_idx;
+    a.r = r;
+    a.c = c;
+    a.V = V;
+    a.D = D;
+    a.ws = static_cast<char*>(ws);
+    return run_step(a, lr, beta2, eps, t, maximize, stream);
+}
+
+int ember_get_error(const void* ws, hipStream_t stream, int* device_status) {
+    if (ws == nullptr || device_status == nullptr) return EMBER_ERR_ARG;
+    if (!aligned(ws, 256)) return EMBER_ERR_ALIGN;
+    if (hipStreamSynchronize(stream) != hipSuccess) return EMBER_ERR_HIP;
+    int flag = 0;
+    const char* base = static_cast<const char*>(ws);
+    if (hipMemcpy(&flag, base + ember::ws_layout(1, 1).status, sizeof flag, hipMemcpyDeviceToHost) != hipSuccess)
+        return EMBER_ERR_HIP;
+    *device_status = flag != 0 ? EMBER_ERR_INDEX : EMBER_OK;
+    return EMBER_OK;
+}
+
+const char* ember_strerror(int status) {
+    switch (status) {
+    case EMBER_OK: return "success";
+    case EMBER_ERR_ARG: return "invalid argument (null pointer or scalar out of range)";
+    case EMBER_ERR_SHAPE: return "invalid shape (V, D, leading dimension or index count)";
+    case EMBER_ERR_ALIGN: return "misaligned pointer or leading dimension";
+    case EMBER_ERR_DTYPE: return "unsupported dtype (expected EMBER_F32 or EMBER_BF16)";
+    case EMBER_ERR_WORKSPACE: return "workspace too small";
+    case EMBER_ERR_INDEX: return "row index out of range or repeated";
+    case EMBER_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+    }
+}
+
+int ember_profile_enable(int enable) {
+    std::lock_guard<std::mutex> lock(g_prof_mu);
+    g_prof_on = enable != 0;
+    return EMBER_OK;
+}
+
+int ember_profile_collect(ember_kernel_stat* out, int max_entries, int* n_entries) {
+    if (n_entries == nullptr || (out == nullptr && max_entries > 0)) return EMBER_ERR_ARG;
+    std::lock_guard<std::mutex> lock(g_prof_mu);
+    std::vector<ember_kernel_stat> stats;
+    int rc = EMBER_OK;
+    for (const Record& rec : g_records) {
+        float ms = 0.0f;
+        if (hipEventSynchronize(rec.stop) != hipSuccess || hipEventElapsedTime(&ms, rec.start, rec.stop) != hipSuccess)
+            rc = EMBER_ERR_HIP;
+        size_t k = 0;
+        while (k < stats.size() && std::string(stats[k].name) != rec.name) ++k;
+        if (k == stats.size()) stats.push_back(ember_kernel_stat{rec.name, 0, 0.0});
+        stats[k].launches += 1;
+        stats[k].total_ms += ms;
+        g_free_events.push_back(rec.start);
+        g_free_events.push_back(rec.stop);
+    }
+    g_records.clear();
+    int n = 0;
+    for (const ember_kernel_stat& st : stats) {
+        if (n < max_entries) out[n] = st;
+        ++n;
+    }
+    *n_entries = n < max_entries ? n : max_entries;
+    return rc;
+}
+
+} // extern "C"

@@ -1,0 +1,148 @@
+"""C-ABI tests that need no GPU: the library loads, exports every function the
+header declares, and rejects bad arguments on the host with the documented
+status codes before touching the device."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ember.h")
+
+
+@pytest.fixture(scope="module")
+def em():
+    lib_path = os.path.join(ROOT, "paper_2607_01455_amd", "libember.so")
+    if not os.path.exists(lib_path):
+        from paper_2607_01455_amd import build
+        build.build()
+    from paper_2607_01455_amd import ember
+    return ember
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(ember_\w+)\s*\(", text, re.M)))
+
+
+def test_header_declares_the_entry_points():
+    names = _declared_functions()
+    for required in ("ember_workspace_bytes", "ember_init_state", "ember_step_dense",
+                     "ember_step_sparse_rows", "ember_get_error", "ember_strerror"):
+        assert required in names
+
+
+def test_library_exports_every_declared_function(em):
+    names = _declared_functions()
+    assert sorted(em.EXPORTED) == names
+    for name in names:
+        assert hasattr(em.LIB, name), name
+
+
+def test_strerror_covers_every_status(em):
+    for st in range(0, -8, -1):
+        assert em.ember_strerror(st) and em.ember_strerror(st) != "unknown status"
+    assert em.ember_strerror(12345) == "unknown status"
+
+
+def test_workspace_bytes(em):
+    out = ctypes.c_size_t(0)
+    assert em.LIB.ember_workspace_bytes(0, 4, ctypes.byref(out)) == em.EMBER_ERR_SHAPE
+    assert em.LIB.ember_workspace_bytes(4, 0, ctypes.byref(out)) == em.EMBER_ERR_SHAPE
+    assert em.LIB.ember_workspace_bytes(4, 4, None) == em.EMBER_ERR_ARG
+    assert em.LIB.ember_workspace_bytes(2 ** 31, 4, ctypes.byref(out)) == em.EMBER_ERR_SHAPE
+    sizes = {}
+    for V, D in [(1, 1), (1024, 64), (128256, 4096), (262144, 8192)]:
+        assert em.LIB.ember_workspace_bytes(V, D, ctypes.byref(out)) == em.EMBER_OK
+        assert out.value % 256 == 0
+        # at least: slot table, per-slab row sums, per-block column partials
+        assert out.value >= 4 * V + 4 * V * math.ceil(D / 4096) + 4 * D
+        sizes[(V, D)] = out.value
+    # fixed-size partial buffers: a few tens of MB at the largest shape
+    assert sizes[(262144, 8192)] < 64 * 2 ** 20
+
+
+# Fake, suitably aligned addresses: every call below must fail validation on
+# the host, so none of them is ever dereferenced or passed to the device.
+A = 1 << 20
+W_, G_, R_, C_, WS_, IDX_ = A, 2 * A, 3 * A, 4 * A, 5 * A, 6 * A
+
+
+def _ws_bytes(em, V, D):
+    out = ctypes.c_size_t(0)
+    em.LIB.ember_workspace_bytes(V, D, ctypes.byref(out))
+    return out.value
+
+
+def _dense(em, **kw):
+    a = dict(W=W_, wd=1, ldw=64, G=G_, gd=1, ldg=64, r=R_, c=C_, V=10, D=64, t=1,
+             lr=1e-3, b2=0.999, eps=1e-8, mx=0, ws=WS_, wsb=None)
+    a.update(kw)
+    if a["wsb"] is None:
+        a["wsb"] = _ws_bytes(em, max(a["V"], 1), max(a["D"], 1))
+    return em.LIB.ember_step_dense(a["W"], a["wd"], a["ldw"], a["G"], a["gd"], a["ldg"], a["r"], a["c"],
+                                   a["V"], a["D"], a["t"], a["lr"], a["b2"], a["eps"], a["mx"],
+                                   a["ws"], a["wsb"], None)
+
+
+def _sparse(em, **kw):
+    a = dict(W=W_, wd=1, ldw=64, G=G_, gd=1, ldg=64, idx=IDX_, n=3, r=R_, c=C_, V=10, D=64, t=1,
+             lr=1e-3, b2=0.999, eps=1e-8, mx=0, ws=WS_, wsb=None)
+    a.update(kw)
+    if a["wsb"] is None:
+        a["wsb"] = _ws_bytes(em, max(a["V"], 1), max(a["D"], 1))
+    return em.LIB.ember_step_sparse_rows(a["W"], a["wd"], a["ldw"], a["G"], a["gd"], a["ldg"], a["idx"],
+                                         a["n"], a["r"], a["c"], a["V"], a["D"], a["t"], a["lr"], a["b2"],
+                                         a["eps"], a["mx"], a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(V=0), "SHAPE"), (dict(D=0), "SHAPE"), (dict(ldw=63), "SHAPE"), (dict(ldg=32), "SHAPE"),
+    (dict(V=2 ** 31), "SHAPE"),
+    (dict(W=None), "ARG"), (dict(G=None), "ARG"), (dict(r=None), "ARG"), (dict(c=None), "ARG"),
+    (dict(ws=None), "ARG"),
+    (dict(W=W_ + 8), "ALIGN"), (dict(G=G_ + 2), "ALIGN"), (dict(ldw=68, D=60), "ALIGN"),
+    (dict(wd=0, ldw=66, D=66), "ALIGN"), (dict(r=R_ + 2), "ALIGN"), (dict(ws=WS_ + 128), "ALIGN"),
+    (dict(wd=2), "DTYPE"), (dict(gd=-1), "DTYPE"),
+    (dict(wsb=1024), "WORKSPACE"),
+    (dict(t=0), "ARG"), (dict(t=-5), "ARG"), (dict(b2=1.0), "ARG"), (dict(b2=-0.5), "ARG"),
+    (dict(b2=float("nan")), "ARG"), (dict(lr=-1e-3), "ARG"), (dict(lr=float("inf")), "ARG"),
+    (dict(eps=-1.0), "ARG"), (dict(eps=float("nan")), "ARG"),
+])
+def test_dense_step_rejects_bad_arguments_on_host(em, kw, status):
+    assert _dense(em, **kw) == getattr(em, "EMBER_ERR_" + status)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n=-1), "SHAPE"), (dict(n=11), "SHAPE"), (dict(idx=None), "ARG"), (dict(idx=IDX_ + 4), "ALIGN"),
+    (dict(G=None), "ARG"), (dict(W=None), "ARG"), (dict(gd=3), "DTYPE"), (dict(t=0), "ARG"),
+    (dict(wsb=0), "WORKSPACE"), (dict(V=0), "SHAPE"),
+])
+def test_sparse_step_rejects_bad_arguments_on_host(em, kw, status):
+    assert _sparse(em, **kw) == getattr(em, "EMBER_ERR_" + status)
+
+
+def test_init_state_and_get_error_reject_bad_arguments(em):
+    wsb = _ws_bytes(em, 10, 64)
+    assert em.LIB.ember_init_state(R_, C_, 0, 64, WS_, wsb, None) == em.EMBER_ERR_SHAPE
+    assert em.LIB.ember_init_state(None, C_, 10, 64, WS_, wsb, None) == em.EMBER_ERR_ARG
+    assert em.LIB.ember_init_state(R_, C_, 10, 64, WS_, 8, None) == em.EMBER_ERR_WORKSPACE
+    assert em.LIB.ember_init_state(R_, C_, 10, 64, WS_ + 4, wsb, None) == em.EMBER_ERR_ALIGN
+    st = ctypes.c_int(0)
+    assert em.LIB.ember_get_error(None, None, ctypes.byref(st)) == em.EMBER_ERR_ARG
+    assert em.LIB.ember_get_error(WS_, None, None) == em.EMBER_ERR_ARG
+    assert em.LIB.ember_get_error(WS_ + 16, None, ctypes.byref(st)) == em.EMBER_ERR_ALIGN
+
+
+def test_binding_marshals_dtypes_and_strides(em):
+    import torch
+    assert em._dtype(torch.zeros(1, dtype=torch.float32)) == em.EMBER_F32
+    assert em._dtype(torch.zeros(1, dtype=torch.bfloat16)) == em.EMBER_BF16
+    assert em._dtype(torch.zeros(1, dtype=torch.float16)) not in (em.EMBER_F32, em.EMBER_BF16)
+    x = torch.zeros(5, 72)[:, :64]
+    assert em._ld(x) == 72
+    with pytest.raises(TypeError):
+        em._ld(torch.zeros(5, 8).t())

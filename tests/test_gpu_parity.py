@@ -1,0 +1,386 @@
+"""GPU parity: the HIP library (through its C ABI) against the CPU oracle.
+
+Lockstep protocol: before every step the oracle receives a bit copy of the
+GPU's current W, the same gradient bits, and its own r, c chain (the state
+does not depend on W, so the chains cannot drift).  Tolerances:
+  r, c       |gpu - oracle| <= 1e-5 |oracle| per element (fp32 sums of up to
+             ~2^18 positive terms in a fixed tree order stay far inside this);
+             bit-exact where the method multiplies by beta2 alone
+             (rows without gradient, an all-zero gradient).
+  fp32 W     |gpu - oracle| <= 1e-5 max(|oracle|, |W before the step|).
+  bf16 W     at most 1 unit in the last place (the GPU rounds an fp32 result to
+             bf16, the oracle rounds its float64 result once).
+  sparse     rows outside idx: W bit-identical to before the step.
+Small shapes are checked on every element; the full-size workloads (the
+shapes and launch configuration the benchmark times) on every state element
+and on a sample of W rows that always includes the heaviest rows.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_01455_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+B2 = 0.999
+LR = 1e-3
+EPS = 1e-8
+
+
+@pytest.fixture(scope="module")
+def em():
+    from paper_2607_01455_amd import ember
+    return ember
+
+
+def host_bits(t: torch.Tensor) -> np.ndarray:
+    """Host copy of a device tensor: float32 values or bf16 bit patterns."""
+    t = t.detach()
+    if t.dtype == torch.bfloat16:
+        return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    return t.contiguous().cpu().numpy()
+
+
+def ordered16(b: np.ndarray) -> np.ndarray:
+    b = b.astype(np.int64)
+    return np.where(b & 0x8000, 0x8000 - (b & 0x7FFF), 0x8000 + b)
+
+
+def check_w(got: np.ndarray, want: np.ndarray, prev: np.ndarray, what: str) -> None:
+    if got.dtype == np.uint16:
+        d = np.abs(ordered16(got) - ordered16(want))
+        bad = d > 1
+        assert not bad.any(), f"{what}: {bad.sum()} bf16 elements differ by > 1 ulp (max {d.max()})"
+    else:
+        tol = 1e-5 * np.maximum(np.abs(want), np.abs(prev))
+        err = np.abs(got.astype(np.float64) - want.astype(np.float64))
+        bad = ~(err <= tol)
+        assert not bad.any(), f"{what}: {bad.sum()} fp32 elements out of tolerance (max err {err.max()})"
+
+
+def check_state(got: torch.Tensor, want: np.ndarray, what: str) -> None:
+    g = got.cpu().numpy().astype(np.float64)
+    w = want.astype(np.float64)
+    err = np.abs(g - w)
+    bad = ~(err <= 1e-5 * np.abs(w))
+    assert not bad.any(), f"{what}: {bad.sum()} of {w.size} out of 1e-5 (max rel {np.max(err / np.maximum(np.abs(w), 1e-300))})"
+
+
+def sample_rows(V: int, n: int = 1024, seed: int = 0) -> np.ndarray:
+    rng = np.random.default_rng(seed)
+    rows = set(rng.choice(V, size=min(n, V), replace=False).tolist())
+    rows |= set(range(min(32, V))) | {V - 1, V // 2}
+    return np.array(sorted(rows), dtype=np.int64)
+
+
+class Table:
+    def __init__(self, em, V, D):
+        self.em = em
+        self.r = torch.empty(V, dtype=torch.float32, device=DEV)
+        self.c = torch.empty(D, dtype=torch.float32, device=DEV)
+        self.ws = torch.empty(em.ember_workspace_bytes(V, D), dtype=torch.uint8, device=DEV)
+        em.ember_init_state(self.r, self.c, self.ws)
+        self.r_o = np.zeros(V, np.float32)
+        self.c_o = np.zeros(D, np.float32)
+
+
+def _ld(D, dtype, pad):
+    q = 8 if dtype == torch.bfloat16 else 4
+    return ((D + q - 1) // q + pad) * q
+
+
+def dense_lockstep(em, cfg, seed=0, steps=None, rows=None, ld_pad=0, maximize=False,
+                   lr=LR, beta2=B2, eps=EPS, all_rows_at=(1,)):
+    """Run `steps` dense steps in lockstep with the oracle; W checked on `rows`
+    (None: every row) and on every row at the steps in all_rows_at."""
+    steps = cfg.steps if steps is None else steps
+    print(f"dense lockstep {cfg.name} V={cfg.V} D={cfg.D} w={cfg.w_dtype} g={cfg.g_dtype} steps={steps}", flush=True)
+    ldw = _ld(cfg.D, cfg.w_dtype, ld_pad) if ld_pad else None
+    ldg = _ld(cfg.D, cfg.g_dtype, ld_pad) if ld_pad else None
+    W = wl.make_weights(cfg, seed=seed, device=DEV, ld=ldw)
+    scales = wl.row_scales(cfg, seed, DEV)
+    tab = Table(em, cfg.V, cfg.D)
+    rows_t = None if rows is None else torch.from_numpy(rows).to(DEV)
+    for t in range(1, steps + 1):
+        G = wl.make_dense_grad(cfg, t, seed=seed, device=DEV, scales=scales, ld=ldg)
+        full = rows is None or t in all_rows_at
+        if full:
+            W_prev = host_bits(W)
+        else:
+            prev_rows = host_bits(W[rows_t])
+        pad_before = host_bits(W.as_strided((cfg.V, ldw - cfg.D), (ldw, 1), cfg.D)) if ld_pad else None
+        em.ember_step_dense(W, G, tab.r, tab.c, t, lr, beta2, eps, maximize, tab.ws)
+        torch.cuda.synchronize()
+        G_h = host_bits(G)
+        if full:
+            W_ref = W_prev.copy()
+        else:
+            # only the sampled rows are read and written by the oracle; the rest
+            # of this array is never touched (and never paged in)
+            W_ref = np.empty((cfg.V, cfg.D), dtype=prev_rows.dtype)
+            W_ref[rows] = prev_rows
+        st = oracle.step(W_ref, G_h, tab.r_o, tab.c_o, t, lr=lr, beta2=beta2, eps=eps,
+                         maximize=maximize, w_rows=None if full else rows)
+        assert st == 0
+        check_state(tab.r, tab.r_o, f"{cfg.name} r step {t}")
+        check_state(tab.c, tab.c_o, f"{cfg.name} c step {t}")
+        if full:
+            check_w(host_bits(W), W_ref, W_prev, f"{cfg.name} W step {t}")
+        else:
+            check_w(host_bits(W[rows_t]), W_ref[rows], prev_rows, f"{cfg.name} W step {t} (sampled rows)")
+        if ld_pad:
+            pad_after = host_bits(W.as_strided((cfg.V, ldw - cfg.D), (ldw, 1), cfg.D))
+            assert np.array_equal(pad_before, pad_after), "row padding of W was written"
+        del G, G_h, W_ref
+    return W, tab
+
+
+def sparse_lockstep(em, cfg, seed=0, steps=None, shuffle=False, check_rows_all=True):
+    steps = cfg.steps if steps is None else steps
+    print(f"sparse lockstep {cfg.name} V={cfg.V} D={cfg.D} steps={steps} shuffle={shuffle}", flush=True)
+    W = wl.make_weights(cfg, seed=seed, device=DEV)
+    tab = Table(em, cfg.V, cfg.D)
+    for t in range(1, steps + 1):
+        idx, Gr = wl.make_sparse_batch(cfg, t, seed=seed, device=DEV, shuffle=shuffle)
+        W_prev = host_bits(W)
+        r_prev = tab.r.cpu().numpy()
+        em.ember_step_sparse_rows(W, Gr, idx, tab.r, tab.c, t, LR, B2, EPS, False, tab.ws)
+        assert em.ember_get_error(tab.ws) == em.EMBER_OK
+        idx_h = idx.cpu().numpy()
+        touched = np.sort(idx_h)
+        W_ref = W_prev.copy()
+        assert oracle.step(W_ref, host_bits(Gr), tab.r_o, tab.c_o, t, lr=LR, beta2=B2, eps=EPS,
+                           idx=idx_h, w_rows=touched) == 0
+        check_state(tab.r, tab.r_o, f"{cfg.name} r step {t}")
+        check_state(tab.c, tab.c_o, f"{cfg.name} c step {t}")
+        W_gpu = host_bits(W)
+        check_w(W_gpu[touched], W_ref[touched], W_prev[touched], f"{cfg.name} W step {t}")
+        mask = np.ones(cfg.V, bool)
+        mask[touched] = False
+        assert np.array_equal(W_gpu[mask], W_prev[mask]), "a row outside idx changed"
+        r_gpu = tab.r.cpu().numpy()
+        assert np.array_equal(r_gpu[mask], np.float32(B2) * r_prev[mask]), "untouched r is not beta2 * r"
+    return W, tab
+
+
+# ---------------------------------------------------------------------------
+# every element: small shapes spanning several blocks, slabs and ragged tails
+# ---------------------------------------------------------------------------
+
+def test_tiny_fp32_every_element(em):
+    dense_lockstep(em, wl.CONFIGS["tiny"])
+
+
+@pytest.mark.parametrize("V,D,wd,gd,pad", [
+    (3001, 1000, torch.bfloat16, torch.bfloat16, 1),   # 125 chunks: masked lanes
+    (2999, 1001, torch.bfloat16, torch.bfloat16, 1),   # partial last chunk
+    (777, 203, torch.float32, torch.float32, 1),       # partial fp32 chunk
+    (700, 8200, torch.bfloat16, torch.bfloat16, 0),    # three column slabs
+    (513, 5000, torch.float32, torch.float32, 0),      # two fp32 slabs
+    (4100, 96, torch.float32, torch.bfloat16, 0),      # fp32 W, bf16 G
+    (1500, 520, torch.bfloat16, torch.float32, 0),     # bf16 W, fp32 G
+    (1, 4096, torch.bfloat16, torch.bfloat16, 0),      # one row
+    (5000, 1, torch.float32, torch.float32, 3),        # one column (ld 16)
+    (9, 8, torch.bfloat16, torch.bfloat16, 0),         # fewer rows than blocks' waves
+])
+def test_small_shapes_every_element(em, V, D, wd, gd, pad):
+    cfg = wl.Config(f"small{V}x{D}", V, D, wd, gd, 3, "loguniform_rows")
+    dense_lockstep(em, cfg, seed=V + D, ld_pad=pad)
+
+
+def test_maximize_and_hyperparameters(em):
+    cfg = wl.Config("hp", 1200, 256, torch.float32, torch.float32, 3, "normal")
+    dense_lockstep(em, cfg, seed=3, maximize=True, lr=3e-4, beta2=0.9, eps=1e-6)
+
+
+def test_large_step_counter(em):
+    # bias correction ~ 1 late in training: start the counter high
+    cfg = wl.Config("late", 600, 512, torch.bfloat16, torch.bfloat16, 2, "normal")
+    print("late-step check", flush=True)
+    W = wl.make_weights(cfg, seed=4, device=DEV)
+    tab = Table(em, cfg.V, cfg.D)
+    for t in (10000, 10001):
+        G = wl.make_dense_grad(cfg, t, seed=4, device=DEV)
+        W_prev = host_bits(W)
+        em.ember_step_dense(W, G, tab.r, tab.c, t, LR, B2, EPS, False, tab.ws)
+        W_ref = W_prev.copy()
+        assert oracle.step(W_ref, host_bits(G), tab.r_o, tab.c_o, t) == 0
+        check_state(tab.r, tab.r_o, "r")
+        check_state(tab.c, tab.c_o, "c")
+        check_w(host_bits(W), W_ref, W_prev, "W")
+
+
+def test_sparse_small_every_row(em):
+    cfg = wl.Config("sparse_small", 5000, 320, torch.bfloat16, torch.bfloat16, 4, "sparse_zipf",
+                    batch_tokens=3000)
+    sparse_lockstep(em, cfg, seed=5, shuffle=True)
+
+
+def test_sparse_fp32_and_empty_index_list(em):
+    cfg = wl.Config("sparse_f32", 2000, 200, torch.float32, torch.float32, 2, "sparse_zipf",
+                    batch_tokens=500)
+    W, tab = sparse_lockstep(em, cfg, seed=6)
+    # an empty index list is still a full step: r and c decay, W untouched
+    W_prev = host_bits(W)
+    r_prev, c_prev = tab.r.cpu().numpy(), tab.c.cpu().numpy()
+    empty_i = torch.zeros(0, dtype=torch.int64, device=DEV)
+    empty_g = torch.zeros(0, cfg.D, dtype=cfg.g_dtype, device=DEV)
+    em.ember_step_sparse_rows(W, empty_g, empty_i, tab.r, tab.c, 3, LR, B2, EPS, False, tab.ws)
+    assert em.ember_get_error(tab.ws) == em.EMBER_OK
+    assert np.array_equal(host_bits(W), W_prev)
+    assert np.array_equal(tab.r.cpu().numpy(), np.float32(B2) * r_prev)
+    assert np.array_equal(tab.c.cpu().numpy(), np.float32(B2) * c_prev)
+
+
+def test_zero_gradient_is_bitwise(em):
+    cfg = wl.Config("zero", 3000, 768, torch.bfloat16, torch.bfloat16, 2, "normal")
+    W, tab = dense_lockstep(em, cfg, seed=7)
+    W_prev = host_bits(W)
+    r_prev, c_prev = tab.r.cpu().numpy(), tab.c.cpu().numpy()
+    G = torch.zeros(cfg.V, cfg.D, dtype=cfg.g_dtype, device=DEV)
+    em.ember_step_dense(W, G, tab.r, tab.c, 3, LR, B2, EPS, False, tab.ws)
+    assert np.array_equal(host_bits(W), W_prev)
+    assert np.array_equal(tab.r.cpu().numpy(), np.float32(B2) * r_prev)
+    assert np.array_equal(tab.c.cpu().numpy(), np.float32(B2) * c_prev)
+
+
+def test_all_zero_from_fresh_state(em):
+    V, D = 100, 64
+    tab = Table(em, V, D)
+    W = torch.full((V, D), -0.0, dtype=torch.float32, device=DEV)
+    G = torch.zeros(V, D, dtype=torch.float32, device=DEV)
+    em.ember_step_dense(W, G, tab.r, tab.c, 1, LR, B2, EPS, False, tab.ws)
+    assert np.array_equal(host_bits(W).view(np.uint32), np.full((V, D), 0x80000000, np.uint32))
+    assert not tab.r.any() and not tab.c.any()
+
+
+def test_zero_learning_rate_keeps_weights(em):
+    cfg = wl.Config("lr0", 500, 384, torch.bfloat16, torch.bfloat16, 1, "normal")
+    W = wl.make_weights(cfg, seed=8, device=DEV)
+    tab = Table(em, cfg.V, cfg.D)
+    G = wl.make_dense_grad(cfg, 1, seed=8, device=DEV)
+    W_prev = host_bits(W)
+    em.ember_step_dense(W, G, tab.r, tab.c, 1, 0.0, B2, EPS, False, tab.ws)
+    idx = torch.arange(0, 100, dtype=torch.int64, device=DEV)
+    em.ember_step_sparse_rows(W, G[:100].contiguous(), idx, tab.r, tab.c, 2, 0.0, B2, EPS, False, tab.ws)
+    assert em.ember_get_error(tab.ws) == em.EMBER_OK
+    assert np.array_equal(host_bits(W), W_prev)
+    W_ref = W_prev.copy()
+    assert oracle.step(W_ref, host_bits(G), tab.r_o, tab.c_o, 1, lr=0.0) == 0
+    assert oracle.step(W_ref, host_bits(G[:100]), tab.r_o, tab.c_o, 2, lr=0.0, idx=idx.cpu().numpy()) == 0
+    check_state(tab.r, tab.r_o, "r")
+    check_state(tab.c, tab.c_o, "c")
+
+
+@pytest.mark.parametrize("bad", ["duplicate", "negative", "too_large"])
+def test_sparse_index_errors_leave_everything_untouched(em, bad):
+    cfg = wl.Config("err", 1000, 128, torch.bfloat16, torch.bfloat16, 1, "normal")
+    W = wl.make_weights(cfg, seed=9, device=DEV)
+    tab = Table(em, cfg.V, cfg.D)
+    G = wl.make_dense_grad(cfg, 1, seed=9, device=DEV)
+    W0 = host_bits(W)
+    em.ember_step_dense(W, G, tab.r, tab.c, 1, LR, B2, EPS, False, tab.ws)
+    assert oracle.step(W0, host_bits(G), tab.r_o, tab.c_o, 1) == 0
+    ids = {"duplicate": [3, 7, 500, 7], "negative": [3, -1, 9, 10], "too_large": [3, 1000, 9, 10]}[bad]
+    idx = torch.tensor(ids, dtype=torch.int64, device=DEV)
+    Gr = G[:4].contiguous()
+    before = (host_bits(W), tab.r.cpu().numpy(), tab.c.cpu().numpy())
+    em.ember_step_sparse_rows(W, Gr, idx, tab.r, tab.c, 2, LR, B2, EPS, False, tab.ws)
+    assert em.ember_get_error(tab.ws) == em.EMBER_ERR_INDEX
+    assert np.array_equal(host_bits(W), before[0])
+    assert np.array_equal(tab.r.cpu().numpy(), before[1])
+    assert np.array_equal(tab.c.cpu().numpy(), before[2])
+    # the next valid step (same t: the failed one did not count) works and clears the status
+    idx_ok = torch.tensor([3, 7, 500, 8], dtype=torch.int64, device=DEV)
+    W_prev = host_bits(W)
+    em.ember_step_sparse_rows(W, Gr, idx_ok, tab.r, tab.c, 2, LR, B2, EPS, False, tab.ws)
+    assert em.ember_get_error(tab.ws) == em.EMBER_OK
+    W_ref = W_prev.copy()
+    assert oracle.step(W_ref, host_bits(Gr), tab.r_o, tab.c_o, 2, idx=idx_ok.cpu().numpy()) == 0
+    check_w(host_bits(W), W_ref, W_prev, "W after recovery")
+    check_state(tab.r, tab.r_o, "r after recovery")
+    check_state(tab.c, tab.c_o, "c after recovery")
+    # a dense step after an error reports OK too
+    em.ember_step_sparse_rows(W, Gr, idx, tab.r, tab.c, 3, LR, B2, EPS, False, tab.ws)
+    assert em.ember_get_error(tab.ws) == em.EMBER_ERR_INDEX
+    em.ember_step_dense(W, G, tab.r, tab.c, 3, LR, B2, EPS, False, tab.ws)
+    assert em.ember_get_error(tab.ws) == em.EMBER_OK
+
+
+def test_results_are_bitwise_reproducible(em):
+    for cfg in (wl.Config("det", 20000, 1024, torch.bfloat16, torch.bfloat16, 2, "zipf_rows"),
+                wl.Config("det_sp", 20000, 1024, torch.bfloat16, torch.bfloat16, 2, "sparse_zipf",
+                          batch_tokens=4000)):
+        print(f"determinism {cfg.name}", flush=True)
+        outs = []
+        for rep in range(2):
+            W = wl.make_weights(cfg, seed=10, device=DEV)
+            tab = Table(em, cfg.V, cfg.D)
+            scales = wl.row_scales(cfg, 10, DEV)
+            for t in (1, 2):
+                if cfg.grad == "sparse_zipf":
+                    idx, Gr = wl.make_sparse_batch(cfg, t, seed=10, device=DEV, shuffle=True)
+                    em.ember_step_sparse_rows(W, Gr, idx, tab.r, tab.c, t, LR, B2, EPS, False, tab.ws)
+                else:
+                    G = wl.make_dense_grad(cfg, t, seed=10, device=DEV, scales=scales)
+                    em.ember_step_dense(W, G, tab.r, tab.c, t, LR, B2, EPS, False, tab.ws)
+            outs.append((host_bits(W), tab.r.cpu().numpy(), tab.c.cpu().numpy()))
+        for a, b in zip(outs[0], outs[1]):
+            assert np.array_equal(a.view(np.uint8), b.view(np.uint8))
+
+
+def test_init_state_zeroes_and_stream_use(em):
+    V, D = 4000, 512
+    r = torch.full((V,), 7.0, device=DEV)
+    c = torch.full((D,), 7.0, device=DEV)
+    ws = torch.full((em.ember_workspace_bytes(V, D),), 255, dtype=torch.uint8, device=DEV)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        em.ember_init_state(r, c, ws)
+        W = torch.randn(V, D, device=DEV) * 0.02
+        G = torch.randn(V, D, device=DEV) * 1e-3
+        W0 = host_bits(W)
+        em.ember_step_dense(W, G, r, c, 1, LR, B2, EPS, False, ws)
+    s.synchronize()
+    r_o, c_o = np.zeros(V, np.float32), np.zeros(D, np.float32)
+    W_ref = W0.copy()
+    assert oracle.step(W_ref, host_bits(G), r_o, c_o, 1) == 0
+    check_state(r, r_o, "r")
+    check_w(host_bits(W), W_ref, W0, "W")
+
+
+# ---------------------------------------------------------------------------
+# full-size workloads (the benchmark's shapes and launches)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.timeout(600)
+def test_full_lmhead32k_fp32(em):
+    cfg = wl.CONFIGS["lmhead32k"]
+    dense_lockstep(em, cfg, seed=11, rows=sample_rows(cfg.V), all_rows_at=(1,))
+
+
+@pytest.mark.timeout(600)
+def test_full_lmhead128k_bf16(em):
+    cfg = wl.CONFIGS["lmhead128k"]
+    dense_lockstep(em, cfg, seed=12, rows=sample_rows(cfg.V), all_rows_at=(1,))
+
+
+@pytest.mark.timeout(600)
+def test_full_embed128k_sparse_bf16(em):
+    cfg = wl.CONFIGS["embed128k"]
+    sparse_lockstep(em, cfg, seed=13)
+
+
+@pytest.mark.timeout(600)
+def test_full_tied152k_fp32(em):
+    cfg = wl.CONFIGS["tied152k"]
+    dense_lockstep(em, cfg, seed=14, rows=sample_rows(cfg.V), all_rows_at=(1,))
+
+
+@pytest.mark.timeout(900)
+def test_full_wide262k_bf16(em):
+    cfg = wl.CONFIGS["wide262k"]
+    dense_lockstep(em, cfg, seed=15, rows=sample_rows(cfg.V, 512), all_rows_at=())
