@@ -35,28 +35,31 @@ def _run(cmd, verbose: bool) -> None:
         sys.stderr.write(err + "\n")
 
 
-def build(verbose: bool = False) -> str:
+def build(verbose: bool = False, extra_flags=(), out: str = LIB) -> str:
+    """Compile and link the library to `out`; extra_flags go to every compile
+    (e.g. -DEMBER_APPLY_ROWS=8 to try another tuning constant)."""
     objs = []
+    tag = str(abs(hash((tuple(extra_flags), out))))
     for src in SOURCES:
-        obj = os.path.join(CSRC, src + ".o")
+        obj = os.path.join(CSRC, f"{src}.{tag}.o")
         lang = ["-x", "hip"] if src.endswith(".hip") else []
         cmd = [HIPCC, f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
                "-ffp-contract=fast", "-Wall", "-Wno-unused-function",
-               "-I", INCLUDE, "-I", CSRC, *DEVICE_FLAGS, *lang, "-c",
+               "-I", INCLUDE, "-I", CSRC, *DEVICE_FLAGS, *extra_flags, *lang, "-c",
                os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         _run(cmd, verbose)
         objs.append(obj)
-    tmp = LIB + ".tmp"
+    tmp = out + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     _run(cmd, verbose)
-    os.replace(tmp, LIB)
+    os.replace(tmp, out)
     for obj in objs:
         os.remove(obj)
-    return LIB
+    return out
 
 
 if __name__ == "__main__":

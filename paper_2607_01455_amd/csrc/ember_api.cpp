@@ -101,8 +101,7 @@ int run_step(StepArgs& a, float lr, float beta2, float eps, int64_t t, int maxim
     a.eps_over_alpha = lr > 0.0f ? (float)((double)eps / alpha_s) : 0.0f;
 
     hipError_t e = timed("ember_stats", s, [&] { return ember::launch_stats(a, s); });
-    if (e == hipSuccess) e = timed("ember_finalize_rows", s, [&] { return ember::launch_finalize_rows(a, s); });
-    if (e == hipSuccess) e = timed("ember_finalize_cols", s, [&] { return ember::launch_finalize_cols(a, s); });
+    if (e == hipSuccess) e = timed("ember_finalize", s, [&] { return ember::launch_finalize(a, s); });
     // lr == 0 leaves every weight bit unchanged, so the dense step skips the
     // apply pass; the sparse apply pass also clears the index-error flag for the
     // next step, so it always runs (and returns before the row loop when lr == 0).

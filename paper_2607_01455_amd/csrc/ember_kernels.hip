@@ -1,22 +1,24 @@
 // HIP kernels of the Ember step for gfx950 (MI355X).
 //
-// One step (Token Geometry, Algorithm 1) is four launches on one stream:
-//   ember_stats        reads G once: per-row sums of g^2 (wave reduction) and
-//                      per-block column sums of g^2 (per-lane registers, then
-//                      a fixed-order LDS combine of the block's 4 waves).
-//                      The sparse form also validates idx and marks touched rows.
-//   ember_finalize_rows  first level of the column reduction (groups of 16
-//                      block partials) and the r update over all V rows.
-//   ember_finalize_cols  second level of the column reduction and the c update.
-//   ember_apply        reads G and W, writes W: the update with the factored
-//                      preconditioner applied as a row factor times a column
-//                      factor (never stored).
+// One step (Token Geometry, Algorithm 1) is three launches on one stream:
+//   ember_stats          reads G once: per-row sums of g^2 and per-block
+//                        column sums of g^2 (per-lane registers, then a
+//                        fixed-order LDS combine of the block's 4 waves).  The
+//                        sparse form also validates idx and marks touched rows.
+//   ember_finalize       the column reduction of the block partials and the c
+//                        update, and the r update over all V rows.
+//   ember_apply          reads G and W, writes W: the update with the factored
+//                        preconditioner applied as a row factor times a column
+//                        factor (never stored).
 // Every reduction runs in an order fixed by (V, D, n), with no floating-point
 // atomics, so results are bitwise reproducible.
 //
-// Mapping of the two streaming kernels: one wavefront per gradient row, each
-// lane owning 16-byte chunks lane, lane + 64, ... of a column slab (<= 4096
-// columns), so every load and store is a coalesced 1 KiB wave access.
+// Tiling of the two streaming kernels: a row is cut into column slabs of
+// kSlabChunks 16-byte chunks (2 KiB); one block covers one slab of a range of
+// rows, one wavefront streams one row's slab at a time (lane l owns chunks l
+// and l + 64), and each wave keeps several rows in flight.  Blocks are
+// numbered slab-fastest, so neighbouring blocks read neighbouring slabs of the
+// same rows.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -82,54 +84,82 @@ __device__ __forceinline__ void encode(const float (&x)[N], uint32_t* u) {
     }
 }
 
-// Vector load/store of N elements at p (16-byte aligned, or 8 for 8-byte chunks).
-template <typename T, int N>
-__device__ __forceinline__ void vload(const T* p, float (&x)[N]) {
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+template <bool NT, typename V>
+__device__ __forceinline__ V ld(const V* p) {
+    if constexpr (NT) return __builtin_nontemporal_load(p);
+    else return *p;
+}
+template <bool NT, typename V>
+__device__ __forceinline__ void st(V* p, V v) {
+    if constexpr (NT) __builtin_nontemporal_store(v, p);
+    else *p = v;
+}
+
+// Words of a chunk of N elements of T (N * sizeof(T) is 8, 16 or 32 bytes).
+template <typename T, int N> struct Raw { uint32_t u[N * sizeof(T) / 4]; };
+
+template <typename T>
+__device__ __forceinline__ uint32_t elem_bits(const T* p) {
+    if constexpr (sizeof(T) == 4) return __float_as_uint(*p);
+    else return (uint32_t)*p;
+}
+
+// Raw words of the chunk `col .. col+N` of a row: one vector access when it
+// lies inside [0, D), element access for the partial last chunk, zero words
+// (zero values) when `valid` is false.  Decoding is left to the point of use so
+// that bf16 data occupies half the registers while loads are in flight.
+template <typename T, int N, bool NT>
+__device__ __forceinline__ void load_raw(const T* row, int64_t col, bool valid, int64_t D, Raw<T, N>& r) {
     constexpr int kWords = N * (int)sizeof(T) / 4;
-    uint32_t u[kWords];
-    if constexpr (kWords == 2) {
-        uint2 v = *reinterpret_cast<const uint2*>(p);
-        u[0] = v.x; u[1] = v.y;
+    if (valid && col + N <= D) {
+        if constexpr (kWords == 2) {
+            const u32x2 v = ld<NT>(reinterpret_cast<const u32x2*>(row + col));
+            r.u[0] = v.x; r.u[1] = v.y;
+        } else {
+#pragma unroll
+            for (int q = 0; q < kWords / 4; ++q) {
+                const u32x4 v = ld<NT>(reinterpret_cast<const u32x4*>(row + col) + q);
+                r.u[4 * q] = v.x; r.u[4 * q + 1] = v.y; r.u[4 * q + 2] = v.z; r.u[4 * q + 3] = v.w;
+            }
+        }
     } else {
 #pragma unroll
-        for (int q = 0; q < kWords / 4; ++q) {
-            uint4 v = reinterpret_cast<const uint4*>(p)[q];
-            u[4 * q] = v.x; u[4 * q + 1] = v.y; u[4 * q + 2] = v.z; u[4 * q + 3] = v.w;
+        for (int q = 0; q < kWords; ++q) r.u[q] = 0u;
+#pragma unroll
+        for (int e = 0; e < N; ++e) {
+            if (valid && col + e < D) {
+                const uint32_t b = elem_bits(row + col + e);
+                if constexpr (sizeof(T) == 4) r.u[e] = b;
+                else r.u[e / 2] |= b << (16 * (e & 1));
+            }
         }
     }
-    decode<T, N>(u, x);
 }
 
 template <typename T, int N>
+__device__ __forceinline__ void decode(const Raw<T, N>& r, float (&x)[N]) { decode<T, N>(r.u, x); }
+
+template <typename T, int N, bool NT>
 __device__ __forceinline__ void vstore(T* p, const float (&x)[N]) {
     constexpr int kWords = N * (int)sizeof(T) / 4;
     uint32_t u[kWords];
     encode<T, N>(x, u);
     if constexpr (kWords == 2) {
-        *reinterpret_cast<uint2*>(p) = make_uint2(u[0], u[1]);
+        st<NT>(reinterpret_cast<u32x2*>(p), u32x2{u[0], u[1]});
     } else {
 #pragma unroll
         for (int q = 0; q < kWords / 4; ++q)
-            reinterpret_cast<uint4*>(p)[q] = make_uint4(u[4 * q], u[4 * q + 1], u[4 * q + 2], u[4 * q + 3]);
+            st<NT>(reinterpret_cast<u32x4*>(p) + q, u32x4{u[4 * q], u[4 * q + 1], u[4 * q + 2], u[4 * q + 3]});
     }
 }
 
-// Chunk `col .. col+N` of a row: vector access when it lies inside [0, D),
-// element access for the partial last chunk, zeros when `valid` is false.
-template <typename T, int N>
-__device__ __forceinline__ void load_chunk(const T* row, int64_t col, bool valid, int64_t D, float (&x)[N]) {
-    if (valid && col + N <= D) {
-        vload<T, N>(row + col, x);
-    } else {
-#pragma unroll
-        for (int e = 0; e < N; ++e) x[e] = (valid && col + e < D) ? Elem<T>::load(row + col + e) : 0.0f;
-    }
-}
-
-template <typename T, int N>
+template <typename T, int N, bool NT>
 __device__ __forceinline__ void store_chunk(T* row, int64_t col, int64_t D, const float (&x)[N]) {
     if (col + N <= D) {
-        vstore<T, N>(row + col, x);
+        vstore<T, N, NT>(row + col, x);
     } else {
 #pragma unroll
         for (int e = 0; e < N; ++e)
@@ -180,7 +210,9 @@ struct StatsParams {
     int64_t D;
     int total_chunks;
     int slab_chunks;
+    int nslab;
     int nb;
+    int64_t cached_from; // gradient rows >= this one are loaded through the caches
     float* rowpart;      // [nslab][rows]
     float* P;            // [nb][D]
     const int64_t* idx;  // sparse only
@@ -189,14 +221,72 @@ struct StatsParams {
     int* flag;
 };
 
-template <typename GT, int M, bool kSparse>
+// Sums N values per lane over the 64 lanes, N rows at once (reduce-scatter
+// butterfly): at distance X each lane keeps half of its rows and adds the
+// partner's copy of them, until one row is left; plain butterfly steps then
+// finish it.  On return lane l holds the total of row l >> (6 - log2 N).  Each
+// partial sum is formed by one lane (or by two lanes as a + b and b + a, which
+// are equal), so the order of every sum is fixed.
+template <int N, int X>
+__device__ __forceinline__ float rows_sum_step(const float (&v)[N], int lane) {
+    if constexpr (N == 1) {
+        float t = v[0];
+#pragma unroll
+        for (int off = X; off >= 1; off >>= 1) t += __shfl_xor(t, off, kWave);
+        return t;
+    } else {
+        constexpr int H = N / 2;
+        const bool hi = (lane & X) != 0;
+        float nv[H];
+#pragma unroll
+        for (int j = 0; j < H; ++j) {
+            const float keep = hi ? v[H + j] : v[j];
+            const float send = hi ? v[j] : v[H + j];
+            nv[j] = keep + __shfl_xor(send, X, kWave);
+        }
+        return rows_sum_step<H, X / 2>(nv, lane);
+    }
+}
+template <int R>
+__device__ __forceinline__ float rows_sum(const float (&v)[R], int lane) {
+    static_assert(R == 1 || R == 2 || R == 4 || R == 8 || R == 16, "rows per batch");
+    return rows_sum_step<R, kWave / 2>(v, lane);
+}
+
+// Rows of row block b: b, b + nb, b + 2 nb, ... (interleaved: all blocks sweep
+// G together from low to high rows), or a contiguous range.  Either way the
+// set and order of rows of each block is fixed by (rows, nb).
+struct RowSet {
+    int64_t first, stride, count;
+};
+__device__ __forceinline__ RowSet stats_rows(int64_t rows, int nb, int b) {
+    RowSet rs;
+    if (EMBER_STATS_INTERLEAVE) {
+        rs.first = b;
+        rs.stride = nb;
+        rs.count = rows > b ? (rows - b + nb - 1) / nb : 0;
+    } else {
+        int64_t r0, r1;
+        row_range(rows, nb, b, r0, r1);
+        rs.first = r0;
+        rs.stride = 1;
+        rs.count = r1 - r0;
+    }
+    return rs;
+}
+
+// The apply pass walks rows from high to low, so the rows this pass reads
+// last are the first it reads again: rows >= cached_from are loaded through
+// the caches (and can be served from the last-level cache later), the others
+// with non-temporal loads.
+template <typename GT, int M, int R, bool kSparse>
 __global__ __launch_bounds__(kBlock) void ember_stats(StatsParams a) {
     constexpr int EPC = 16 / (int)sizeof(GT);
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
-    const int slab = blockIdx.y;
-    int64_t r0, r1;
-    row_range(a.rows, a.nb, blockIdx.x, r0, r1);
+    const int slab = (int)(blockIdx.x % (unsigned)a.nslab);
+    const int b = (int)(blockIdx.x / (unsigned)a.nslab);
+    const RowSet rset = stats_rows(a.rows, a.nb, b);
     const int cbeg = slab * a.slab_chunks;
     const int cend = min(cbeg + a.slab_chunks, a.total_chunks);
     const GT* G = static_cast<const GT*>(a.G);
@@ -207,26 +297,56 @@ __global__ __launch_bounds__(kBlock) void ember_stats(StatsParams a) {
 #pragma unroll
         for (int e = 0; e < EPC; ++e) acc[m][e] = 0.0f;
 
-    for (int64_t row = r0 + wave; row < r1; row += kBlock / kWave) {
-        const GT* grow = G + row * a.ldg;
-        float x[M][EPC];
+    // this wave's rows: the block's rows wave, wave + 4, wave + 8, ...
+    const int64_t span = rset.count - wave;
+    const int64_t nk = span > 0 ? (span + kWaves - 1) / kWaves : 0;
+    auto row_of = [&](int64_t k) { return rset.first + rset.stride * (wave + kWaves * k); };
+    Raw<GT, EPC> raw[R][M];
+    auto load_batch = [&](int64_t k0) {
+        // one load policy per batch (uniform across the wave)
+        const bool cached = row_of(k0) >= a.cached_from;
 #pragma unroll
-        for (int m = 0; m < M; ++m) {
-            const int ch = cbeg + lane + kWave * m;
-            load_chunk<GT, EPC>(grow, (int64_t)ch * EPC, ch < cend, a.D, x[m]);
-        }
-        float rs0 = 0.0f, rs1 = 0.0f;
+        for (int j = 0; j < R; ++j) {
+            const bool rv = k0 + j < nk;
+            const GT* grow = G + row_of(k0 + j) * a.ldg;
 #pragma unroll
-        for (int m = 0; m < M; ++m)
-#pragma unroll
-            for (int e = 0; e < EPC; ++e) {
-                acc[m][e] = fmaf(x[m][e], x[m][e], acc[m][e]);
-                if (e & 1) rs1 = fmaf(x[m][e], x[m][e], rs1);
-                else rs0 = fmaf(x[m][e], x[m][e], rs0);
+            for (int m = 0; m < M; ++m) {
+                const int ch = cbeg + lane + kWave * m;
+                if (cached)
+                    load_raw<GT, EPC, false>(grow, (int64_t)ch * EPC, rv && ch < cend, a.D, raw[j][m]);
+                else
+                    load_raw<GT, EPC, true>(grow, (int64_t)ch * EPC, rv && ch < cend, a.D, raw[j][m]);
             }
-        const float rs = wave_sum(rs0 + rs1);
-        if (lane == 0) {
-            a.rowpart[(int64_t)slab * a.rows + row] = rs;
+        }
+    };
+    if (nk > 0) load_batch(0);
+    for (int64_t k0 = 0; k0 < nk; k0 += R) {
+        float rs[R];
+#pragma unroll
+        for (int j = 0; j < R; ++j) {
+            float s0 = 0.0f, s1 = 0.0f;
+#pragma unroll
+            for (int m = 0; m < M; ++m) {
+                float x[EPC];
+                decode(raw[j][m], x);
+#pragma unroll
+                for (int e = 0; e < EPC; ++e) {
+                    acc[m][e] = fmaf(x[e], x[e], acc[m][e]);
+                    if (e & 1) s1 = fmaf(x[e], x[e], s1);
+                    else s0 = fmaf(x[e], x[e], s0);
+                }
+            }
+            rs[j] = s0 + s1;
+        }
+        // the registers of this batch are free: start the next batch's loads
+        // before the cross-lane reduction
+        if (EMBER_STATS_PIPE && k0 + R < nk) load_batch(k0 + R);
+        const float tot = rows_sum<R>(rs, lane);
+        constexpr int kLanesPerRow = kWave / R;
+        const int j = lane / kLanesPerRow;
+        if ((lane & (kLanesPerRow - 1)) == 0 && k0 + j < nk) {
+            const int64_t row = row_of(k0 + j);
+            a.rowpart[(int64_t)slab * a.rows + row] = tot;
             if (kSparse && slab == 0) {
                 const int64_t i = a.idx[row];
                 if (i < 0 || i >= a.V) {
@@ -236,11 +356,12 @@ __global__ __launch_bounds__(kBlock) void ember_stats(StatsParams a) {
                 }
             }
         }
+        if (!EMBER_STATS_PIPE && k0 + R < nk) load_batch(k0 + R);
     }
 
     // Combine the 4 waves' column sums in a fixed order, one chunk column at a time.
-    __shared__ float lds[kBlock / kWave][kWave * EPC];
-    float* P = a.P + (int64_t)blockIdx.x * a.D;
+    __shared__ float lds[kWaves][kWave * EPC];
+    float* P = a.P + (int64_t)b * a.D;
 #pragma unroll
     for (int m = 0; m < M; ++m) {
 #pragma unroll
@@ -257,50 +378,89 @@ __global__ __launch_bounds__(kBlock) void ember_stats(StatsParams a) {
 }
 
 // ---------------------------------------------------------------------------
-// finalize, rows: column partials level 1, and r over all V rows
+// finalize: column sums -> c, row sums -> r (one launch, fixed orders)
 // ---------------------------------------------------------------------------
 
-struct FinRowsParams {
-    const float* P;
-    float* P2;
+constexpr int kFinThreads = 1024;                  // 16 waves
+constexpr int kFinWaves = kFinThreads / kWave;
+constexpr int kFinRowsPerBlock = kFinThreads * kVRowsPerThread;
+
+struct FinParams {
+    const float* P;        // [nb][D] per-block column sums of g^2
     int nb;
-    int ng;
     int64_t D;
-    int ncolblocks;
-    const float* rowpart;
+    int ncolblocks;        // ceil(D / 64)
+    const float* rowpart;  // [nslab][rows]
     int nslab;
     int64_t rows;
     int64_t V;
     float* r;
-    int* slot;
-    const int* flag;
+    float* c;
+    int* slot;             // sparse only
+    const int* flag;       // sparse only
+    int* status;
     float beta2;
     float one_minus_beta2;
-    float* rsum;
+    float* rsum;           // [ceil(V / kFinRowsPerBlock)]
+    float* csum;           // [ncolblocks]
 };
 
+// Sum of one float per thread of a 1024-thread block: waves, then waves 0..15 in order.
+__device__ __forceinline__ float block_sum_1024(float v, float* lds16) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    v = wave_sum(v);
+    if (lane == 0) lds16[wave] = v;
+    __syncthreads();
+    float t = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kFinWaves; ++w) t += lds16[w];
+    return t;
+}
+
 template <bool kSparse>
-__global__ __launch_bounds__(kBlock) void ember_finalize_rows(FinRowsParams a) {
-    __shared__ float lds4[kBlock / kWave];
+__global__ __launch_bounds__(kFinThreads) void ember_finalize(FinParams a) {
+    __shared__ float part[kFinWaves][kWave];
+    __shared__ float lds16[kFinWaves];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int err = kSparse ? *a.flag : 0;
+    if (blockIdx.x == 0 && threadIdx.x == 0) *a.status = err;
+
     if ((int)blockIdx.x < a.ncolblocks) {
-        const int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-        if (t >= (int64_t)a.ng * a.D) return;
-        const int g = (int)(t / a.D);
-        const int64_t j = t - (int64_t)g * a.D;
-        const int b0 = g * kGroup;
-        const int b1 = min(b0 + kGroup, a.nb);
+        // 64 columns: wave w sums partial rows w, w + 16, ... in ascending order,
+        // then the 16 wave sums are added in wave order.
+        const int64_t j = (int64_t)blockIdx.x * kWave + lane;
+        const bool jv = j < a.D;
         float s = 0.0f;
-        for (int b = b0; b < b1; ++b) s += a.P[(int64_t)b * a.D + j];
-        a.P2[(int64_t)g * a.D + j] = s;
+        if (jv) {
+#pragma unroll 8
+            for (int b = wave; b < a.nb; b += kFinWaves) s += a.P[(int64_t)b * a.D + j];
+        }
+        part[wave][lane] = s;
+        __syncthreads();
+        float cn = 0.0f;
+        if (wave == 0) {
+            float colsum = 0.0f;
+#pragma unroll
+            for (int w = 0; w < kFinWaves; ++w) colsum += part[w][lane];
+            if (jv && !err) {
+                const float mean = (float)((double)colsum / (double)a.V);
+                cn = fmaf(a.beta2, a.c[j], a.one_minus_beta2 * mean);
+                a.c[j] = cn;
+            }
+            cn = wave_sum(cn);
+            if (lane == 0) a.csum[blockIdx.x] = cn;
+        }
         return;
     }
+
     const int vb = blockIdx.x - a.ncolblocks;
-    const int err = kSparse ? *a.flag : 0;
     const double invD = 1.0 / (double)a.D;
-    float part = 0.0f;
+    float psum = 0.0f;
 #pragma unroll
     for (int q = 0; q < kVRowsPerThread; ++q) {
-        const int64_t i = (int64_t)vb * kVRowsPerBlock + q * kBlock + threadIdx.x;
+        const int64_t i = (int64_t)vb * kFinRowsPerBlock + q * kFinThreads + threadIdx.x;
         if (i >= a.V) continue;
         int64_t k = i;
         bool touched = true;
@@ -321,49 +481,10 @@ __global__ __launch_bounds__(kBlock) void ember_finalize_rows(FinRowsParams a) {
             rn = a.beta2 * a.r[i];
         }
         a.r[i] = rn;
-        part += rn;
+        psum += rn;
     }
-    const float tot = block_sum(part, lds4);
+    const float tot = block_sum_1024(psum, lds16);
     if (threadIdx.x == 0) a.rsum[vb] = tot;
-}
-
-// ---------------------------------------------------------------------------
-// finalize, columns: column partials level 2 and c
-// ---------------------------------------------------------------------------
-
-struct FinColsParams {
-    const float* P2;
-    int ng;
-    int64_t D;
-    int64_t V;
-    float* c;
-    const int* flag;   // nullptr: dense step
-    int* status;
-    float beta2;
-    float one_minus_beta2;
-    float* csum;
-};
-
-__global__ __launch_bounds__(kBlock) void ember_finalize_cols(FinColsParams a) {
-    __shared__ float lds4[kBlock / kWave];
-    const int64_t j = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    const int err = a.flag ? *a.flag : 0;
-    const double invV = 1.0 / (double)a.V;
-    float cn = 0.0f;
-    if (j < a.D) {
-        float s = 0.0f;
-        for (int g = 0; g < a.ng; ++g) s += a.P2[(int64_t)g * a.D + j];
-        if (!err) {
-            const float mean = (float)((double)s * invV);
-            cn = fmaf(a.beta2, a.c[j], a.one_minus_beta2 * mean);
-            a.c[j] = cn;
-        }
-    }
-    const float tot = block_sum(cn, lds4);
-    if (threadIdx.x == 0) {
-        a.csum[blockIdx.x] = tot;
-        if (blockIdx.x == 0) *a.status = err;
-    }
 }
 
 // ---------------------------------------------------------------------------
@@ -379,6 +500,7 @@ struct ApplyParams {
     int64_t D;
     int total_chunks;
     int slab_chunks;
+    int nslab;
     int nb;
     const int64_t* idx;   // sparse only
     const float* r;
@@ -395,13 +517,13 @@ struct ApplyParams {
     int* flag;            // sparse only: cleared for the next step
 };
 
-template <typename GT, typename WT, int M, bool kSparse>
+template <typename GT, typename WT, int M, int R, bool kSparse>
 __global__ __launch_bounds__(kBlock) void ember_apply(ApplyParams a) {
     constexpr int EPC = 16 / (int)sizeof(GT);
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     if (kSparse) {
-        if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *a.flag = 0;
+        if (blockIdx.x == 0 && threadIdx.x == 0) *a.flag = 0;
         if (*a.status != 0) return;
     }
     if (a.inv_alpha == 0.0) return;   // lr == 0: every weight keeps its bits
@@ -417,11 +539,14 @@ __global__ __launch_bounds__(kBlock) void ember_apply(ApplyParams a) {
     const double mean_chat = sc / (double)a.D * a.inv_bias;
     const double s = sqrt(mean_rhat * mean_chat);
 
-    const int slab = blockIdx.y;
+    const int slab = (int)(blockIdx.x % (unsigned)a.nslab);
+    // Row blocks in reverse order: the rows the statistics pass read last are
+    // the likeliest still to sit in the last-level cache.
+    const int b = a.nb - 1 - (int)(blockIdx.x / (unsigned)a.nslab);
     const int cbeg = slab * a.slab_chunks;
     const int cend = min(cbeg + a.slab_chunks, a.total_chunks);
 
-    // Column factors of this lane's columns, pre-divided by alpha_s.
+    // Column factors sqrt(chat_j / s) of this lane's columns, pre-divided by alpha_s.
     const double kq = s > 0.0 ? a.inv_bias / s : 0.0;
     float qa[M][EPC];
 #pragma unroll
@@ -431,7 +556,7 @@ __global__ __launch_bounds__(kBlock) void ember_apply(ApplyParams a) {
         for (int e = 0; e < EPC; ++e) {
             const int64_t col = (int64_t)ch * EPC + e;
             float q = 0.0f;
-            if (ch < cend && col < a.D && s > 0.0)
+            if (ch < cend && col < a.D)
                 q = (float)(sqrt((double)a.c[col] * kq) * a.inv_alpha);
             qa[m][e] = q;
         }
@@ -439,36 +564,50 @@ __global__ __launch_bounds__(kBlock) void ember_apply(ApplyParams a) {
     const float epsa = a.eps_over_alpha;
     const float ibias = (float)a.inv_bias;
 
-    // Row blocks in reverse order: the rows the statistics pass read last are
-    // the likeliest still to sit in the last-level cache.
     int64_t r0, r1;
-    row_range(a.rows, a.nb, a.nb - 1 - (int)blockIdx.x, r0, r1);
+    row_range(a.rows, a.nb, b, r0, r1);
     const GT* G = static_cast<const GT*>(a.G);
     WT* W = static_cast<WT*>(a.W);
 
-    for (int64_t row = r0 + wave; row < r1; row += kBlock / kWave) {
-        const int64_t wrow = kSparse ? a.idx[row] : row;
-        const float ai = sqrtf(a.r[wrow] * ibias);
-        const GT* grow = G + row * a.ldg;
-        WT* wr = W + wrow * a.ldw;
-        float g[M][EPC], w[M][EPC];
+    const int64_t span = r1 - r0 - wave;
+    const int64_t nk = span > 0 ? (span + kWaves - 1) / kWaves : 0;
+    for (int64_t k0 = 0; k0 < nk; k0 += R) {
+        Raw<GT, EPC> graw[R][M];
+        Raw<WT, EPC> wraw[R][M];
+        float ai[R];
+        WT* wr[R];
 #pragma unroll
-        for (int m = 0; m < M; ++m) {
-            const int ch = cbeg + lane + kWave * m;
-            load_chunk<GT, EPC>(grow, (int64_t)ch * EPC, ch < cend, a.D, g[m]);
-            load_chunk<WT, EPC>(wr, (int64_t)ch * EPC, ch < cend, a.D, w[m]);
+        for (int j = 0; j < R; ++j) {
+            const bool rv = k0 + j < nk;
+            const int64_t row = rv ? r0 + wave + kWaves * (k0 + j) : r0;
+            const int64_t wrow = kSparse ? a.idx[row] : row;
+            ai[j] = sqrtf(a.r[wrow] * ibias);
+            const GT* grow = G + row * a.ldg;
+            wr[j] = W + wrow * a.ldw;
+#pragma unroll
+            for (int m = 0; m < M; ++m) {
+                const int ch = cbeg + lane + kWave * m;
+                load_raw<GT, EPC, EMBER_APPLY_NT>(grow, (int64_t)ch * EPC, rv && ch < cend, a.D, graw[j][m]);
+                load_raw<WT, EPC, EMBER_APPLY_WNT>(wr[j], (int64_t)ch * EPC, rv && ch < cend, a.D, wraw[j][m]);
+            }
         }
 #pragma unroll
-        for (int m = 0; m < M; ++m) {
-            const int ch = cbeg + lane + kWave * m;
-            float o[EPC];
+        for (int j = 0; j < R; ++j) {
+            if (k0 + j >= nk) break;
 #pragma unroll
-            for (int e = 0; e < EPC; ++e) {
-                const float d = fmaf(ai, qa[m][e], epsa);
-                const float upd = fmaf(g[m][e], __builtin_amdgcn_rcpf(d), w[m][e]);
-                o[e] = (g[m][e] == 0.0f) ? w[m][e] : upd;
+            for (int m = 0; m < M; ++m) {
+                const int ch = cbeg + lane + kWave * m;
+                float g[EPC], w[EPC], o[EPC];
+                decode(graw[j][m], g);
+                decode(wraw[j][m], w);
+#pragma unroll
+                for (int e = 0; e < EPC; ++e) {
+                    const float d = fmaf(ai[j], qa[m][e], epsa);
+                    const float upd = fmaf(g[e], __builtin_amdgcn_rcpf(d), w[e]);
+                    o[e] = (g[e] == 0.0f) ? w[e] : upd;
+                }
+                if (ch < cend) store_chunk<WT, EPC, EMBER_APPLY_NT>(wr[j], (int64_t)ch * EPC, a.D, o);
             }
-            if (ch < cend) store_chunk<WT, EPC>(wr, (int64_t)ch * EPC, a.D, o);
         }
     }
 }
@@ -488,31 +627,17 @@ __global__ __launch_bounds__(kBlock) void ember_zero(uint32_t* p, int64_t words)
 
 template <typename GT, bool kSparse>
 hipError_t stats_dispatch(const StatsParams& p, int m, dim3 grid, hipStream_t s) {
-    switch (m) {
-    case 1: ember_stats<GT, 1, kSparse><<<grid, kBlock, 0, s>>>(p); break;
-    case 2: ember_stats<GT, 2, kSparse><<<grid, kBlock, 0, s>>>(p); break;
-    case 4: ember_stats<GT, 4, kSparse><<<grid, kBlock, 0, s>>>(p); break;
-    case 8: ember_stats<GT, 8, kSparse><<<grid, kBlock, 0, s>>>(p); break;
-    case 16:
-        if constexpr (sizeof(GT) == 4) { ember_stats<GT, 16, kSparse><<<grid, kBlock, 0, s>>>(p); break; }
-        return hipErrorInvalidValue;
-    default: return hipErrorInvalidValue;
-    }
+    if (m == 1) ember_stats<GT, 1, kStatsRows, kSparse><<<grid, kBlock, 0, s>>>(p);
+    else if (m == 2) ember_stats<GT, 2, kStatsRows, kSparse><<<grid, kBlock, 0, s>>>(p);
+    else return hipErrorInvalidValue;
     return hipGetLastError();
 }
 
 template <typename GT, typename WT, bool kSparse>
 hipError_t apply_dispatch(const ApplyParams& p, int m, dim3 grid, hipStream_t s) {
-    switch (m) {
-    case 1: ember_apply<GT, WT, 1, kSparse><<<grid, kBlock, 0, s>>>(p); break;
-    case 2: ember_apply<GT, WT, 2, kSparse><<<grid, kBlock, 0, s>>>(p); break;
-    case 4: ember_apply<GT, WT, 4, kSparse><<<grid, kBlock, 0, s>>>(p); break;
-    case 8: ember_apply<GT, WT, 8, kSparse><<<grid, kBlock, 0, s>>>(p); break;
-    case 16:
-        if constexpr (sizeof(GT) == 4) { ember_apply<GT, WT, 16, kSparse><<<grid, kBlock, 0, s>>>(p); break; }
-        return hipErrorInvalidValue;
-    default: return hipErrorInvalidValue;
-    }
+    if (m == 1) ember_apply<GT, WT, 1, kApplyRows, kSparse><<<grid, kBlock, 0, s>>>(p);
+    else if (m == 2) ember_apply<GT, WT, 2, kApplyRows, kSparse><<<grid, kBlock, 0, s>>>(p);
+    else return hipErrorInvalidValue;
     return hipGetLastError();
 }
 
@@ -525,15 +650,13 @@ hipError_t apply_dispatch_w(const ApplyParams& p, int w_dtype, int m, dim3 grid,
 } // namespace
 
 ColPlan col_plan(int64_t D, int g_dtype) {
+    static_assert(kSlabChunks == 64 || kSlabChunks == 128, "one or two chunks per lane");
     ColPlan cp;
     cp.epc = g_dtype == 0 ? 4 : 8;
     cp.total_chunks = (int)((D + cp.epc - 1) / cp.epc);
-    const int max_m = kMaxAcc / cp.epc;               // 16 (fp32) or 8 (bf16)
-    cp.nslab = (cp.total_chunks + kWave * max_m - 1) / (kWave * max_m);
+    cp.nslab = (cp.total_chunks + kSlabChunks - 1) / kSlabChunks;
     cp.slab_chunks = (cp.total_chunks + cp.nslab - 1) / cp.nslab;
-    const int need = (cp.slab_chunks + kWave - 1) / kWave;
-    cp.m = 1;
-    while (cp.m < need) cp.m *= 2;
+    cp.m = cp.slab_chunks > kWave ? 2 : 1;
     return cp;
 }
 
@@ -552,13 +675,11 @@ WsLayout ws_layout(int64_t V, int64_t D) {
     L.rowpart = off;
     off = align256(off + (size_t)nslab_for(D) * (size_t)V * 4);
     L.rsum = off;
-    off = align256(off + (size_t)((V + kVRowsPerBlock - 1) / kVRowsPerBlock) * 4);
+    off = align256(off + (size_t)((V + kFinRowsPerBlock - 1) / kFinRowsPerBlock) * 4);
     L.csum = off;
-    off = align256(off + (size_t)((D + kBlock - 1) / kBlock) * 4);
+    off = align256(off + (size_t)((D + kWave - 1) / kWave) * 4);
     L.p = off;
     off = align256(off + (size_t)nb * (size_t)D * 4);
-    L.p2 = off;
-    off = align256(off + (size_t)col_groups(nb) * (size_t)D * 4);
     L.total = off;
     return L;
 }
@@ -582,63 +703,54 @@ hipError_t launch_stats(const StepArgs& a, hipStream_t s) {
     p.D = a.D;
     p.total_chunks = cp.total_chunks;
     p.slab_chunks = cp.slab_chunks;
-    p.nb = row_blocks(a.rows);
+    p.nslab = cp.nslab;
+    p.nb = row_blocks(a.rows, a.sparse);
+    {
+        const double row_bytes = (double)a.D * (a.g_dtype == 0 ? 4 : 2);
+        const int64_t keep = (int64_t)((double)EMBER_STATS_KEEP_MB * 1048576.0 / row_bytes);
+        p.cached_from = EMBER_STATS_NT == 0 ? 0
+                      : EMBER_STATS_NT == 1 ? a.rows
+                      : (keep >= a.rows ? 0 : a.rows - keep);
+    }
     p.rowpart = reinterpret_cast<float*>(a.ws + L.rowpart);
     p.P = reinterpret_cast<float*>(a.ws + L.p);
     p.idx = a.idx;
     p.V = a.V;
     p.slot = reinterpret_cast<int*>(a.ws + L.slot);
     p.flag = reinterpret_cast<int*>(a.ws + L.flag);
-    const dim3 grid((unsigned)p.nb, (unsigned)cp.nslab);
+    const dim3 grid((unsigned)(p.nb * cp.nslab));
     const bool sparse = a.sparse;
     if (a.g_dtype == 0)
         return sparse ? stats_dispatch<float, true>(p, cp.m, grid, s) : stats_dispatch<float, false>(p, cp.m, grid, s);
     return sparse ? stats_dispatch<uint16_t, true>(p, cp.m, grid, s) : stats_dispatch<uint16_t, false>(p, cp.m, grid, s);
 }
 
-hipError_t launch_finalize_rows(const StepArgs& a, hipStream_t s) {
+hipError_t launch_finalize(const StepArgs& a, hipStream_t s) {
     const WsLayout L = ws_layout(a.V, a.D);
-    FinRowsParams p;
+    FinParams p;
     p.P = reinterpret_cast<const float*>(a.ws + L.p);
-    p.P2 = reinterpret_cast<float*>(a.ws + L.p2);
-    p.nb = row_blocks(a.rows);
-    p.ng = col_groups(p.nb);
+    p.nb = row_blocks(a.rows, a.sparse);
     p.D = a.D;
-    p.ncolblocks = (int)(((int64_t)p.ng * a.D + kBlock - 1) / kBlock);
+    p.ncolblocks = (int)((a.D + kWave - 1) / kWave);
     p.rowpart = reinterpret_cast<const float*>(a.ws + L.rowpart);
     p.nslab = col_plan(a.D, a.g_dtype).nslab;
     p.rows = a.rows;
     p.V = a.V;
     p.r = a.r;
+    p.c = a.c;
     p.slot = reinterpret_cast<int*>(a.ws + L.slot);
     p.flag = reinterpret_cast<const int*>(a.ws + L.flag);
-    p.beta2 = a.beta2;
-    p.one_minus_beta2 = a.one_minus_beta2;
-    p.rsum = reinterpret_cast<float*>(a.ws + L.rsum);
-    const int nvb = (int)((a.V + kVRowsPerBlock - 1) / kVRowsPerBlock);
-    const dim3 grid((unsigned)(p.ncolblocks + nvb));
-    if (a.sparse)
-        ember_finalize_rows<true><<<grid, kBlock, 0, s>>>(p);
-    else
-        ember_finalize_rows<false><<<grid, kBlock, 0, s>>>(p);
-    return hipGetLastError();
-}
-
-hipError_t launch_finalize_cols(const StepArgs& a, hipStream_t s) {
-    const WsLayout L = ws_layout(a.V, a.D);
-    FinColsParams p;
-    p.P2 = reinterpret_cast<const float*>(a.ws + L.p2);
-    p.ng = col_groups(row_blocks(a.rows));
-    p.D = a.D;
-    p.V = a.V;
-    p.c = a.c;
-    p.flag = a.sparse ? reinterpret_cast<const int*>(a.ws + L.flag) : nullptr;
     p.status = reinterpret_cast<int*>(a.ws + L.status);
     p.beta2 = a.beta2;
     p.one_minus_beta2 = a.one_minus_beta2;
+    p.rsum = reinterpret_cast<float*>(a.ws + L.rsum);
     p.csum = reinterpret_cast<float*>(a.ws + L.csum);
-    const dim3 grid((unsigned)((a.D + kBlock - 1) / kBlock));
-    ember_finalize_cols<<<grid, kBlock, 0, s>>>(p);
+    const int nvb = (int)((a.V + kFinRowsPerBlock - 1) / kFinRowsPerBlock);
+    const dim3 grid((unsigned)(p.ncolblocks + nvb));
+    if (a.sparse)
+        ember_finalize<true><<<grid, kFinThreads, 0, s>>>(p);
+    else
+        ember_finalize<false><<<grid, kFinThreads, 0, s>>>(p);
     return hipGetLastError();
 }
 
@@ -654,21 +766,22 @@ hipError_t launch_apply(const StepArgs& a, hipStream_t s) {
     p.D = a.D;
     p.total_chunks = cp.total_chunks;
     p.slab_chunks = cp.slab_chunks;
-    p.nb = row_blocks(a.rows);
+    p.nslab = cp.nslab;
+    p.nb = apply_blocks(a.rows);
     p.idx = a.idx;
     p.r = a.r;
     p.c = a.c;
     p.rsum = reinterpret_cast<const float*>(a.ws + L.rsum);
-    p.nrsum = (int)((a.V + kVRowsPerBlock - 1) / kVRowsPerBlock);
+    p.nrsum = (int)((a.V + kFinRowsPerBlock - 1) / kFinRowsPerBlock);
     p.csum = reinterpret_cast<const float*>(a.ws + L.csum);
-    p.ncsum = (int)((a.D + kBlock - 1) / kBlock);
+    p.ncsum = (int)((a.D + kWave - 1) / kWave);
     p.V = a.V;
     p.inv_bias = a.inv_bias;
     p.inv_alpha = a.inv_alpha;
     p.eps_over_alpha = a.eps_over_alpha;
     p.status = reinterpret_cast<const int*>(a.ws + L.status);
     p.flag = reinterpret_cast<int*>(a.ws + L.flag);
-    const dim3 grid((unsigned)p.nb, (unsigned)cp.nslab);
+    const dim3 grid((unsigned)(p.nb * cp.nslab));
     const bool sparse = a.sparse;
     if (a.g_dtype == 0)
         return sparse ? apply_dispatch_w<float, true>(p, a.w_dtype, cp.m, grid, s)

@@ -11,13 +11,57 @@ namespace ember {
 
 constexpr int kWave = 64;           // CDNA wavefront width
 constexpr int kBlock = 256;         // threads per block: 4 waves
-constexpr int kMaxBlocks = 1024;    // row blocks of the statistics pass
+constexpr int kWaves = kBlock / kWave;
+
+// Tuning constants of the streaming kernels (compile-time).
+#ifndef EMBER_SLAB_CHUNKS
+#define EMBER_SLAB_CHUNKS 128       // 16-byte chunks of a row per block (2 KiB)
+#endif
+#ifndef EMBER_STATS_ROWS
+#define EMBER_STATS_ROWS 4          // rows in flight per wave, statistics pass
+#endif
+#ifndef EMBER_APPLY_ROWS
+#define EMBER_APPLY_ROWS 2          // rows in flight per wave, apply pass
+#endif
+#ifndef EMBER_APPLY_BATCHES
+#define EMBER_APPLY_BATCHES 4       // row batches per wave, apply pass
+#endif
+#ifndef EMBER_STATS_NT
+#define EMBER_STATS_NT 2            // gradient loads of the statistics pass: 0 cached,
+                                    // 1 non-temporal, 2 non-temporal except the last
+                                    // EMBER_STATS_KEEP_MB of rows (reused by apply)
+#endif
+#ifndef EMBER_STATS_KEEP_MB
+#define EMBER_STATS_KEEP_MB 192
+#endif
+#ifndef EMBER_APPLY_NT
+#define EMBER_APPLY_NT 1            // non-temporal gradient loads and weight stores in apply
+#endif
+#ifndef EMBER_STATS_INTERLEAVE
+#define EMBER_STATS_INTERLEAVE 0    // statistics pass: block b takes rows b, b + nb, ...
+                                    // (all blocks sweep G together), else a contiguous range
+#endif
+#ifndef EMBER_STATS_PIPE
+#define EMBER_STATS_PIPE 1          // statistics pass: issue the next batch's loads before
+                                    // reducing the current batch across lanes
+#endif
+#ifndef EMBER_SPARSE_ROWS_PER_BLOCK
+#define EMBER_SPARSE_ROWS_PER_BLOCK 32  // minimum gradient rows per block, sparse step
+#endif
+#ifndef EMBER_APPLY_WNT
+#define EMBER_APPLY_WNT 1           // non-temporal weight loads in apply
+#endif
+#ifndef EMBER_MAX_BLOCKS
+#define EMBER_MAX_BLOCKS 512        // row blocks of the statistics pass
+#endif
+
+constexpr int kSlabChunks = EMBER_SLAB_CHUNKS;
+constexpr int kStatsRows = EMBER_STATS_ROWS;
+constexpr int kApplyRows = EMBER_APPLY_ROWS;
+constexpr int kApplyBatches = EMBER_APPLY_BATCHES;
+constexpr int kMaxBlocks = EMBER_MAX_BLOCKS;
 constexpr int kRowsPerBlockMin = 8; // fewer rows than this per block: fewer blocks
-constexpr int kGroup = 16;          // partial rows summed per first-level column group
 constexpr int kVRowsPerThread = 4;  // rows per thread in the r pass
-constexpr int kVRowsPerBlock = kBlock * kVRowsPerThread;
-constexpr int kMaxAcc = 64;         // fp32 column accumulators per lane (one slab)
-constexpr int kSlabCols = 4096;     // columns per slab for both dtypes (64 lanes x 64 acc)
 
 // Status bits written by the sparse statistics pass.
 constexpr int kFlagRange = 1;
@@ -27,21 +71,33 @@ constexpr int kFlagDuplicate = 2;
 struct ColPlan {
     int epc;          // elements per 16-byte chunk of G: 4 (fp32) or 8 (bf16)
     int total_chunks; // ceil(D / epc)
-    int nslab;        // grid.y of the streaming kernels
+    int nslab;        // column slabs: blocks per row block of the streaming kernels
     int slab_chunks;  // chunks per slab (last slab may hold fewer)
-    int m;            // chunks per lane per slab, a power of two in 1..16
+    int m;            // chunks per lane per slab: 1 or 2 (kSlabChunks / 64)
 };
 
 // Row blocking of the statistics pass for `rows` gradient rows.  The block
-// count depends only on the row count, so results do not depend on the device.
-inline int row_blocks(int64_t rows) {
-    int64_t nb = (rows + kRowsPerBlockMin - 1) / kRowsPerBlockMin;
+// count depends only on the row count and the step kind, so results do not
+// depend on the device.  The sparse step uses fewer, fuller blocks: its few
+// thousand rows would otherwise produce more column partials than gradient.
+inline int row_blocks(int64_t rows, bool sparse = false) {
+    const int64_t per = sparse ? EMBER_SPARSE_ROWS_PER_BLOCK : kRowsPerBlockMin;
+    int64_t nb = (rows + per - 1) / per;
     if (nb < 1) nb = 1;
     if (nb > kMaxBlocks) nb = kMaxBlocks;
     return (int)nb;
 }
-inline int col_groups(int nb) { return (nb + kGroup - 1) / kGroup; }
-inline int nslab_for(int64_t D) { return (int)((D + kSlabCols - 1) / kSlabCols); }
+// Largest slab count over both gradient dtypes (fp32 has more chunks per row).
+inline int nslab_for(int64_t D) {
+    const int64_t chunks = (D + 3) / 4;
+    return (int)((chunks + kSlabChunks - 1) / kSlabChunks);
+}
+// Row blocks of the apply pass (any count gives the same bits).
+inline int apply_blocks(int64_t rows) {
+    const int64_t per = (int64_t)kWaves * kApplyRows * kApplyBatches;
+    int64_t nb = (rows + per - 1) / per;
+    return (int)(nb < 1 ? 1 : nb);
+}
 
 ColPlan col_plan(int64_t D, int g_dtype);
 
@@ -52,10 +108,9 @@ struct WsLayout {
     size_t slot;    // int32[V]: 1 + position in idx of a touched row, else 0
     size_t zero_end;// [0, zero_end) must be zero before the first step
     size_t rowpart; // float[nslab][V]: per-slab row sums of g^2
-    size_t rsum;    // float[ceil(V / kVRowsPerBlock)]: per-block sums of the new r
-    size_t csum;    // float[ceil(D / kBlock)]: per-block sums of the new c
+    size_t rsum;    // float[ceil(V / 4096)]: per-block sums of the new r
+    size_t csum;    // float[ceil(D / 64)]: per-block sums of the new c
     size_t p;       // float[row_blocks(V)][D]: per-block column sums of g^2
-    size_t p2;      // float[col_groups(row_blocks(V))][D]
     size_t total;
 };
 WsLayout ws_layout(int64_t V, int64_t D);
@@ -85,8 +140,7 @@ struct StepArgs {
 // Each launcher enqueues one kernel on `s` and returns hipGetLastError().
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
 hipError_t launch_stats(const StepArgs& a, hipStream_t s);
-hipError_t launch_finalize_rows(const StepArgs& a, hipStream_t s);
-hipError_t launch_finalize_cols(const StepArgs& a, hipStream_t s);
+hipError_t launch_finalize(const StepArgs& a, hipStream_t s);
 hipError_t launch_apply(const StepArgs& a, hipStream_t s);
 
 } // namespace ember

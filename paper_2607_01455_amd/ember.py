@@ -43,10 +43,10 @@ class _KernelStat(ctypes.Structure):
     _fields_ = [("name", ctypes.c_char_p), ("launches", ctypes.c_int64), ("total_ms", ctypes.c_double)]
 
 
-def _load() -> ctypes.CDLL:
-    if not os.path.exists(_LIB_PATH):
-        raise ImportError(f"{_LIB_PATH} is missing: build it with `python -m paper_2607_01455_amd.build`")
-    lib = ctypes.CDLL(_LIB_PATH)
+def _load(path: str = _LIB_PATH) -> ctypes.CDLL:
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build it with `python -m paper_2607_01455_amd.build`")
+    lib = ctypes.CDLL(path)
     vp, i64, f32, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_float, ctypes.c_int, ctypes.c_size_t
     lib.ember_workspace_bytes.argtypes = [i64, i64, ctypes.POINTER(sz)]
     lib.ember_init_state.argtypes = [vp, vp, i64, i64, vp, sz, vp]

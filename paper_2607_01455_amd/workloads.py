@@ -114,16 +114,19 @@ def make_sparse_batch(cfg: Config, step: int, seed: int = 0, device="cuda", shuf
     that occurs k times is the sum of k independent N(0, g_std) vectors, drawn
     here directly as sqrt(k) * N(0, g_std), which has the same distribution.
     """
-    g = _gen(device, seed, 1000 + step)
-    p = zipf_probs(cfg.V, device=device).float()
-    ids = torch.multinomial(p, cfg.batch_tokens, replacement=True, generator=g)
+    # ids on the CPU generator: its multinomial and randperm are reproducible
+    # for a given seed, which the device versions are not
+    gc = _gen("cpu", seed, 1000 + step)
+    p = zipf_probs(cfg.V).float()
+    ids = torch.multinomial(p, cfg.batch_tokens, replacement=True, generator=gc)
     uniq, counts = torch.unique(ids, sorted=True, return_counts=True)
     if shuffle:
-        uniq_perm = torch.randperm(uniq.numel(), generator=g, device=device)
-        uniq, counts = uniq[uniq_perm], counts[uniq_perm]
+        perm = torch.randperm(uniq.numel(), generator=gc)
+        uniq, counts = uniq[perm], counts[perm]
+    g = _gen(device, seed, 1000 + step)
     x = torch.randn(uniq.numel(), cfg.D, generator=g, device=device) * cfg.g_std
-    x *= counts.to(torch.float32).sqrt()[:, None]
-    return uniq.to(torch.int64).contiguous(), x.to(cfg.g_dtype)
+    x *= counts.to(device=device, dtype=torch.float32).sqrt()[:, None]
+    return uniq.to(device=device, dtype=torch.int64).contiguous(), x.to(cfg.g_dtype)
 
 
 def algorithmic_bytes(V: int, D: int, w_size: int, g_size: int, rows: int | None = None) -> int:

@@ -9,7 +9,10 @@ does not depend on W, so the chains cannot drift).  Tolerances:
              (rows without gradient, an all-zero gradient).
   fp32 W     |gpu - oracle| <= 1e-5 max(|oracle|, |W before the step|).
   bf16 W     at most 1 unit in the last place (the GPU rounds an fp32 result to
-             bf16, the oracle rounds its float64 result once).
+             bf16, the oracle rounds its float64 result once), or, where the
+             update cancels the weight to far below its previous magnitude, the
+             fp32-weight bound above: there the few-fp32-ulp error of the update
+             u is many bf16 ulps of the tiny result, for any fp32 evaluation.
   sparse     rows outside idx: W bit-identical to before the step.
 Small shapes are checked on every element; the full-size workloads (the
 shapes and launch configuration the benchmark times) on every state element
@@ -44,6 +47,10 @@ def host_bits(t: torch.Tensor) -> np.ndarray:
     return t.contiguous().cpu().numpy()
 
 
+def bf16_values(b: np.ndarray) -> np.ndarray:
+    return (b.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
 def ordered16(b: np.ndarray) -> np.ndarray:
     b = b.astype(np.int64)
     return np.where(b & 0x8000, 0x8000 - (b & 0x7FFF), 0x8000 + b)
@@ -53,7 +60,12 @@ def check_w(got: np.ndarray, want: np.ndarray, prev: np.ndarray, what: str) -> N
     if got.dtype == np.uint16:
         d = np.abs(ordered16(got) - ordered16(want))
         bad = d > 1
-        assert not bad.any(), f"{what}: {bad.sum()} bf16 elements differ by > 1 ulp (max {d.max()})"
+        if bad.any():
+            gv, wv, pv = (bf16_values(x[bad]) for x in (got, want, prev))
+            cancel_ok = np.abs(gv - wv) <= 1e-5 * np.maximum(np.abs(wv), np.abs(pv))
+            assert cancel_ok.all(), (
+                f"{what}: {(~cancel_ok).sum()} bf16 elements differ by > 1 ulp outside cancellation "
+                f"(max {d.max()} ulp); first: got {gv[~cancel_ok][:3]} want {wv[~cancel_ok][:3]} prev {pv[~cancel_ok][:3]}")
     else:
         tol = 1e-5 * np.maximum(np.abs(want), np.abs(prev))
         err = np.abs(got.astype(np.float64) - want.astype(np.float64))
@@ -328,6 +340,10 @@ def test_results_are_bitwise_reproducible(em):
                     G = wl.make_dense_grad(cfg, t, seed=10, device=DEV, scales=scales)
                     em.ember_step_dense(W, G, tab.r, tab.c, t, LR, B2, EPS, False, tab.ws)
             outs.append((host_bits(W), tab.r.cpu().numpy(), tab.c.cpu().numpy()))
+        if cfg.grad == "sparse_zipf":
+            a = wl.make_sparse_batch(cfg, 1, seed=10, device=DEV, shuffle=True)
+            b = wl.make_sparse_batch(cfg, 1, seed=10, device=DEV, shuffle=True)
+            assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1]), "input generator is not reproducible"
         for a, b in zip(outs[0], outs[1]):
             assert np.array_equal(a.view(np.uint8), b.view(np.uint8))
 
