@@ -28,7 +28,7 @@ METRIC = "Ember step ms + achieved HBM GB/s (% of peak) at V=128256, D=4096"
 PEAK_GBPS = 8000.0
 V, D = 128256, 4096
 KERNEL_SRC = os.path.join(ROOT, "paper_2607_01455_amd", "csrc", "ember_kernels.hip")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ember_apply_lmhead128k_traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ember_apply_lmhead128k_traffic.txt")
 
 
 def parse():
@@ -47,16 +47,23 @@ def kernel_source_hash() -> str:
 
 
 def traffic_for_current_kernel():
-    """HBM bytes per dense apply launch from committed PMC counters, if they were
+    """HBM bytes per dense apply launch from the committed PMC summary, if it was
     taken on the current kernel source (else None)."""
+    rec = {}
     try:
         with open(TRAFFIC_FILE) as f:
-            rec = json.load(f)
-    except (OSError, ValueError):
+            for line in f:
+                if "=" in line and not line.lstrip().startswith("#"):
+                    k, v = line.split("=", 1)
+                    rec[k.strip()] = v.strip()
+    except OSError:
         return None
     if rec.get("kernel_source_sha256_16") != kernel_source_hash():
         return None
-    return rec.get("bytes_per_launch")
+    try:
+        return int(rec["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def cpu_baseline(rows: int, steps: int = 2):
@@ -156,31 +163,24 @@ def main():
     step_bytes = dense_bytes + sum(sparse_bytes) / K
     value = step_bytes / (ms_step * 1e-3) / 1e9
 
-    # --- timed region B: the same steps with HIP events around every kernel --
-    ember.ember_profile_enable(True)
-    torch.cuda.synchronize()
-    tb0 = torch.cuda.Event(enable_timing=True)
-    tb1 = torch.cuda.Event(enable_timing=True)
-    tb0.record(stream)
-    for k in range(K):
-        head.step(W_head, grads[(Wm + K + k) % n_grads])
-        idx, Gr = batches[Wm + k]
-        emb.step_sparse_rows(W_emb, Gr, idx)
-    tb1.record(stream)
-    torch.cuda.synchronize()
-    ember.ember_profile_enable(False)
-    kstats = ember.ember_profile_collect()
-    ms_step_with_kernel_events = tb0.elapsed_time(tb1) / K
+    # --- timed region B: dense steps with HIP events around every kernel ------
+    def kernel_region(fn):
+        ember.ember_profile_enable(True)
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for k in range(K):
+            fn(k)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ember.ember_profile_enable(False)
+        return ember.ember_profile_collect(), e0.elapsed_time(e1) / K
 
-    # the dense apply pass: one launch per dense step and one per sparse step
-    # carry the same name; split them by launch order is not possible from the
-    # totals, so region C times the dense apply alone.
-    ember.ember_profile_enable(True)
-    for k in range(K):
-        head.step(W_head, grads[k % n_grads])
-    torch.cuda.synchronize()
-    ember.ember_profile_enable(False)
-    dstats = ember.ember_profile_collect()
+    dstats, dense_ms_events = kernel_region(lambda k: head.step(W_head, grads[(Wm + K + k) % n_grads]))
+    sstats, sparse_ms_events = kernel_region(lambda k: emb.step_sparse_rows(W_emb, batches[Wm + k][1], batches[Wm + k][0]))
+    if ember.ember_get_error(emb.ws) != ember.EMBER_OK:
+        raise RuntimeError("sparse step reported an index error")
     apply_launches, apply_ms = dstats["ember_apply"]
     apply_avg_ms = apply_ms / apply_launches
     apply_bytes = V * D * (2 + 2 * 2) + 4 * (V + D)
@@ -230,8 +230,11 @@ def main():
             "sparse_embedding": {"ms": round(sparse_ms, 4), "bytes": int(sum(sparse_bytes) / K),
                                  "GBps": round(sum(sparse_bytes) / K / (sparse_ms * 1e-3) / 1e9, 1)},
         },
-        "kernels_ms_avg": {k: round(v[1] / v[0], 5) for k, v in kstats.items()},
-        "ms_per_step_with_kernel_events": round(ms_step_with_kernel_events, 4),
+        "kernels_ms_avg": {
+            "dense": {k: round(v[1] / v[0], 5) for k, v in dstats.items()},
+            "sparse": {k: round(v[1] / v[0], 5) for k, v in sstats.items()},
+        },
+        "ms_with_kernel_events": {"dense": round(dense_ms_events, 4), "sparse": round(sparse_ms_events, 4)},
         "roofline": {
             "kernel": "ember_apply (dense LM-head step)",
             "bound": "hbm",

@@ -142,6 +142,22 @@ __device__ __forceinline__ void load_raw(const T* row, int64_t col, bool valid, 
 template <typename T, int N>
 __device__ __forceinline__ void decode(const Raw<T, N>& r, float (&x)[N]) { decode<T, N>(r.u, x); }
 
+// N fp32 values from a buffer padded to a multiple of 8 floats; zeros past D.
+template <int N>
+__device__ __forceinline__ void load_chunk_f32(const float* p, int64_t col, bool valid, int64_t D, float (&x)[N]) {
+#pragma unroll
+    for (int e = 0; e < N; ++e) x[e] = 0.0f;
+    if (!valid) return;
+#pragma unroll
+    for (int q = 0; q < N / 4; ++q) {
+        const float4 v = reinterpret_cast<const float4*>(p + col)[q];
+        x[4 * q] = v.x; x[4 * q + 1] = v.y; x[4 * q + 2] = v.z; x[4 * q + 3] = v.w;
+    }
+#pragma unroll
+    for (int e = 0; e < N; ++e)
+        if (col + e >= D) x[e] = 0.0f;
+}
+
 template <typename T, int N, bool NT>
 __device__ __forceinline__ void vstore(T* p, const float (&x)[N]) {
     constexpr int kWords = N * (int)sizeof(T) / 4;
@@ -403,7 +419,36 @@ struct FinParams {
     float one_minus_beta2;
     float* rsum;           // [ceil(V / kFinRowsPerBlock)]
     float* csum;           // [ncolblocks]
+    int* ticket;           // finished blocks; the last one derives the column factors
+    float* qa;             // [D] column factors sqrt(chat_j / s) / alpha_s
+    double inv_bias;
+    double inv_alpha;
 };
+
+// Run by the last block of the finalize pass, once every r, c and partial sum
+// of this step is stored: s = sqrt(mean(rhat) mean(chat)) from the per-block
+// sums in a fixed order, then the column factors qa_j = sqrt(chat_j / s) / alpha_s
+// that the apply pass multiplies by the row factor sqrt(rhat_i).
+__device__ void column_factors(const FinParams& a, int nrsum, double* s_lds) {
+    const int lane = threadIdx.x & (kWave - 1);
+    if (threadIdx.x < kWave) {
+        double sr = 0.0, sc = 0.0;
+        for (int k = lane; k < nrsum; k += kWave) sr += (double)a.rsum[k];
+        for (int k = lane; k < a.ncolblocks; k += kWave) sc += (double)a.csum[k];
+        sr = wave_sum(sr);
+        sc = wave_sum(sc);
+        if (lane == 0) {
+            const double mean_rhat = sr / (double)a.V * a.inv_bias;
+            const double mean_chat = sc / (double)a.D * a.inv_bias;
+            *s_lds = sqrt(mean_rhat * mean_chat);
+        }
+    }
+    __syncthreads();
+    const double s = *s_lds;
+    const double kq = s > 0.0 ? a.inv_bias / s : 0.0;
+    for (int64_t j = threadIdx.x; j < a.D; j += kFinThreads)
+        a.qa[j] = (float)(sqrt((double)a.c[j] * kq) * a.inv_alpha);
+}
 
 // Sum of one float per thread of a 1024-thread block: waves, then waves 0..15 in order.
 __device__ __forceinline__ float block_sum_1024(float v, float* lds16) {
@@ -419,14 +464,44 @@ __device__ __forceinline__ float block_sum_1024(float v, float* lds16) {
 }
 
 template <bool kSparse>
+__device__ __forceinline__ void finalize_body(const FinParams& a, int err, float (*part)[kWave], float* lds16);
+
+template <bool kSparse>
 __global__ __launch_bounds__(kFinThreads) void ember_finalize(FinParams a) {
     __shared__ float part[kFinWaves][kWave];
     __shared__ float lds16[kFinWaves];
-    const int lane = threadIdx.x & (kWave - 1);
-    const int wave = threadIdx.x / kWave;
+    __shared__ int last;
+    __shared__ double s_lds;
     const int err = kSparse ? *a.flag : 0;
     if (blockIdx.x == 0 && threadIdx.x == 0) *a.status = err;
+    finalize_body<kSparse>(a, err, part, lds16);
 
+    // Completion ticket: every wave waits until its own stores are complete in
+    // L2, then one thread counts the block with an agent-scope acquire-release
+    // atomic (one L2 write-back per block, which also covers the other waves'
+    // stores), and the block that completes the count derives the column
+    // factors from the stored state.  The ticket orders work; no value is
+    // accumulated through it.
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        __builtin_amdgcn_s_waitcnt(0);  // the write-back has completed
+        const int t = __hip_atomic_fetch_add(a.ticket, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        last = t == (int)gridDim.x - 1;
+    }
+    __syncthreads();
+    if (!last) return;
+    const int nrsum = (int)((a.V + kFinRowsPerBlock - 1) / kFinRowsPerBlock);
+    if (!err) column_factors(a, nrsum, &s_lds);
+    if (threadIdx.x == 0) *a.ticket = 0;
+}
+
+template <bool kSparse>
+__device__ __forceinline__ void finalize_body(const FinParams& a, int err, float (*part)[kWave], float* lds16) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
     if ((int)blockIdx.x < a.ncolblocks) {
         // 64 columns: wave w sums partial rows w, w + 16, ... in ascending order,
         // then the 16 wave sums are added in wave order.
@@ -504,12 +579,7 @@ struct ApplyParams {
     int nb;
     const int64_t* idx;   // sparse only
     const float* r;
-    const float* c;
-    const float* rsum;
-    int nrsum;
-    const float* csum;
-    int ncsum;
-    int64_t V;
+    const float* qa;      // [D] column factors sqrt(chat_j / s) / alpha_s
     double inv_bias;
     double inv_alpha;     // 1 / alpha_s, alpha_s = -lr (descent) or +lr (ascent)
     float eps_over_alpha; // eps / alpha_s
@@ -528,17 +598,6 @@ __global__ __launch_bounds__(kBlock) void ember_apply(ApplyParams a) {
     }
     if (a.inv_alpha == 0.0) return;   // lr == 0: every weight keeps its bits
 
-    // Normaliser s = sqrt(mean(rhat) mean(chat)) from the per-block sums, in a
-    // fixed order (identical in every wave of every block).
-    double sr = 0.0, sc = 0.0;
-    for (int k = lane; k < a.nrsum; k += kWave) sr += (double)a.rsum[k];
-    for (int k = lane; k < a.ncsum; k += kWave) sc += (double)a.csum[k];
-    sr = wave_sum(sr);
-    sc = wave_sum(sc);
-    const double mean_rhat = sr / (double)a.V * a.inv_bias;
-    const double mean_chat = sc / (double)a.D * a.inv_bias;
-    const double s = sqrt(mean_rhat * mean_chat);
-
     const int slab = (int)(blockIdx.x % (unsigned)a.nslab);
     // Row blocks in reverse order: the rows the statistics pass read last are
     // the likeliest still to sit in the last-level cache.
@@ -546,20 +605,13 @@ __global__ __launch_bounds__(kBlock) void ember_apply(ApplyParams a) {
     const int cbeg = slab * a.slab_chunks;
     const int cend = min(cbeg + a.slab_chunks, a.total_chunks);
 
-    // Column factors sqrt(chat_j / s) of this lane's columns, pre-divided by alpha_s.
-    const double kq = s > 0.0 ? a.inv_bias / s : 0.0;
+    // Column factors sqrt(chat_j / s) / alpha_s of this lane's columns, derived
+    // once per step by the finalize pass.
     float qa[M][EPC];
 #pragma unroll
     for (int m = 0; m < M; ++m) {
         const int ch = cbeg + lane + kWave * m;
-#pragma unroll
-        for (int e = 0; e < EPC; ++e) {
-            const int64_t col = (int64_t)ch * EPC + e;
-            float q = 0.0f;
-            if (ch < cend && col < a.D)
-                q = (float)(sqrt((double)a.c[col] * kq) * a.inv_alpha);
-            qa[m][e] = q;
-        }
+        load_chunk_f32<EPC>(a.qa, (int64_t)ch * EPC, ch < cend, a.D, qa[m]);
     }
     const float epsa = a.eps_over_alpha;
     const float ibias = (float)a.inv_bias;
@@ -668,10 +720,13 @@ WsLayout ws_layout(int64_t V, int64_t D) {
     size_t off = 0;
     L.flag = off;
     L.status = off + 4;
-    off = align256(8);
+    L.ticket = off + 8;
+    off = align256(12);
     L.slot = off;
     off = align256(off + (size_t)V * 4);
     L.zero_end = off;
+    L.qa = off;
+    off = align256(off + (size_t)((D + 7) / 8 * 8) * 4);
     L.rowpart = off;
     off = align256(off + (size_t)nslab_for(D) * (size_t)V * 4);
     L.rsum = off;
@@ -745,6 +800,10 @@ hipError_t launch_finalize(const StepArgs& a, hipStream_t s) {
     p.one_minus_beta2 = a.one_minus_beta2;
     p.rsum = reinterpret_cast<float*>(a.ws + L.rsum);
     p.csum = reinterpret_cast<float*>(a.ws + L.csum);
+    p.ticket = reinterpret_cast<int*>(a.ws + L.ticket);
+    p.qa = reinterpret_cast<float*>(a.ws + L.qa);
+    p.inv_bias = a.inv_bias;
+    p.inv_alpha = a.inv_alpha;
     const int nvb = (int)((a.V + kFinRowsPerBlock - 1) / kFinRowsPerBlock);
     const dim3 grid((unsigned)(p.ncolblocks + nvb));
     if (a.sparse)
@@ -767,15 +826,10 @@ hipError_t launch_apply(const StepArgs& a, hipStream_t s) {
     p.total_chunks = cp.total_chunks;
     p.slab_chunks = cp.slab_chunks;
     p.nslab = cp.nslab;
-    p.nb = apply_blocks(a.rows);
+    p.nb = apply_blocks(a.rows, a.sparse);
     p.idx = a.idx;
     p.r = a.r;
-    p.c = a.c;
-    p.rsum = reinterpret_cast<const float*>(a.ws + L.rsum);
-    p.nrsum = (int)((a.V + kFinRowsPerBlock - 1) / kFinRowsPerBlock);
-    p.csum = reinterpret_cast<const float*>(a.ws + L.csum);
-    p.ncsum = (int)((a.D + kWave - 1) / kWave);
-    p.V = a.V;
+    p.qa = reinterpret_cast<const float*>(a.ws + L.qa);
     p.inv_bias = a.inv_bias;
     p.inv_alpha = a.inv_alpha;
     p.eps_over_alpha = a.eps_over_alpha;

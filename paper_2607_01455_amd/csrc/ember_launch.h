@@ -24,7 +24,7 @@ constexpr int kWaves = kBlock / kWave;
 #define EMBER_APPLY_ROWS 2          // rows in flight per wave, apply pass
 #endif
 #ifndef EMBER_APPLY_BATCHES
-#define EMBER_APPLY_BATCHES 4       // row batches per wave, apply pass
+#define EMBER_APPLY_BATCHES 1       // row batches per wave, apply pass
 #endif
 #ifndef EMBER_STATS_NT
 #define EMBER_STATS_NT 2            // gradient loads of the statistics pass: 0 cached,
@@ -48,11 +48,14 @@ constexpr int kWaves = kBlock / kWave;
 #ifndef EMBER_SPARSE_ROWS_PER_BLOCK
 #define EMBER_SPARSE_ROWS_PER_BLOCK 32  // minimum gradient rows per block, sparse step
 #endif
+#ifndef EMBER_SPARSE_APPLY_BATCHES
+#define EMBER_SPARSE_APPLY_BATCHES 1  // row batches per wave, apply pass of the sparse step
+#endif
 #ifndef EMBER_APPLY_WNT
 #define EMBER_APPLY_WNT 1           // non-temporal weight loads in apply
 #endif
 #ifndef EMBER_MAX_BLOCKS
-#define EMBER_MAX_BLOCKS 512        // row blocks of the statistics pass
+#define EMBER_MAX_BLOCKS 384        // row blocks of the statistics pass
 #endif
 
 constexpr int kSlabChunks = EMBER_SLAB_CHUNKS;
@@ -92,9 +95,10 @@ inline int nslab_for(int64_t D) {
     const int64_t chunks = (D + 3) / 4;
     return (int)((chunks + kSlabChunks - 1) / kSlabChunks);
 }
-// Row blocks of the apply pass (any count gives the same bits).
-inline int apply_blocks(int64_t rows) {
-    const int64_t per = (int64_t)kWaves * kApplyRows * kApplyBatches;
+// Row blocks of the apply pass (any count gives the same bits).  The sparse
+// step has few rows, so its blocks are smaller to spread them over the chip.
+inline int apply_blocks(int64_t rows, bool sparse = false) {
+    const int64_t per = (int64_t)kWaves * kApplyRows * (sparse ? EMBER_SPARSE_APPLY_BATCHES : kApplyBatches);
     int64_t nb = (rows + per - 1) / per;
     return (int)(nb < 1 ? 1 : nb);
 }
@@ -105,8 +109,10 @@ ColPlan col_plan(int64_t D, int g_dtype);
 struct WsLayout {
     size_t flag;    // int32: index-error bits set by the sparse statistics pass
     size_t status;  // int32: status of the last step (read by ember_get_error)
+    size_t ticket;  // int32: blocks of the finalize pass that have finished
     size_t slot;    // int32[V]: 1 + position in idx of a touched row, else 0
     size_t zero_end;// [0, zero_end) must be zero before the first step
+    size_t qa;      // float[D rounded up to 8]: sqrt(chat_j / s) / alpha_s
     size_t rowpart; // float[nslab][V]: per-slab row sums of g^2
     size_t rsum;    // float[ceil(V / 4096)]: per-block sums of the new r
     size_t csum;    // float[ceil(D / 64)]: per-block sums of the new c
