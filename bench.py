@@ -11,8 +11,8 @@ timed region and resident in HBM.
 Prints one JSON line: whole-step throughput in algorithmic GB/s (the bytes
 the method must move, see paper_2607_01455_amd.workloads.algorithmic_bytes),
 ms per step, per-part times, the roofline of the dominant kernel (the dense
-apply pass, timed with HIP events around each launch), a plain device copy as
-a practical bandwidth ceiling, and the CPU oracle timed on a sample.
+apply pass, timed with HIP events around each launch), torch's device copy
+for reference, the other table shapes, and the CPU oracle timed on a sample.
 """
 import argparse
 import hashlib
@@ -37,7 +37,8 @@ def parse():
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=2)
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-rows", type=int, default=16384, help="rows of the oracle's sample")
+    p.add_argument("--cpu-rows", type=int, default=65536, help="rows of the oracle's sample")
+    p.add_argument("--no-other-configs", action="store_true")
     return p.parse_args()
 
 
@@ -66,7 +67,7 @@ def traffic_for_current_kernel():
         return None
 
 
-def cpu_baseline(rows: int, steps: int = 2):
+def cpu_baseline(rows: int, steps: int = 3):
     """The oracle on the first `rows` rows of the LM-head table (dense, bf16)."""
     import numpy as np
     import torch
@@ -91,6 +92,37 @@ def cpu_baseline(rows: int, steps: int = 2):
     return {"value": round(gbps, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
             "sample": f"dense bf16 step on the first {rows} of {V} LM-head rows x {D}, "
                       f"{steps} steps, float64 C oracle, single thread; {sec * 1e3:.0f} ms/step"}
+
+
+def other_configs(ember, wl, torch, dev, K):
+    """ms/step and algorithmic GB/s of the dense configurations other than the
+    headline one, each timed over K steps after 2 warm-up steps."""
+    out = {}
+    for name in ("tiny", "lmhead32k", "tied152k", "wide262k"):
+        cfg = wl.CONFIGS[name]
+        W = wl.make_weights(cfg, seed=41, device=dev)
+        sc = wl.row_scales(cfg, 41, dev)
+        grads = [wl.make_dense_grad(cfg, t + 1, seed=41, device=dev, scales=sc) for t in range(2)]
+        tab = ember.EmberTable(cfg.V, cfg.D, device=dev)
+        for k in range(2):
+            tab.step(W, grads[k % 2])
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for k in range(K):
+            tab.step(W, grads[k % 2])
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / K
+        ws, gs = W.element_size(), grads[0].element_size()
+        nbytes = wl.algorithmic_bytes(cfg.V, cfg.D, ws, gs)
+        out[name] = {"V": cfg.V, "D": cfg.D, "dtype_w": str(cfg.w_dtype).replace("torch.", ""),
+                     "ms": round(ms, 4), "GBps": round(nbytes / (ms * 1e-3) / 1e9, 1),
+                     "pct_of_peak": round(100.0 * nbytes / (ms * 1e-3) / 1e9 / PEAK_GBPS, 2)}
+        del W, grads, tab
+        torch.cuda.empty_cache()
+    return out
 
 
 def main():
@@ -246,9 +278,14 @@ def main():
             "avg_launch_ms": round(apply_avg_ms, 5),
             "algorithmic_bytes_per_launch": apply_bytes,
         },
-        "copy_ceiling_GBps": round(copy_gbps, 1),
+        "torch_device_copy_GBps": round(copy_gbps, 1),
+        "other_configs": None,
         "cpu_baseline": None,
     }
+    if not args.no_other_configs:
+        del W_head, W_emb, grads, batches, head, emb
+        torch.cuda.empty_cache()
+        out["other_configs"] = other_configs(ember, wl, torch, dev, K)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.cpu_rows)
     print(json.dumps(out), flush=True)
