@@ -71,7 +71,7 @@ typedef enum {
 
 /* Largest supported V (row indices are kept in 31 bits) and D. */
 #define EMBER_MAX_V ((int64_t)0x7FFFFFFE)
-#define EMBER_MAX_D ((int64_t)(1 << 24))
+#define EMBER_MAX_D ((int64_t)(1 << 22))
 
 /*
  * Workspace size for a V x D table, valid for both the dense and the sparse

@@ -183,6 +183,31 @@ __device__ __forceinline__ void store_chunk(T* row, int64_t col, int64_t D, cons
     }
 }
 
+// Stores and loads at agent scope: coherent across the XCDs' L2 caches without
+// an L2 write-back, for the few values one block hands to another inside a
+// launch.
+__device__ __forceinline__ void st_agent(float* p, float v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_agent(const float* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Completion ticket of a block: every wave waits until its own stores have
+// completed, then one thread counts the block.  Returns true (in every thread)
+// for the block that completes the count of `total`.  The ticket orders work;
+// no value is accumulated through it.
+__device__ __forceinline__ bool block_ticket(int* ticket, int total, int* lds_flag) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const int t = __hip_atomic_fetch_add(ticket, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        *lds_flag = t == total - 1;
+    }
+    __syncthreads();
+    return *lds_flag != 0;
+}
+
 // ---------------------------------------------------------------------------
 // fixed-order reductions
 // ---------------------------------------------------------------------------
@@ -433,8 +458,8 @@ __device__ void column_factors(const FinParams& a, int nrsum, double* s_lds) {
     const int lane = threadIdx.x & (kWave - 1);
     if (threadIdx.x < kWave) {
         double sr = 0.0, sc = 0.0;
-        for (int k = lane; k < nrsum; k += kWave) sr += (double)a.rsum[k];
-        for (int k = lane; k < a.ncolblocks; k += kWave) sc += (double)a.csum[k];
+        for (int k = lane; k < nrsum; k += kWave) sr += (double)ld_agent(a.rsum + k);
+        for (int k = lane; k < a.ncolblocks; k += kWave) sc += (double)ld_agent(a.csum + k);
         sr = wave_sum(sr);
         sc = wave_sum(sc);
         if (lane == 0) {
@@ -447,7 +472,7 @@ __device__ void column_factors(const FinParams& a, int nrsum, double* s_lds) {
     const double s = *s_lds;
     const double kq = s > 0.0 ? a.inv_bias / s : 0.0;
     for (int64_t j = threadIdx.x; j < a.D; j += kFinThreads)
-        a.qa[j] = (float)(sqrt((double)a.c[j] * kq) * a.inv_alpha);
+        a.qa[j] = (float)(sqrt((double)ld_agent(a.c + j) * kq) * a.inv_alpha);
 }
 
 // Sum of one float per thread of a 1024-thread block: waves, then waves 0..15 in order.
@@ -476,23 +501,9 @@ __global__ __launch_bounds__(kFinThreads) void ember_finalize(FinParams a) {
     if (blockIdx.x == 0 && threadIdx.x == 0) *a.status = err;
     finalize_body<kSparse>(a, err, part, lds16);
 
-    // Completion ticket: every wave waits until its own stores are complete in
-    // L2, then one thread counts the block with an agent-scope acquire-release
-    // atomic (one L2 write-back per block, which also covers the other waves'
-    // stores), and the block that completes the count derives the column
-    // factors from the stored state.  The ticket orders work; no value is
-    // accumulated through it.
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-        __builtin_amdgcn_s_waitcnt(0);  // the write-back has completed
-        const int t = __hip_atomic_fetch_add(a.ticket, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-        last = t == (int)gridDim.x - 1;
-    }
-    __syncthreads();
-    if (!last) return;
+    // The block that finishes last derives the column factors from the stored
+    // state (c and the per-block sums are written with agent-scope stores).
+    if (!block_ticket(a.ticket, (int)gridDim.x, &last)) return;
     const int nrsum = (int)((a.V + kFinRowsPerBlock - 1) / kFinRowsPerBlock);
     if (!err) column_factors(a, nrsum, &s_lds);
     if (threadIdx.x == 0) *a.ticket = 0;
@@ -522,10 +533,10 @@ __device__ __forceinline__ void finalize_body(const FinParams& a, int err, float
             if (jv && !err) {
                 const float mean = (float)((double)colsum / (double)a.V);
                 cn = fmaf(a.beta2, a.c[j], a.one_minus_beta2 * mean);
-                a.c[j] = cn;
+                st_agent(a.c + j, cn);
             }
             cn = wave_sum(cn);
-            if (lane == 0) a.csum[blockIdx.x] = cn;
+            if (lane == 0) st_agent(a.csum + blockIdx.x, cn);
         }
         return;
     }
@@ -559,7 +570,7 @@ __device__ __forceinline__ void finalize_body(const FinParams& a, int err, float
         psum += rn;
     }
     const float tot = block_sum_1024(psum, lds16);
-    if (threadIdx.x == 0) a.rsum[vb] = tot;
+    if (threadIdx.x == 0) st_agent(a.rsum + vb, tot);
 }
 
 // ---------------------------------------------------------------------------

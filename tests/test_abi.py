@@ -101,7 +101,7 @@ def _sparse(em, **kw):
 
 @pytest.mark.parametrize("kw,status", [
     (dict(V=0), "SHAPE"), (dict(D=0), "SHAPE"), (dict(ldw=63), "SHAPE"), (dict(ldg=32), "SHAPE"),
-    (dict(V=2 ** 31), "SHAPE"),
+    (dict(V=2 ** 31), "SHAPE"), (dict(D=2 ** 22 + 8, ldw=2 ** 22 + 8, ldg=2 ** 22 + 8), "SHAPE"),
     (dict(W=None), "ARG"), (dict(G=None), "ARG"), (dict(r=None), "ARG"), (dict(c=None), "ARG"),
     (dict(ws=None), "ARG"),
     (dict(W=W_ + 8), "ALIGN"), (dict(G=G_ + 2), "ALIGN"), (dict(ldw=68, D=60), "ALIGN"),
