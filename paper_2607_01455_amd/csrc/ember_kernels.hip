@@ -471,8 +471,23 @@ __device__ void column_factors(const FinParams& a, int nrsum, double* s_lds) {
     __syncthreads();
     const double s = *s_lds;
     const double kq = s > 0.0 ? a.inv_bias / s : 0.0;
-    for (int64_t j = threadIdx.x; j < a.D; j += kFinThreads)
-        a.qa[j] = (float)(sqrt((double)ld_agent(a.c + j) * kq) * a.inv_alpha);
+    // all loads of a thread first (they are coherent, i.e. uncached, loads),
+    // then sqrt(c_j * kq) / alpha_s, kq = 1 / (bias s): the product in f64
+    // (kq alone may exceed the fp32 range for tiny gradients), the root in fp32
+    const float ia = (float)a.inv_alpha;
+    for (int64_t j0 = 0; j0 < a.D; j0 += 4 * kFinThreads) {
+        float cv[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int64_t j = j0 + u * kFinThreads + threadIdx.x;
+            cv[u] = j < a.D ? ld_agent(a.c + j) : 0.0f;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int64_t j = j0 + u * kFinThreads + threadIdx.x;
+            if (j < a.D) a.qa[j] = sqrtf((float)((double)cv[u] * kq)) * ia;
+        }
+    }
 }
 
 // Sum of one float per thread of a 1024-thread block: waves, then waves 0..15 in order.

@@ -208,6 +208,13 @@ def test_maximize_and_hyperparameters(em):
     dense_lockstep(em, cfg, seed=3, maximize=True, lr=3e-4, beta2=0.9, eps=1e-6)
 
 
+@pytest.mark.parametrize("scale,eps", [(1e-15, 0.0), (1e-15, 1e-8), (1e10, 1e-8), (1e10, 0.0)])
+def test_extreme_gradient_scales(em, scale, eps):
+    # tiny gradients drive r and c into fp32 subnormals; huge ones test range
+    cfg = wl.Config("scale", 900, 192, torch.float32, torch.float32, 3, "loguniform_rows", g_std=scale)
+    dense_lockstep(em, cfg, seed=21, eps=eps)
+
+
 def test_large_step_counter(em):
     # bias correction ~ 1 late in training: start the counter high
     cfg = wl.Config("late", 600, 512, torch.bfloat16, torch.bfloat16, 2, "normal")
