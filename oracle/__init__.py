@@ -45,7 +45,7 @@ def _load():
     lib = ctypes.CDLL(_LIB)
     vp, i64, f32, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_float, ctypes.c_int
     lib.ember_oracle_step.argtypes = [vp, i32, i64, vp, i32, i64, vp, i64,
-                                      vp, vp, i64, i64, i64, f32, f32, f32, i32, vp, i64]
+                                      vp, vp, i64, i64, i64, f32, f32, f32, i32, vp, i64, i32]
     lib.ember_oracle_step.restype = i32
     lib.ember_oracle_bf16_to_f64.argtypes = [ctypes.c_uint16]
     lib.ember_oracle_bf16_to_f64.restype = ctypes.c_double
@@ -71,23 +71,30 @@ def _ld(a: np.ndarray) -> int:
     return a.strides[0] // a.itemsize
 
 
-def step(W: np.ndarray, G: np.ndarray, r: np.ndarray, c: np.ndarray, t: int,
+def step(W: np.ndarray, G: np.ndarray, r: np.ndarray, c: np.ndarray | None, t: int,
          lr: float = 1e-3, beta2: float = 0.999, eps: float = 1e-8,
          maximize: bool = False, idx: np.ndarray | None = None,
-         w_rows: np.ndarray | None = None) -> int:
+         w_rows: np.ndarray | None = None, row_only: bool = False) -> int:
     """One Ember step, in place on W, r and c.  Returns the oracle's status.
 
     ``idx`` (int64) selects the sparse-row form: G then holds ``len(idx)``
     rows, row k being the gradient of W's row ``idx[k]``.  ``w_rows``
     (strictly increasing int64) restricts which rows of W are written; the
-    state is always updated in full.
+    state is always updated in full.  ``row_only`` selects row-only Ember
+    (c is then unused and may be None).
     """
     lib = _load()
     V, D = W.shape
-    if r.dtype != np.float32 or c.dtype != np.float32 or r.shape != (V,) or c.shape != (D,):
-        raise ValueError("r must be float32[V] and c float32[D]")
-    if not (r.flags.c_contiguous and c.flags.c_contiguous):
-        raise ValueError("r and c must be contiguous")
+    if r.dtype != np.float32 or r.shape != (V,) or not r.flags.c_contiguous:
+        raise ValueError("r must be contiguous float32[V]")
+    if c is None:
+        if not row_only:
+            raise ValueError("c is required unless row_only")
+        c_ptr = None
+    else:
+        if c.dtype != np.float32 or c.shape != (D,) or not c.flags.c_contiguous:
+            raise ValueError("c must be contiguous float32[D]")
+        c_ptr = c.ctypes.data
     if idx is None:
         if G.shape != (V, D):
             raise ValueError("dense G must have W's shape")
@@ -106,9 +113,9 @@ def step(W: np.ndarray, G: np.ndarray, r: np.ndarray, c: np.ndarray, t: int,
     g_ld = _ld(G) if G.shape[0] > 0 else D
     return lib.ember_oracle_step(W.ctypes.data, _dtype_code(W), _ld(W),
                                  g_ptr, _dtype_code(G), g_ld, idx_ptr, n_idx,
-                                 r.ctypes.data, c.ctypes.data, V, D, int(t),
+                                 r.ctypes.data, c_ptr, V, D, int(t),
                                  float(lr), float(beta2), float(eps), int(bool(maximize)),
-                                 wr_ptr, n_wr)
+                                 wr_ptr, n_wr, int(bool(row_only)))
 
 
 def bf16_to_f64(bits: int) -> float:

@@ -37,6 +37,14 @@
  *     the loops below skip them without changing a bit.
  *   - idx must hold unique values in [0, V); otherwise the call fails and
  *     modifies nothing.
+ *
+ * Row-only Ember (row_only = 1).  Section 2.1 describes a variant that keeps
+ * only the V row statistics, bias-corrects them and divides each row's
+ * gradient by their square root (the ablation table lists it with state V);
+ * no formula is printed.  Reading taken here: the row statistic and bias
+ * correction of Algorithm 1 unchanged, vtil_ij = rhat_i (no column factor and
+ * no normaliser, since rhat already has the units of g^2), and the same update
+ * theta +/- alpha g / (sqrt(vtil) + eps).  c is neither read nor written.
  */
 #include <math.h>
 #include <stdint.h>
@@ -127,11 +135,11 @@ int ember_oracle_step(void* W, int w_dtype, int64_t ldw,
                       const int64_t* idx, int64_t n_idx,
                       float* r, float* c, int64_t V, int64_t D, int64_t t,
                       float lr, float beta2, float eps, int maximize,
-                      const int64_t* w_rows, int64_t n_w_rows)
+                      const int64_t* w_rows, int64_t n_w_rows, int row_only)
 {
     if (V < 1 || D < 1 || ldw < D || ldg < D || t < 1)
         return ORACLE_BAD_ARG;
-    if (!W || !r || !c || (!G && (idx == NULL || n_idx > 0)))
+    if (!W || !r || (!c && !row_only) || (!G && (idx == NULL || n_idx > 0)))
         return ORACLE_BAD_ARG;
     if ((w_dtype != ORACLE_F32 && w_dtype != ORACLE_BF16) ||
         (g_dtype != ORACLE_F32 && g_dtype != ORACLE_BF16))
@@ -189,29 +197,34 @@ int ember_oracle_step(void* W, int w_dtype, int64_t ldw,
 
     /* Column second moment: c_j <- beta2 c_j + (1-beta2) mean_i g_ij^2,
      * summing rows in ascending row order. */
-    for (int64_t i = 0; i < V; ++i) {
-        if (grow[i] < 0)
-            continue;
-        for (int64_t j = 0; j < D; ++j) {
-            double g = load_elem(G, g_dtype, grow[i] * ldg + j);
-            colsum[j] += g * g;
+    if (!row_only) {
+        for (int64_t i = 0; i < V; ++i) {
+            if (grow[i] < 0)
+                continue;
+            for (int64_t j = 0; j < D; ++j) {
+                double g = load_elem(G, g_dtype, grow[i] * ldg + j);
+                colsum[j] += g * g;
+            }
         }
-    }
-    for (int64_t j = 0; j < D; ++j) {
-        double mean_i = colsum[j] / (double)V;
-        c[j] = (float)(b2 * (double)c[j] + one_minus_b2 * mean_i);
+        for (int64_t j = 0; j < D; ++j) {
+            double mean_i = colsum[j] / (double)V;
+            c[j] = (float)(b2 * (double)c[j] + one_minus_b2 * mean_i);
+        }
     }
 
     /* Bias correction, from the fp32-stored state. */
     const double bias = 1.0 - pow(b2, (double)t);
 
     /* Geometric-mean normaliser s = sqrt(mean(rhat) mean(chat)). */
-    double sum_rhat = 0.0, sum_chat = 0.0;
-    for (int64_t i = 0; i < V; ++i)
-        sum_rhat += (double)r[i] / bias;
-    for (int64_t j = 0; j < D; ++j)
-        sum_chat += (double)c[j] / bias;
-    const double s = sqrt((sum_rhat / (double)V) * (sum_chat / (double)D));
+    double s = 0.0;
+    if (!row_only) {
+        double sum_rhat = 0.0, sum_chat = 0.0;
+        for (int64_t i = 0; i < V; ++i)
+            sum_rhat += (double)r[i] / bias;
+        for (int64_t j = 0; j < D; ++j)
+            sum_chat += (double)c[j] / bias;
+        s = sqrt((sum_rhat / (double)V) * (sum_chat / (double)D));
+    }
 
     /* Update with the factored preconditioner vtil_ij = rhat_i chat_j / s. */
     const double alpha = (double)lr;
@@ -226,8 +239,13 @@ int ember_oracle_step(void* W, int w_dtype, int64_t ldw,
             double g = load_elem(G, g_dtype, grow[i] * ldg + j);
             if (g == 0.0 || alpha == 0.0)
                 continue;
-            const double chat = (double)c[j] / bias;
-            const double vtil = (s > 0.0) ? rhat * chat / s : 0.0;
+            double vtil;
+            if (row_only) {
+                vtil = rhat;
+            } else {
+                const double chat = (double)c[j] / bias;
+                vtil = (s > 0.0) ? rhat * chat / s : 0.0;
+            }
             const double u = alpha * g / (sqrt(vtil) + e);
             const double w = load_elem(W, w_dtype, i * ldw + j);
             store_elem(W, w_dtype, i * ldw + j, maximize ? w + u : w - u);

@@ -441,3 +441,100 @@ def test_row_update_scale_is_independent_of_token_frequency():
             raw += np.sqrt((G.astype(np.float64) ** 2).mean(1))
     assert raw.max() / raw.min() > 100
     assert upd.max() / upd.min() < 1.5
+
+
+# ---------------------------------------------------------------------------
+# Row-only Ember (Section 2.1 and the ablation table; reading: vtil_ij = rhat_i)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("eps", [0.0, 1e-8])
+def test_row_only_worked_2x2(eps):
+    gd = _golden_2x2()
+    beta2 = float(gd["beta2"][0])
+    lr = 1e-3
+    r = np.zeros(2, np.float32)
+    c = np.full(2, 7.0, np.float32)                      # must stay untouched
+    for t, gkey, rkey, vkey in ((1, "G1", "r1", "vrow1"), (2, "G2", "r2", "vrow2")):
+        G = np.array([float(x) for x in gd[gkey]], np.float32).reshape(2, 2)
+        W = np.zeros((2, 2), np.float32)
+        assert oracle.step(W, G, r, c, t, lr=lr, beta2=beta2, eps=eps, maximize=True, row_only=True) == 0
+        assert r.tolist() == [float(x) for x in gd[rkey]]
+        assert c.tolist() == [7.0, 7.0]
+        for k in range(4):
+            g = float(gd[gkey][k])
+            want = lr * g / (math.sqrt(float(gd[vkey][k // 2])) + eps)
+            got = float(W.reshape(-1)[k])
+            assert abs(got - want) <= 1e-7 * abs(want), (t, k, got, want)
+
+
+def _row_only_updates(grads, shape, lr=1e-3, beta2=B2_F32, eps=1e-8):
+    r = np.zeros(shape[0], np.float32)
+    ups = []
+    for t, g in enumerate(grads, 1):
+        W = np.zeros(shape, np.float32)
+        assert oracle.step(W, g, r, None, t, lr=lr, beta2=beta2, eps=eps, row_only=True) == 0
+        ups.append(W.astype(np.float64))
+    return ups
+
+
+@pytest.mark.parametrize("shape", [(9, 1), (7, 16)])
+def test_row_only_equal_magnitude_rows_equal_adam_beta1_zero(shape):
+    # |g_ij| constant along each row: mean_j g^2 = g_ij^2, so the row statistic is
+    # Adam's elementwise second moment and row-only Ember is Adam with beta1 = 0.
+    rng = np.random.default_rng(18)
+    V, D = shape
+    grads = []
+    for _ in range(5):
+        x = rng.uniform(0.1, 3, (V, 1)) * rng.uniform(0.5, 2)
+        grads.append((x * rng.choice([-1.0, 1.0], (V, D))).astype(np.float32))
+    for a, b in zip(_adam_updates(grads, 1e-3, B2_F32, 1e-8, shape), _row_only_updates(grads, shape)):
+        np.testing.assert_allclose(b, a, rtol=1e-6, atol=0)
+
+
+def test_row_only_equals_canonical_when_columns_are_flat():
+    # g_ij^2 = x_i^2 for every j: every column statistic is the same number, so
+    # s = chat_j and the canonical preconditioner reduces to rhat_i.
+    rng = np.random.default_rng(19)
+    V, D = 12, 10
+    r1, r2 = np.zeros(V, np.float32), np.zeros(V, np.float32)
+    c = np.zeros(D, np.float32)
+    for t in range(1, 6):
+        x = rng.uniform(0.1, 3, (V, 1))
+        G = (x * rng.choice([-1.0, 1.0], (V, D))).astype(np.float32)
+        Wa, Wb = np.zeros((V, D), np.float32), np.zeros((V, D), np.float32)
+        assert oracle.step(Wa, G, r1, c, t) == 0
+        assert oracle.step(Wb, G, r2, None, t, row_only=True) == 0
+        assert np.array_equal(r1, r2)
+        assert np.all(c == c[0])
+        np.testing.assert_allclose(Wb, Wa, rtol=1e-6, atol=0)
+
+
+def test_row_only_sparse_equals_dense_with_zero_rows_bitwise():
+    rng = np.random.default_rng(20)
+    V, D, n = 30, 16, 9
+    idx = rng.permutation(V)[:n].astype(np.int64)
+    W0 = (rng.standard_normal((V, D)) * 0.02).astype(np.float32)
+    r0 = rng.uniform(0, 1e-6, V).astype(np.float32)
+    Grows = (rng.standard_normal((n, D)) * 1e-3).astype(np.float32)
+    Gd = np.zeros((V, D), np.float32)
+    Gd[idx] = Grows
+    Ws, rs = W0.copy(), r0.copy()
+    Wd, rd = W0.copy(), r0.copy()
+    assert oracle.step(Ws, Grows, rs, None, 4, idx=idx, row_only=True) == 0
+    assert oracle.step(Wd, Gd, rd, None, 4, row_only=True) == 0
+    assert np.array_equal(Ws.view(np.uint32), Wd.view(np.uint32))
+    assert np.array_equal(rs, rd)
+    untouched = np.setdiff1d(np.arange(V), idx)
+    assert np.array_equal(rs[untouched], np.float32(B2_F32) * r0[untouched])
+    assert np.array_equal(Ws[untouched], W0[untouched])
+
+
+def test_row_only_zero_gradient_is_bitwise():
+    rng = np.random.default_rng(21)
+    V, D = 8, 6
+    W = (rng.standard_normal((V, D)) * 0.02).astype(np.float32)
+    r = rng.uniform(0, 1, V).astype(np.float32)
+    W0, r0 = W.copy(), r.copy()
+    assert oracle.step(W, np.zeros((V, D), np.float32), r, None, 3, row_only=True) == 0
+    assert np.array_equal(W, W0)
+    assert np.array_equal(r, np.float32(B2_F32) * r0)
