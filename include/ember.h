@@ -74,8 +74,8 @@ typedef enum {
 #define EMBER_MAX_D ((int64_t)(1 << 22))
 
 /*
- * Workspace size for a V x D table, valid for both the dense and the sparse
- * step.  The workspace holds the per-block partial sums of the fixed-order
+ * Workspace size for a V x D table, valid for every step (dense, sparse,
+ * canonical and row-only).  The workspace holds the per-block partial sums of the fixed-order
  * reductions, a V-entry row-slot table used by the sparse step, and a status
  * word.  It is caller-allocated device memory, 256-byte aligned, and must be
  * initialised once by ember_init_state before its first step.
@@ -129,6 +129,48 @@ int ember_step_sparse_rows(void* W, int w_dtype, int64_t ldw,
                            float* r, float* c, int64_t V, int64_t D, int64_t t,
                            float lr, float beta2, float eps, int maximize,
                            void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Row-only Ember (Section 2.1, the variant the paper analyses most, listed in
+ * its ablation table with V floats of state): only the row statistic r is
+ * kept, and each row's gradient is divided by the square root of its own
+ * bias-corrected statistic:
+ *
+ *   r <- beta2 r + (1 - beta2) mean_j G_ij^2,   rhat = r / (1 - beta2^t)
+ *   W_ij <- W_ij -/+ lr G_ij / (sqrt(rhat_i) + eps)
+ *
+ * (the canonical step with vtil_ij = rhat_i: no column statistic and no
+ * normaliser s).  Each row is then independent of the others, so the step is
+ * one pass that reads G and W once and writes W once.  Arguments, layouts,
+ * dtypes, streams and error handling are those of the canonical entry points
+ * above, without c.  The workspace is sized by ember_workspace_bytes(V, D)
+ * and may be shared with nothing else while in use.
+ */
+
+/* Row-only state initialisation: zero fills of r (V floats) and of the parts
+ * of the workspace that must start at zero.  The caller sets t = 0. */
+int ember_rowonly_init_state(float* r, int64_t V, int64_t D,
+                             void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* One dense row-only step on W (V x D) with gradient G (V x D); r is updated
+ * in place, then W.  Scalar ranges as for ember_step_dense. */
+int ember_rowonly_step_dense(void* W, int w_dtype, int64_t ldw,
+                             const void* G, int g_dtype, int64_t ldg,
+                             float* r, int64_t V, int64_t D, int64_t t,
+                             float lr, float beta2, float eps, int maximize,
+                             void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* One sparse-row row-only step (G_rows, idx and n_idx as for
+ * ember_step_sparse_rows): the dense row-only step on the gradient that is zero
+ * outside idx.  Rows outside idx only see r decay by beta2; their W rows are
+ * not touched.  Index errors leave W and r unchanged and are reported by
+ * ember_get_error. */
+int ember_rowonly_step_sparse_rows(void* W, int w_dtype, int64_t ldw,
+                                   const void* G_rows, int g_dtype, int64_t ldg,
+                                   const int64_t* idx, int64_t n_idx,
+                                   float* r, int64_t V, int64_t D, int64_t t,
+                                   float lr, float beta2, float eps, int maximize,
+                                   void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * Device status of the most recent step enqueued with this workspace.

@@ -91,15 +91,10 @@ hipError_t timed(const char* name, hipStream_t s, F&& launch) {
 // one step
 // ---------------------------------------------------------------------------
 
-int run_step(StepArgs& a, float lr, float beta2, float eps, int64_t t, int maximize, hipStream_t s) {
-    const double b2 = (double)beta2;
-    a.beta2 = beta2;
-    a.one_minus_beta2 = (float)(1.0 - b2);
-    a.inv_bias = 1.0 / (1.0 - std::pow(b2, (double)t));
-    const double alpha_s = maximize ? (double)lr : -(double)lr;
-    a.inv_alpha = lr > 0.0f ? 1.0 / alpha_s : 0.0;
-    a.eps_over_alpha = lr > 0.0f ? (float)((double)eps / alpha_s) : 0.0f;
+void set_scalars(StepArgs& a, float lr, float beta2, float eps, int64_t t, int maximize);
 
+int run_step(StepArgs& a, float lr, float beta2, float eps, int64_t t, int maximize, hipStream_t s) {
+    set_scalars(a, lr, beta2, eps, t, maximize);
     hipError_t e = timed("ember_stats", s, [&] { return ember::launch_stats(a, s); });
     if (e == hipSuccess) e = timed("ember_finalize", s, [&] { return ember::launch_finalize(a, s); });
     // lr == 0 leaves every weight bit unchanged, so the dense step skips the
@@ -108,6 +103,31 @@ int run_step(StepArgs& a, float lr, float beta2, float eps, int64_t t, int maxim
     if (e == hipSuccess && (lr > 0.0f || a.sparse))
         e = timed("ember_apply", s, [&] { return ember::launch_apply(a, s); });
     return e == hipSuccess ? EMBER_OK : EMBER_ERR_HIP;
+}
+
+void set_scalars(StepArgs& a, float lr, float beta2, float eps, int64_t t, int maximize) {
+    const double b2 = (double)beta2;
+    a.beta2 = beta2;
+    a.one_minus_beta2 = (float)(1.0 - b2);
+    a.inv_bias = 1.0 / (1.0 - std::pow(b2, (double)t));
+    const double alpha_s = maximize ? (double)lr : -(double)lr;
+    a.inv_alpha = lr > 0.0f ? 1.0 / alpha_s : 0.0;
+    a.eps_over_alpha = lr > 0.0f ? (float)((double)eps / alpha_s) : 0.0f;
+}
+
+int run_rowonly_step(StepArgs& a, float lr, float beta2, float eps, int64_t t, int maximize, hipStream_t s) {
+    set_scalars(a, lr, beta2, eps, t, maximize);
+    hipError_t e = hipSuccess;
+    if (a.sparse) e = timed("ember_rowonly_validate", s, [&] { return ember::launch_rowonly_validate(a, s); });
+    if (e == hipSuccess) e = timed("ember_rowonly", s, [&] { return ember::launch_rowonly(a, s); });
+    return e == hipSuccess ? EMBER_OK : EMBER_ERR_HIP;
+}
+
+int check_rowonly_state(const float* r, const void* ws, size_t ws_bytes, int64_t V, int64_t D) {
+    if (r == nullptr || ws == nullptr) return EMBER_ERR_ARG;
+    if (!aligned(r, 4) || !aligned(ws, 256)) return EMBER_ERR_ALIGN;
+    if (ws_bytes < ember::ws_layout(V, D).total) return EMBER_ERR_WORKSPACE;
+    return EMBER_OK;
 }
 
 } // namespace
@@ -192,6 +212,77 @@ int ember_step_sparse_rows(void* W, int w_dtype, int64_t ldw, const void* G_rows
     a.D = D;
     a.ws = static_cast<char*>(ws);
     return run_step(a, lr, beta2, eps, t, maximize, stream);
+}
+
+int ember_rowonly_init_state(float* r, int64_t V, int64_t D, void* ws, size_t ws_bytes, hipStream_t stream) {
+    int st = check_shape(V, D);
+    if (st != EMBER_OK) return st;
+    st = check_rowonly_state(r, ws, ws_bytes, V, D);
+    if (st != EMBER_OK) return st;
+    const WsLayout L = ember::ws_layout(V, D);
+    hipError_t e = ember::launch_zero(r, (size_t)V * 4, stream);
+    if (e == hipSuccess) e = ember::launch_zero(ws, L.zero_end, stream);
+    return e == hipSuccess ? EMBER_OK : EMBER_ERR_HIP;
+}
+
+int ember_rowonly_step_dense(void* W, int w_dtype, int64_t ldw, const void* G, int g_dtype, int64_t ldg,
+                             float* r, int64_t V, int64_t D, int64_t t,
+                             float lr, float beta2, float eps, int maximize,
+                             void* ws, size_t ws_bytes, hipStream_t stream) {
+    int st = check_shape(V, D);
+    if (st == EMBER_OK) st = check_matrix(W, w_dtype, ldw, D, false);
+    if (st == EMBER_OK) st = check_matrix(G, g_dtype, ldg, D, false);
+    if (st == EMBER_OK) st = check_rowonly_state(r, ws, ws_bytes, V, D);
+    if (st == EMBER_OK) st = check_scalars(t, lr, beta2, eps);
+    if (st != EMBER_OK) return st;
+    StepArgs a{};
+    a.sparse = false;
+    a.W = W;
+    a.w_dtype = w_dtype;
+    a.ldw = ldw;
+    a.G = G;
+    a.g_dtype = g_dtype;
+    a.ldg = ldg;
+    a.idx = nullptr;
+    a.rows = V;
+    a.r = r;
+    a.c = nullptr;
+    a.V = V;
+    a.D = D;
+    a.ws = static_cast<char*>(ws);
+    return run_rowonly_step(a, lr, beta2, eps, t, maximize, stream);
+}
+
+int ember_rowonly_step_sparse_rows(void* W, int w_dtype, int64_t ldw, const void* G_rows, int g_dtype, int64_t ldg,
+                                   const int64_t* idx, int64_t n_idx,
+                                   float* r, int64_t V, int64_t D, int64_t t,
+                                   float lr, float beta2, float eps, int maximize,
+                                   void* ws, size_t ws_bytes, hipStream_t stream) {
+    int st = check_shape(V, D);
+    if (st == EMBER_OK && (n_idx < 0 || n_idx > V)) st = EMBER_ERR_SHAPE;
+    if (st == EMBER_OK) st = check_matrix(W, w_dtype, ldw, D, false);
+    if (st == EMBER_OK) st = check_matrix(G_rows, g_dtype, ldg, D, n_idx == 0);
+    if (st == EMBER_OK && n_idx > 0 && idx == nullptr) st = EMBER_ERR_ARG;
+    if (st == EMBER_OK && idx != nullptr && !aligned(idx, 8)) st = EMBER_ERR_ALIGN;
+    if (st == EMBER_OK) st = check_rowonly_state(r, ws, ws_bytes, V, D);
+    if (st == EMBER_OK) st = check_scalars(t, lr, beta2, eps);
+    if (st != EMBER_OK) return st;
+    StepArgs a{};
+    a.sparse = true;
+    a.W = W;
+    a.w_dtype = w_dtype;
+    a.ldw = ldw;
+    a.G = G_rows;
+    a.g_dtype = g_dtype;
+    a.ldg = ldg;
+    a.idx = idx;
+    a.rows = n_idx;
+    a.r = r;
+    a.c = nullptr;
+    a.V = V;
+    a.D = D;
+    a.ws = static_cast<char*>(ws);
+    return run_rowonly_step(a, lr, beta2, eps, t, maximize, stream);
 }
 
 int ember_get_error(const void* ws, hipStream_t stream, int* device_status) {

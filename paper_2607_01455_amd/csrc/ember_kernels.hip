@@ -691,6 +691,253 @@ __global__ __launch_bounds__(kBlock) void ember_apply(ApplyParams a) {
 }
 
 // ---------------------------------------------------------------------------
+// row-only Ember (Section 2.1): vtil_ij = rhat_i, so the whole step is one pass
+// over the rows, W += g / (sqrt(rhat_i) / alpha_s + eps / alpha_s)
+// ---------------------------------------------------------------------------
+
+constexpr int kRowOnlyRows = 2;          // rows in flight per block
+constexpr int kRowOnlyMaxWaves = 8;      // waves per block
+constexpr int kRowOnlyRowsPerBlock = 16;
+
+struct RowOnlyParams {
+    void* W;
+    int64_t ldw;
+    const void* G;
+    int64_t ldg;
+    int64_t rows;          // V (dense) or n (sparse)
+    int64_t D;
+    int total_chunks;
+    int slab_chunks;
+    int nslab;
+    int nb;                // row blocks
+    const int64_t* idx;    // sparse only
+    float* r;
+    int64_t V;
+    float beta2;
+    float one_minus_beta2;
+    float inv_bias;
+    float inv_alpha;       // 1 / alpha_s; 0 when lr == 0 (no weight is written)
+    float eps_over_alpha;
+    int* slot;             // sparse only
+    int* flag;             // sparse only: index-error bits, cleared by the last block
+    int* ticket;           // sparse only
+    int* status;
+};
+
+// The rows of one block, kRowOnlyRows at a time.  Resident: the block has
+// ceil(nslab / S) waves and wave w holds slabs w*S .. w*S+S-1 of the rows in
+// registers from the row sum to the update, so G is read once.  Otherwise
+// (rows too long to hold) wave w takes slabs w, w + nw, ... and reads them
+// once for the row sum and again, with W, for the update.
+template <typename GT, typename WT, int M, int S, bool kSparse, bool kResident>
+__device__ __forceinline__ void rowonly_rows(const RowOnlyParams& a, float (*part)[kRowOnlyRows], float* rn_lds) {
+    constexpr int EPC = 16 / (int)sizeof(GT);
+    constexpr int R = kRowOnlyRows;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int nw = blockDim.x / kWave;
+    const bool update = a.inv_alpha != 0.0f;
+
+    const int64_t r0 = (int64_t)blockIdx.x * kRowOnlyRowsPerBlock;
+    const int64_t r1 = min(r0 + kRowOnlyRowsPerBlock, a.rows);
+    const GT* G = static_cast<const GT*>(a.G);
+    WT* W = static_cast<WT*>(a.W);
+    const double invD = 1.0 / (double)a.D;
+
+    for (int64_t k0 = r0; k0 < r1; k0 += R) {
+        const GT* gr[R];
+        WT* wr[R];
+        int64_t wrow[R];
+        bool rv[R];
+#pragma unroll
+        for (int j = 0; j < R; ++j) {
+            rv[j] = k0 + j < r1;
+            const int64_t row = rv[j] ? k0 + j : r0;
+            wrow[j] = kSparse ? a.idx[row] : row;
+            gr[j] = G + row * a.ldg;
+            wr[j] = W + wrow[j] * a.ldw;
+        }
+        float s0[R], s1[R];
+#pragma unroll
+        for (int j = 0; j < R; ++j) s0[j] = s1[j] = 0.0f;
+        auto accumulate = [&](const Raw<GT, EPC>& raw, int j) {
+            float x[EPC];
+            decode(raw, x);
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) {
+                if (e & 1) s1[j] = fmaf(x[e], x[e], s1[j]);
+                else s0[j] = fmaf(x[e], x[e], s0[j]);
+            }
+        };
+        auto apply = [&](const Raw<GT, EPC>& graw, const Raw<WT, EPC>& wraw, float rc, WT* wrow_ptr, int ch) {
+            float g[EPC], w[EPC], o[EPC];
+            decode(graw, g);
+            decode(wraw, w);
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) {
+                const float upd = fmaf(g[e], rc, w[e]);
+                o[e] = (g[e] == 0.0f) ? w[e] : upd;
+            }
+            store_chunk<WT, EPC, true>(wrow_ptr, (int64_t)ch * EPC, a.D, o);
+        };
+
+        Raw<GT, EPC> graw[R][S][M];
+        Raw<WT, EPC> wraw[R][S][M];
+        if constexpr (kResident) {
+#pragma unroll
+            for (int j = 0; j < R; ++j)
+#pragma unroll
+                for (int q = 0; q < S; ++q) {
+                    const int slab = wave * S + q;
+                    const int cbeg = slab * a.slab_chunks;
+                    const int cend = min(cbeg + a.slab_chunks, a.total_chunks);
+#pragma unroll
+                    for (int m = 0; m < M; ++m) {
+                        const int ch = cbeg + lane + kWave * m;
+                        const bool v = rv[j] && slab < a.nslab && ch < cend;
+                        load_raw<GT, EPC, true>(gr[j], (int64_t)ch * EPC, v, a.D, graw[j][q][m]);
+                        load_raw<WT, EPC, true>(wr[j], (int64_t)ch * EPC, v && update, a.D, wraw[j][q][m]);
+                    }
+                }
+#pragma unroll
+            for (int j = 0; j < R; ++j)
+#pragma unroll
+                for (int q = 0; q < S; ++q)
+#pragma unroll
+                    for (int m = 0; m < M; ++m) accumulate(graw[j][q][m], j);
+        } else {
+            for (int slab = wave; slab < a.nslab; slab += nw) {
+                const int cbeg = slab * a.slab_chunks;
+                const int cend = min(cbeg + a.slab_chunks, a.total_chunks);
+#pragma unroll
+                for (int j = 0; j < R; ++j)
+#pragma unroll
+                    for (int m = 0; m < M; ++m) {
+                        const int ch = cbeg + lane + kWave * m;
+                        load_raw<GT, EPC, false>(gr[j], (int64_t)ch * EPC, rv[j] && ch < cend, a.D, graw[j][0][m]);
+                    }
+#pragma unroll
+                for (int j = 0; j < R; ++j)
+#pragma unroll
+                    for (int m = 0; m < M; ++m) accumulate(graw[j][0][m], j);
+            }
+        }
+
+        // Row sums of g^2: this wave's part, then the waves in order.
+        float rs[R];
+#pragma unroll
+        for (int j = 0; j < R; ++j) rs[j] = s0[j] + s1[j];
+        const float tot = rows_sum<R>(rs, lane);
+        if ((lane & (kWave / R - 1)) == 0) part[wave][lane / (kWave / R)] = tot;
+        __syncthreads();
+        if (threadIdx.x < R && rv[threadIdx.x]) {
+            const int j = threadIdx.x;
+            float sum = 0.0f;
+            for (int w = 0; w < nw; ++w) sum += part[w][j];
+            const float mean = (float)((double)sum * invD);
+            const float rnew = fmaf(a.beta2, a.r[wrow[j]], a.one_minus_beta2 * mean);
+            a.r[wrow[j]] = rnew;
+            rn_lds[j] = rnew;
+        }
+        __syncthreads();
+        if (update) {
+            float rc[R];
+#pragma unroll
+            for (int j = 0; j < R; ++j)
+                rc[j] = __builtin_amdgcn_rcpf(fmaf(sqrtf(rn_lds[j] * a.inv_bias), a.inv_alpha, a.eps_over_alpha));
+            if constexpr (kResident) {
+#pragma unroll
+                for (int j = 0; j < R; ++j) {
+                    if (!rv[j]) break;
+#pragma unroll
+                    for (int q = 0; q < S; ++q) {
+                        const int slab = wave * S + q;
+                        const int cbeg = slab * a.slab_chunks;
+                        const int cend = min(cbeg + a.slab_chunks, a.total_chunks);
+#pragma unroll
+                        for (int m = 0; m < M; ++m) {
+                            const int ch = cbeg + lane + kWave * m;
+                            if (slab < a.nslab && ch < cend) apply(graw[j][q][m], wraw[j][q][m], rc[j], wr[j], ch);
+                        }
+                    }
+                }
+            } else {
+                for (int slab = wave; slab < a.nslab; slab += nw) {
+                    const int cbeg = slab * a.slab_chunks;
+                    const int cend = min(cbeg + a.slab_chunks, a.total_chunks);
+#pragma unroll
+                    for (int j = 0; j < R; ++j)
+#pragma unroll
+                        for (int m = 0; m < M; ++m) {
+                            const int ch = cbeg + lane + kWave * m;
+                            const bool v = rv[j] && ch < cend;
+                            load_raw<GT, EPC, true>(gr[j], (int64_t)ch * EPC, v, a.D, graw[j][0][m]);
+                            load_raw<WT, EPC, true>(wr[j], (int64_t)ch * EPC, v, a.D, wraw[j][0][m]);
+                        }
+#pragma unroll
+                    for (int j = 0; j < R; ++j) {
+                        if (!rv[j]) break;
+#pragma unroll
+                        for (int m = 0; m < M; ++m) {
+                            const int ch = cbeg + lane + kWave * m;
+                            if (ch < cend) apply(graw[j][0][m], wraw[j][0][m], rc[j], wr[j], ch);
+                        }
+                    }
+                }
+            }
+        }
+        __syncthreads();  // part and rn_lds are reused by the next rows
+    }
+}
+
+// Dense: blocks [0, nb), 16 rows each.  Sparse: the same over the n gradient
+// rows (mapped through idx), then decay blocks that scale r by beta2 on every
+// row outside idx and clear the row marks.
+template <typename GT, typename WT, int M, int S, bool kSparse, bool kResident>
+__global__ __launch_bounds__(kRowOnlyMaxWaves * kWave) void ember_rowonly(RowOnlyParams a) {
+    __shared__ float part[kRowOnlyMaxWaves][kRowOnlyRows];
+    __shared__ float rn_lds[kRowOnlyRows];
+    __shared__ int last;
+    if (!kSparse) {
+        if (blockIdx.x == 0 && threadIdx.x == 0) *a.status = 0;
+        rowonly_rows<GT, WT, M, S, false, kResident>(a, part, rn_lds);
+        return;
+    }
+    const int err = *a.flag;
+    if (blockIdx.x == 0 && threadIdx.x == 0) *a.status = err;
+    if ((int)blockIdx.x >= a.nb) {
+        const int64_t i0 = (int64_t)(blockIdx.x - a.nb) * kDecayRows;
+        for (int64_t i = i0 + threadIdx.x; i < i0 + kDecayRows && i < a.V; i += blockDim.x) {
+            const int sl = a.slot[i];
+            if (sl != 0) a.slot[i] = 0;
+            else if (!err) a.r[i] = a.beta2 * a.r[i];
+        }
+    } else if (!err) {
+        rowonly_rows<GT, WT, M, S, true, kResident>(a, part, rn_lds);
+    }
+    // Every block has read the error bits: the last one clears them for the
+    // next step.
+    if (block_ticket(a.ticket, (int)gridDim.x, &last) && threadIdx.x == 0) {
+        *a.flag = 0;
+        *a.ticket = 0;
+    }
+}
+
+// Sparse row-only step, first launch: validates idx and marks the touched rows
+// (slot = 1 + position in idx).  Error bits are ORed into the flag, which the
+// fused launch reads and clears.
+__global__ __launch_bounds__(kBlock) void ember_rowonly_validate(const int64_t* idx, int64_t n, int64_t V,
+                                                                int* slot, int* flag) {
+    const int64_t k = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (k >= n) return;
+    const int64_t i = idx[k];
+    int bits = 0;
+    if (i < 0 || i >= V) bits = kFlagRange;
+    else if (atomicCAS(&slot[i], 0, (int)(k + 1)) != 0) bits = kFlagDuplicate;
+    if (bits) atomicOr(flag, bits);
+}
+
+// ---------------------------------------------------------------------------
 // zero fill (used instead of a memset node so the step stays capturable)
 // ---------------------------------------------------------------------------
 
@@ -723,6 +970,29 @@ template <typename GT, bool kSparse>
 hipError_t apply_dispatch_w(const ApplyParams& p, int w_dtype, int m, dim3 grid, hipStream_t s) {
     if (w_dtype == 0) return apply_dispatch<GT, float, kSparse>(p, m, grid, s);
     return apply_dispatch<GT, uint16_t, kSparse>(p, m, grid, s);
+}
+
+// Launch shapes of the row-only kernel: (chunks per lane, slabs per wave,
+// resident).  Rows of up to 8 slabs take one slab per wave, up to 16 two.
+template <typename GT, typename WT, bool kSparse>
+hipError_t rowonly_dispatch(const RowOnlyParams& p, int m, int spw, bool resident, dim3 grid, int threads,
+                            hipStream_t s) {
+    if (!resident) ember_rowonly<GT, WT, 2, 1, kSparse, false><<<grid, threads, 0, s>>>(p);
+    else if (m == 1 && spw == 1) ember_rowonly<GT, WT, 1, 1, kSparse, true><<<grid, threads, 0, s>>>(p);
+    else if (m == 2 && spw == 1) ember_rowonly<GT, WT, 2, 1, kSparse, true><<<grid, threads, 0, s>>>(p);
+    else if (m == 2 && spw == 2) ember_rowonly<GT, WT, 2, 2, kSparse, true><<<grid, threads, 0, s>>>(p);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+template <bool kSparse>
+hipError_t rowonly_dispatch_t(const RowOnlyParams& p, int g_dtype, int w_dtype, int m, int spw, bool resident,
+                              dim3 grid, int threads, hipStream_t s) {
+    if (g_dtype == 0)
+        return w_dtype == 0 ? rowonly_dispatch<float, float, kSparse>(p, m, spw, resident, grid, threads, s)
+                            : rowonly_dispatch<float, uint16_t, kSparse>(p, m, spw, resident, grid, threads, s);
+    return w_dtype == 0 ? rowonly_dispatch<uint16_t, float, kSparse>(p, m, spw, resident, grid, threads, s)
+                        : rowonly_dispatch<uint16_t, uint16_t, kSparse>(p, m, spw, resident, grid, threads, s);
 }
 
 } // namespace
@@ -820,7 +1090,8 @@ hipError_t launch_finalize(const StepArgs& a, hipStream_t s) {
     p.r = a.r;
     p.c = a.c;
     p.slot = reinterpret_cast<int*>(a.ws + L.slot);
-    p.flag = reinterpret_cast<const int*>(a.ws + L.flag);
+    p.flag = reinterpret_cast<int*>(a.ws + L.flag);
+    p.ticket = reinterpret_cast<int*>(a.ws + L.ticket);
     p.status = reinterpret_cast<int*>(a.ws + L.status);
     p.beta2 = a.beta2;
     p.one_minus_beta2 = a.one_minus_beta2;
@@ -868,6 +1139,53 @@ hipError_t launch_apply(const StepArgs& a, hipStream_t s) {
                       : apply_dispatch_w<float, false>(p, a.w_dtype, cp.m, grid, s);
     return sparse ? apply_dispatch_w<uint16_t, true>(p, a.w_dtype, cp.m, grid, s)
                   : apply_dispatch_w<uint16_t, false>(p, a.w_dtype, cp.m, grid, s);
+}
+
+hipError_t launch_rowonly_validate(const StepArgs& a, hipStream_t s) {
+    const WsLayout L = ws_layout(a.V, a.D);
+    if (a.rows == 0) return hipSuccess;
+    const unsigned nblk = (unsigned)((a.rows + kBlock - 1) / kBlock);
+    ember_rowonly_validate<<<nblk, kBlock, 0, s>>>(a.idx, a.rows, a.V, reinterpret_cast<int*>(a.ws + L.slot),
+                                                   reinterpret_cast<int*>(a.ws + L.flag));
+    return hipGetLastError();
+}
+
+hipError_t launch_rowonly(const StepArgs& a, hipStream_t s) {
+    const WsLayout L = ws_layout(a.V, a.D);
+    const ColPlan cp = col_plan(a.D, a.g_dtype);
+    const bool resident = cp.nslab <= 2 * kRowOnlyMaxWaves;
+    const int spw = cp.nslab <= kRowOnlyMaxWaves ? 1 : 2;
+    const int waves = resident ? (cp.nslab + spw - 1) / spw : kRowOnlyMaxWaves;
+    if ((spw == 2 || !resident) && cp.m != 2) return hipErrorInvalidValue;
+    RowOnlyParams p;
+    p.W = a.W;
+    p.ldw = a.ldw;
+    p.G = a.G;
+    p.ldg = a.ldg;
+    p.rows = a.rows;
+    p.D = a.D;
+    p.total_chunks = cp.total_chunks;
+    p.slab_chunks = cp.slab_chunks;
+    p.nslab = cp.nslab;
+    p.nb = (int)((a.rows + kRowOnlyRowsPerBlock - 1) / kRowOnlyRowsPerBlock);
+    p.idx = a.idx;
+    p.r = a.r;
+    p.V = a.V;
+    p.beta2 = a.beta2;
+    p.one_minus_beta2 = a.one_minus_beta2;
+    p.inv_bias = (float)a.inv_bias;
+    p.inv_alpha = (float)a.inv_alpha;
+    p.eps_over_alpha = a.eps_over_alpha;
+    p.slot = reinterpret_cast<int*>(a.ws + L.slot);
+    p.flag = reinterpret_cast<int*>(a.ws + L.flag);
+    p.ticket = reinterpret_cast<int*>(a.ws + L.ticket);
+    p.status = reinterpret_cast<int*>(a.ws + L.status);
+    const int ndecay = a.sparse ? (int)((a.V + kDecayRows - 1) / kDecayRows) : 0;
+    const dim3 grid((unsigned)(p.nb + ndecay));
+    if (p.nb + ndecay == 0) return hipSuccess;
+    if (a.sparse)
+        return rowonly_dispatch_t<true>(p, a.g_dtype, a.w_dtype, cp.m, spw, resident, grid, waves * kWave, s);
+    return rowonly_dispatch_t<false>(p, a.g_dtype, a.w_dtype, cp.m, spw, resident, grid, waves * kWave, s);
 }
 
 } // namespace ember

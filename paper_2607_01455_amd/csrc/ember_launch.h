@@ -65,6 +65,7 @@ constexpr int kApplyBatches = EMBER_APPLY_BATCHES;
 constexpr int kMaxBlocks = EMBER_MAX_BLOCKS;
 constexpr int kRowsPerBlockMin = 8; // fewer rows than this per block: fewer blocks
 constexpr int kVRowsPerThread = 4;  // rows per thread in the r pass
+constexpr int kDecayRows = 1024;    // rows per decay block of the row-only sparse step
 
 // Status bits written by the sparse statistics pass.
 constexpr int kFlagRange = 1;
@@ -148,5 +149,10 @@ hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
 hipError_t launch_stats(const StepArgs& a, hipStream_t s);
 hipError_t launch_finalize(const StepArgs& a, hipStream_t s);
 hipError_t launch_apply(const StepArgs& a, hipStream_t s);
+
+// Row-only Ember (one fused pass over the rows; the sparse step first
+// validates idx and marks the touched rows).
+hipError_t launch_rowonly_validate(const StepArgs& a, hipStream_t s);
+hipError_t launch_rowonly(const StepArgs& a, hipStream_t s);
 
 } // namespace ember

@@ -29,7 +29,8 @@ EMBER_ERR_HIP = -7
 
 # Every function the C header declares, checked by the CPU test suite.
 EXPORTED = ("ember_workspace_bytes", "ember_init_state", "ember_step_dense",
-            "ember_step_sparse_rows", "ember_get_error", "ember_strerror",
+            "ember_step_sparse_rows", "ember_rowonly_init_state", "ember_rowonly_step_dense",
+            "ember_rowonly_step_sparse_rows", "ember_get_error", "ember_strerror",
             "ember_profile_enable", "ember_profile_collect")
 
 
@@ -54,6 +55,11 @@ def _load(path: str = _LIB_PATH) -> ctypes.CDLL:
                                      f32, f32, f32, i32, vp, sz, vp]
     lib.ember_step_sparse_rows.argtypes = [vp, i32, i64, vp, i32, i64, vp, i64, vp, vp, i64, i64, i64,
                                            f32, f32, f32, i32, vp, sz, vp]
+    lib.ember_rowonly_init_state.argtypes = [vp, i64, i64, vp, sz, vp]
+    lib.ember_rowonly_step_dense.argtypes = [vp, i32, i64, vp, i32, i64, vp, i64, i64, i64,
+                                             f32, f32, f32, i32, vp, sz, vp]
+    lib.ember_rowonly_step_sparse_rows.argtypes = [vp, i32, i64, vp, i32, i64, vp, i64, vp, i64, i64, i64,
+                                                   f32, f32, f32, i32, vp, sz, vp]
     lib.ember_get_error.argtypes = [vp, vp, ctypes.POINTER(i32)]
     lib.ember_strerror.argtypes = [i32]
     lib.ember_strerror.restype = ctypes.c_char_p
@@ -136,6 +142,38 @@ def ember_step_sparse_rows(W: torch.Tensor, G_rows: torch.Tensor, idx: torch.Ten
            "ember_step_sparse_rows")
 
 
+def ember_rowonly_init_state(r: torch.Tensor, D: int, ws: torch.Tensor) -> None:
+    _check(LIB.ember_rowonly_init_state(_ptr(r), r.numel(), int(D), _ptr(ws),
+                                        ws.numel() * ws.element_size(), _stream(r)),
+           "ember_rowonly_init_state")
+
+
+def ember_rowonly_step_dense(W: torch.Tensor, G: torch.Tensor, r: torch.Tensor, t: int,
+                             lr: float = 1e-3, beta2: float = 0.999, eps: float = 1e-8,
+                             maximize: bool = False, ws: torch.Tensor | None = None) -> None:
+    V, D = W.shape
+    _check(LIB.ember_rowonly_step_dense(_ptr(W), _dtype(W), _ld(W), _ptr(G), _dtype(G), _ld(G),
+                                        _ptr(r), V, D, int(t), float(lr), float(beta2), float(eps),
+                                        int(bool(maximize)), _ptr(ws), ws.numel() * ws.element_size(),
+                                        _stream(W)), "ember_rowonly_step_dense")
+
+
+def ember_rowonly_step_sparse_rows(W: torch.Tensor, G_rows: torch.Tensor, idx: torch.Tensor,
+                                   r: torch.Tensor, t: int,
+                                   lr: float = 1e-3, beta2: float = 0.999, eps: float = 1e-8,
+                                   maximize: bool = False, ws: torch.Tensor | None = None) -> None:
+    V, D = W.shape
+    n = idx.numel()
+    if idx.dtype != torch.int64:
+        raise TypeError("idx must be int64")
+    ldg = _ld(G_rows) if G_rows.numel() else D
+    _check(LIB.ember_rowonly_step_sparse_rows(_ptr(W), _dtype(W), _ld(W), _ptr(G_rows), _dtype(G_rows),
+                                              ldg, _ptr(idx), n, _ptr(r), V, D, int(t), float(lr),
+                                              float(beta2), float(eps), int(bool(maximize)), _ptr(ws),
+                                              ws.numel() * ws.element_size(), _stream(W)),
+           "ember_rowonly_step_sparse_rows")
+
+
 def ember_get_error(ws: torch.Tensor) -> int:
     """Device status of the last step on this workspace (synchronises the stream)."""
     st = ctypes.c_int(0)
@@ -159,31 +197,44 @@ class EmberTable:
     """Ember state of one V x D token table on one device: r, c, workspace, t.
 
     A convenience holder around the C entry points (Algorithm 1: r_0 = 0,
-    c_0 = 0, t = 0, then t += 1 before each update).
+    c_0 = 0, t = 0, then t += 1 before each update).  ``row_only`` selects the
+    row-only variant of Section 2.1 (no c).
     """
 
     def __init__(self, V: int, D: int, device="cuda", lr: float = 1e-3, beta2: float = 0.999,
-                 eps: float = 1e-8, maximize: bool = False):
+                 eps: float = 1e-8, maximize: bool = False, row_only: bool = False):
         self.V, self.D = int(V), int(D)
         self.lr, self.beta2, self.eps, self.maximize = lr, beta2, eps, maximize
+        self.row_only = bool(row_only)
         self.r = torch.empty(self.V, dtype=torch.float32, device=device)
-        self.c = torch.empty(self.D, dtype=torch.float32, device=device)
+        self.c = None if self.row_only else torch.empty(self.D, dtype=torch.float32, device=device)
         nbytes = ember_workspace_bytes(self.V, self.D)
         self.ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
         self.t = 0
-        ember_init_state(self.r, self.c, self.ws)
+        if self.row_only:
+            ember_rowonly_init_state(self.r, self.D, self.ws)
+        else:
+            ember_init_state(self.r, self.c, self.ws)
 
     def step(self, W: torch.Tensor, G: torch.Tensor) -> None:
-        ember_step_dense(W, G, self.r, self.c, self.t + 1, self.lr, self.beta2, self.eps,
-                         self.maximize, self.ws)
+        if self.row_only:
+            ember_rowonly_step_dense(W, G, self.r, self.t + 1, self.lr, self.beta2, self.eps,
+                                     self.maximize, self.ws)
+        else:
+            ember_step_dense(W, G, self.r, self.c, self.t + 1, self.lr, self.beta2, self.eps,
+                             self.maximize, self.ws)
         self.t += 1
 
     def step_sparse_rows(self, W: torch.Tensor, G_rows: torch.Tensor, idx: torch.Tensor,
                          check: bool = False) -> None:
         """Sparse-row step.  With check=True the index status is read back (a
         stream sync) and t advances only if idx was valid."""
-        ember_step_sparse_rows(W, G_rows, idx, self.r, self.c, self.t + 1, self.lr, self.beta2,
-                               self.eps, self.maximize, self.ws)
+        if self.row_only:
+            ember_rowonly_step_sparse_rows(W, G_rows, idx, self.r, self.t + 1, self.lr, self.beta2,
+                                           self.eps, self.maximize, self.ws)
+        else:
+            ember_step_sparse_rows(W, G_rows, idx, self.r, self.c, self.t + 1, self.lr, self.beta2,
+                                   self.eps, self.maximize, self.ws)
         if check:
             _check(ember_get_error(self.ws), "ember_step_sparse_rows (device)")
         self.t += 1

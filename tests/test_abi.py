@@ -31,7 +31,8 @@ def _declared_functions():
 def test_header_declares_the_entry_points():
     names = _declared_functions()
     for required in ("ember_workspace_bytes", "ember_init_state", "ember_step_dense",
-                     "ember_step_sparse_rows", "ember_get_error", "ember_strerror"):
+                     "ember_step_sparse_rows", "ember_rowonly_init_state", "ember_rowonly_step_dense",
+                     "ember_rowonly_step_sparse_rows", "ember_get_error", "ember_strerror"):
         assert required in names
 
 
@@ -125,12 +126,59 @@ def test_sparse_step_rejects_bad_arguments_on_host(em, kw, status):
     assert _sparse(em, **kw) == getattr(em, "EMBER_ERR_" + status)
 
 
+def _rowonly_dense(em, **kw):
+    a = dict(W=W_, wd=1, ldw=64, G=G_, gd=1, ldg=64, r=R_, V=10, D=64, t=1,
+             lr=1e-3, b2=0.999, eps=1e-8, mx=0, ws=WS_, wsb=None)
+    a.update(kw)
+    if a["wsb"] is None:
+        a["wsb"] = _ws_bytes(em, max(a["V"], 1), max(a["D"], 1))
+    return em.LIB.ember_rowonly_step_dense(a["W"], a["wd"], a["ldw"], a["G"], a["gd"], a["ldg"], a["r"],
+                                           a["V"], a["D"], a["t"], a["lr"], a["b2"], a["eps"], a["mx"],
+                                           a["ws"], a["wsb"], None)
+
+
+def _rowonly_sparse(em, **kw):
+    a = dict(W=W_, wd=1, ldw=64, G=G_, gd=1, ldg=64, idx=IDX_, n=3, r=R_, V=10, D=64, t=1,
+             lr=1e-3, b2=0.999, eps=1e-8, mx=0, ws=WS_, wsb=None)
+    a.update(kw)
+    if a["wsb"] is None:
+        a["wsb"] = _ws_bytes(em, max(a["V"], 1), max(a["D"], 1))
+    return em.LIB.ember_rowonly_step_sparse_rows(a["W"], a["wd"], a["ldw"], a["G"], a["gd"], a["ldg"],
+                                                 a["idx"], a["n"], a["r"], a["V"], a["D"], a["t"], a["lr"],
+                                                 a["b2"], a["eps"], a["mx"], a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(V=0), "SHAPE"), (dict(D=0), "SHAPE"), (dict(ldw=63), "SHAPE"), (dict(ldg=32), "SHAPE"),
+    (dict(V=2 ** 31), "SHAPE"), (dict(D=2 ** 22 + 8, ldw=2 ** 22 + 8, ldg=2 ** 22 + 8), "SHAPE"),
+    (dict(W=None), "ARG"), (dict(G=None), "ARG"), (dict(r=None), "ARG"), (dict(ws=None), "ARG"),
+    (dict(W=W_ + 8), "ALIGN"), (dict(G=G_ + 2), "ALIGN"), (dict(r=R_ + 2), "ALIGN"),
+    (dict(ws=WS_ + 128), "ALIGN"), (dict(wd=2), "DTYPE"), (dict(wsb=1024), "WORKSPACE"),
+    (dict(t=0), "ARG"), (dict(b2=1.0), "ARG"), (dict(lr=-1e-3), "ARG"), (dict(eps=float("inf")), "ARG"),
+])
+def test_rowonly_dense_step_rejects_bad_arguments_on_host(em, kw, status):
+    assert _rowonly_dense(em, **kw) == getattr(em, "EMBER_ERR_" + status)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n=-1), "SHAPE"), (dict(n=11), "SHAPE"), (dict(idx=None), "ARG"), (dict(idx=IDX_ + 4), "ALIGN"),
+    (dict(G=None), "ARG"), (dict(r=None), "ARG"), (dict(gd=3), "DTYPE"), (dict(t=0), "ARG"),
+    (dict(wsb=0), "WORKSPACE"), (dict(V=0), "SHAPE"),
+])
+def test_rowonly_sparse_step_rejects_bad_arguments_on_host(em, kw, status):
+    assert _rowonly_sparse(em, **kw) == getattr(em, "EMBER_ERR_" + status)
+
+
 def test_init_state_and_get_error_reject_bad_arguments(em):
     wsb = _ws_bytes(em, 10, 64)
     assert em.LIB.ember_init_state(R_, C_, 0, 64, WS_, wsb, None) == em.EMBER_ERR_SHAPE
     assert em.LIB.ember_init_state(None, C_, 10, 64, WS_, wsb, None) == em.EMBER_ERR_ARG
     assert em.LIB.ember_init_state(R_, C_, 10, 64, WS_, 8, None) == em.EMBER_ERR_WORKSPACE
     assert em.LIB.ember_init_state(R_, C_, 10, 64, WS_ + 4, wsb, None) == em.EMBER_ERR_ALIGN
+    assert em.LIB.ember_rowonly_init_state(R_, 0, 64, WS_, wsb, None) == em.EMBER_ERR_SHAPE
+    assert em.LIB.ember_rowonly_init_state(None, 10, 64, WS_, wsb, None) == em.EMBER_ERR_ARG
+    assert em.LIB.ember_rowonly_init_state(R_, 10, 64, WS_, 8, None) == em.EMBER_ERR_WORKSPACE
+    assert em.LIB.ember_rowonly_init_state(R_, 10, 64, WS_ + 4, wsb, None) == em.EMBER_ERR_ALIGN
     st = ctypes.c_int(0)
     assert em.LIB.ember_get_error(None, None, ctypes.byref(st)) == em.EMBER_ERR_ARG
     assert em.LIB.ember_get_error(WS_, None, None) == em.EMBER_ERR_ARG
