@@ -39,6 +39,7 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-rows", type=int, default=65536, help="rows of the oracle's sample")
     p.add_argument("--no-other-configs", action="store_true")
+    p.add_argument("--no-row-only", action="store_true")
     return p.parse_args()
 
 
@@ -123,6 +124,81 @@ def other_configs(ember, wl, torch, dev, K):
         del W, grads, tab
         torch.cuda.empty_cache()
     return out
+
+
+def row_only_section(ember, wl, torch, dev, K, Wm, W_head, W_emb, grads, batches):
+    """The same two-table workload with row-only Ember (Section 2.1; state V,
+    one fused pass per table): whole-step time, per-table medians and kernel
+    averages, in row-only algorithmic bytes."""
+    stream = torch.cuda.current_stream()
+    head = ember.EmberTable(V, D, device=dev, row_only=True)
+    emb = ember.EmberTable(V, D, device=dev, row_only=True)
+    n_grads = len(grads)
+
+    def step(k):
+        head.step(W_head, grads[k % n_grads])
+        idx, Gr = batches[k]
+        emb.step_sparse_rows(W_emb, Gr, idx)
+
+    for k in range(Wm):
+        step(k)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for k in range(K):
+        step(Wm + k)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / K
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+    for k in range(K):
+        ev[k][0].record(stream)
+        head.step(W_head, grads[(Wm + k) % n_grads])
+        ev[k][1].record(stream)
+        idx, Gr = batches[Wm + k]
+        emb.step_sparse_rows(W_emb, Gr, idx)
+        ev[k][2].record(stream)
+    torch.cuda.synchronize()
+    dense_ms = sorted(e[0].elapsed_time(e[1]) for e in ev)[K // 2]
+    sparse_ms = sorted(e[1].elapsed_time(e[2]) for e in ev)[K // 2]
+    def profiled(fn):
+        ember.ember_profile_enable(True)
+        for k in range(K):
+            fn(k)
+        torch.cuda.synchronize()
+        ember.ember_profile_enable(False)
+        return ember.ember_profile_collect()
+
+    dstats = profiled(lambda k: head.step(W_head, grads[(Wm + k) % n_grads]))
+    sstats = profiled(lambda k: emb.step_sparse_rows(W_emb, batches[Wm + k][1], batches[Wm + k][0]))
+    if ember.ember_get_error(emb.ws) != ember.EMBER_OK:
+        raise RuntimeError("row-only sparse step reported an index error")
+    fused_launches, fused_ms = dstats["ember_rowonly"]
+    fused_avg_ms = fused_ms / fused_launches
+    dense_bytes = wl.rowonly_algorithmic_bytes(V, D, 2, 2)
+    n_rows = [int(b[0].numel()) for b in batches[Wm:Wm + K]]
+    sparse_bytes = sum(wl.rowonly_algorithmic_bytes(V, D, 2, 2, rows=n) for n in n_rows) / K
+    gbps = (dense_bytes + sparse_bytes) / (ms_step * 1e-3) / 1e9
+    fused_gbps = dense_bytes / (fused_avg_ms * 1e-3) / 1e9
+    return {
+        "ms_per_step": round(ms_step, 4),
+        "GBps": round(gbps, 1),
+        "pct_of_peak": round(100.0 * gbps / PEAK_GBPS, 2),
+        "algorithmic_bytes_per_step": int(dense_bytes + sparse_bytes),
+        "dense_lmhead": {"ms": round(dense_ms, 4), "bytes": dense_bytes,
+                         "GBps": round(dense_bytes / (dense_ms * 1e-3) / 1e9, 1),
+                         "pct_of_peak": round(100.0 * dense_bytes / (dense_ms * 1e-3) / 1e9 / PEAK_GBPS, 2)},
+        "sparse_embedding": {"ms": round(sparse_ms, 4), "bytes": int(sparse_bytes)},
+        "kernels_ms_avg": {
+            "dense": {k: round(v[1] / v[0], 5) for k, v in dstats.items()},
+            "sparse": {k: round(v[1] / v[0], 5) for k, v in sstats.items()},
+        },
+        "roofline": {"kernel": "ember_rowonly (dense LM-head step)", "bound": "hbm",
+                     "achieved": round(fused_gbps, 1), "peak": PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(fused_gbps / PEAK_GBPS, 4), "avg_launch_ms": round(fused_avg_ms, 5),
+                     "algorithmic_bytes_per_launch": dense_bytes},
+    }
 
 
 def main():
@@ -285,11 +361,15 @@ def main():
             "algorithmic_bytes_per_launch": apply_bytes,
         },
         "torch_device_copy_GBps": round(copy_gbps, 1),
+        "row_only": None,
         "other_configs": None,
         "cpu_baseline": None,
     }
+    del head, emb
+    if not args.no_row_only:
+        out["row_only"] = row_only_section(ember, wl, torch, dev, K, Wm, W_head, W_emb, grads, batches)
     if not args.no_other_configs:
-        del W_head, W_emb, grads, batches, head, emb
+        del W_head, W_emb, grads, batches
         torch.cuda.empty_cache()
         out["other_configs"] = other_configs(ember, wl, torch, dev, K)
     if not args.no_cpu_baseline:

@@ -101,6 +101,16 @@ __device__ __forceinline__ void st(V* p, V v) {
 // Words of a chunk of N elements of T (N * sizeof(T) is 8, 16 or 32 bytes).
 template <typename T, int N> struct Raw { uint32_t u[N * sizeof(T) / 4]; };
 
+// Makes the compiler treat the words as rewritten (no instruction is emitted),
+// so values decoded from them before this point are not kept alive to be
+// reused after it: a decode is two ALU operations, a register held per
+// element across a reduction costs occupancy.
+template <typename T, int N>
+__device__ __forceinline__ void launder(Raw<T, N>& r) {
+#pragma unroll
+    for (int q = 0; q < N * (int)sizeof(T) / 4; ++q) asm volatile("" : "+v"(r.u[q]));
+}
+
 template <typename T>
 __device__ __forceinline__ uint32_t elem_bits(const T* p) {
     if constexpr (sizeof(T) == 4) return __float_as_uint(*p);
@@ -136,6 +146,51 @@ __device__ __forceinline__ void load_raw(const T* row, int64_t col, bool valid, 
                 else r.u[e / 2] |= b << (16 * (e & 1));
             }
         }
+    }
+}
+
+// Raw buffer access to one row (base and byte length in a buffer resource).
+// The hardware checks every access against the length: loads past it return
+// zero and stores past it are dropped, so the row tail and absent rows (length
+// 0) need no branch.  Lengths here are multiples of 16 bytes, so a chunk is
+// wholly inside or wholly outside.
+constexpr int kBufferWord3 = 0x00020000;  // raw 32-bit data format, gfx9 family
+constexpr int kCachePolicy = EMBER_ROWONLY_NT ? 2 : 0;  // 2: non-temporal
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_buffer(const void* row, int bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(row), 0, bytes, kBufferWord3);
+}
+
+template <typename T, int N>
+__device__ __forceinline__ void buf_load(__amdgpu_buffer_rsrc_t rs, int byte_off, Raw<T, N>& r) {
+    constexpr int kWords = N * (int)sizeof(T) / 4;
+    if constexpr (kWords == 2) {
+        const u32x2 v = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rs, byte_off, 0, kCachePolicy));
+        r.u[0] = v.x; r.u[1] = v.y;
+    } else {
+#pragma unroll
+        for (int q = 0; q < kWords / 4; ++q) {
+            const u32x4 v = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, byte_off + 16 * q, 0, kCachePolicy));
+            r.u[4 * q] = v.x; r.u[4 * q + 1] = v.y; r.u[4 * q + 2] = v.z; r.u[4 * q + 3] = v.w;
+        }
+    }
+}
+
+template <typename T, int N>
+__device__ __forceinline__ void buf_store(__amdgpu_buffer_rsrc_t rs, int byte_off, const float (&x)[N]) {
+    constexpr int kWords = N * (int)sizeof(T) / 4;
+    uint32_t u[kWords];
+    encode<T, N>(x, u);
+    if constexpr (kWords == 2) {
+        __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b64(rs, 0, 0, 0)), u32x2{u[0], u[1]}),
+                                              rs, byte_off, 0, kCachePolicy);
+    } else {
+#pragma unroll
+        for (int q = 0; q < kWords / 4; ++q)
+            __builtin_amdgcn_raw_buffer_store_b128(
+                __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b128(rs, 0, 0, 0)),
+                                   u32x4{u[4 * q], u[4 * q + 1], u[4 * q + 2], u[4 * q + 3]}),
+                rs, byte_off + 16 * q, 0, kCachePolicy);
     }
 }
 
@@ -695,9 +750,11 @@ __global__ __launch_bounds__(kBlock) void ember_apply(ApplyParams a) {
 // over the rows, W += g / (sqrt(rhat_i) / alpha_s + eps / alpha_s)
 // ---------------------------------------------------------------------------
 
-constexpr int kRowOnlyRows = 2;          // rows in flight per block
-constexpr int kRowOnlyMaxWaves = 8;      // waves per block
-constexpr int kRowOnlyRowsPerBlock = 16;
+constexpr int kRowOnlyRows = EMBER_ROWONLY_ROWS;         // rows in flight per block
+constexpr int kRowOnlyMaxWaves = 8;                      // waves per block
+constexpr int kRowOnlyRowsPerBlock = EMBER_ROWONLY_RPB;  // rows per block
+constexpr int kRowOnlyWaveRows = EMBER_ROWONLY_WAVE_ROWS; // rows in flight per wave (one-wave rows)
+constexpr int kRowOnlyWaveChunks = 16 * kWave;           // longest row held by one wave, in chunks
 
 struct RowOnlyParams {
     void* W;
@@ -778,7 +835,7 @@ __device__ __forceinline__ void rowonly_rows(const RowOnlyParams& a, float (*par
                 const float upd = fmaf(g[e], rc, w[e]);
                 o[e] = (g[e] == 0.0f) ? w[e] : upd;
             }
-            store_chunk<WT, EPC, true>(wrow_ptr, (int64_t)ch * EPC, a.D, o);
+            store_chunk<WT, EPC, EMBER_ROWONLY_NT>(wrow_ptr, (int64_t)ch * EPC, a.D, o);
         };
 
         Raw<GT, EPC> graw[R][S][M];
@@ -795,8 +852,9 @@ __device__ __forceinline__ void rowonly_rows(const RowOnlyParams& a, float (*par
                     for (int m = 0; m < M; ++m) {
                         const int ch = cbeg + lane + kWave * m;
                         const bool v = rv[j] && slab < a.nslab && ch < cend;
-                        load_raw<GT, EPC, true>(gr[j], (int64_t)ch * EPC, v, a.D, graw[j][q][m]);
-                        load_raw<WT, EPC, true>(wr[j], (int64_t)ch * EPC, v && update, a.D, wraw[j][q][m]);
+                        load_raw<GT, EPC, EMBER_ROWONLY_NT>(gr[j], (int64_t)ch * EPC, v, a.D, graw[j][q][m]);
+                        load_raw<WT, EPC, EMBER_ROWONLY_NT>(wr[j], (int64_t)ch * EPC, v && update, a.D,
+                                                            wraw[j][q][m]);
                     }
                 }
 #pragma unroll
@@ -890,9 +948,148 @@ __device__ __forceinline__ void rowonly_rows(const RowOnlyParams& a, float (*par
     }
 }
 
-// Dense: blocks [0, nb), 16 rows each.  Sparse: the same over the n gradient
-// rows (mapped through idx), then decay blocks that scale r by beta2 on every
-// row outside idx and clear the row marks.
+// Rows up to 1024 chunks (bf16 D <= 8192, fp32 D <= 4096): one wave per row.
+// Lane l holds chunks l, l + 64, ..., l + 64 (C - 1) of G and W in registers,
+// the row sum is a butterfly over the wave, and no barrier is needed.  Each
+// wave takes kRowOnlyWaveRows adjacent rows at a time; the waves of a block
+// interleave over the block's rows.
+template <typename GT, typename WT, int C, bool kSparse, bool kExact>
+__device__ __forceinline__ void rowonly_wave_rows(const RowOnlyParams& a) {
+    constexpr int EPC = 16 / (int)sizeof(GT);
+    constexpr int R = kRowOnlyWaveRows;
+    constexpr int kWBytes = EPC * (int)sizeof(WT);   // bytes of W per chunk
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const bool update = a.inv_alpha != 0.0f;
+    const int64_t r0 = (int64_t)blockIdx.x * kRowOnlyRowsPerBlock;
+    const int64_t r1 = min(r0 + kRowOnlyRowsPerBlock, a.rows);
+    const GT* G = static_cast<const GT*>(a.G);
+    WT* W = static_cast<WT*>(a.W);
+    const double invD = 1.0 / (double)a.D;
+    const int gbytes = (int)a.D * (int)sizeof(GT);
+    const int wbytes = (int)a.D * (int)sizeof(WT);
+
+    for (int64_t k0 = r0 + (int64_t)wave * R; k0 < r1; k0 += (int64_t)kWaves * R) {
+        const GT* gr[R];
+        WT* wr[R];
+        int64_t wrow[R];
+        bool rv[R];
+        float rold[R];
+        Raw<GT, EPC> graw[R][C];
+        Raw<WT, EPC> wraw[R][C];
+        __amdgpu_buffer_rsrc_t gb[R], wb[R];
+#pragma unroll
+        for (int j = 0; j < R; ++j) {
+            rv[j] = k0 + j < r1;
+            const int64_t row = rv[j] ? k0 + j : r0;
+            wrow[j] = kSparse ? a.idx[row] : row;
+            gr[j] = G + row * a.ldg;
+            wr[j] = W + wrow[j] * a.ldw;
+            rold[j] = a.r[wrow[j]];
+            gb[j] = row_buffer(gr[j], rv[j] ? gbytes : 0);
+            wb[j] = row_buffer(wr[j], rv[j] && update ? wbytes : 0);
+        }
+        // G first: the row sums wait only for these loads, W arrives meanwhile.
+#pragma unroll
+        for (int j = 0; j < R; ++j)
+#pragma unroll
+            for (int c = 0; c < C; ++c) {
+                const int ch = lane + kWave * c;
+                if constexpr (kExact) buf_load<GT, EPC>(gb[j], ch * 16, graw[j][c]);
+                else load_raw<GT, EPC, EMBER_ROWONLY_NT>(gr[j], (int64_t)ch * EPC, rv[j] && ch < a.total_chunks,
+                                                         a.D, graw[j][c]);
+            }
+#pragma unroll
+        for (int j = 0; j < R; ++j)
+#pragma unroll
+            for (int c = 0; c < C; ++c) {
+                const int ch = lane + kWave * c;
+                if constexpr (kExact) buf_load<WT, EPC>(wb[j], ch * kWBytes, wraw[j][c]);
+                else load_raw<WT, EPC, EMBER_ROWONLY_NT>(wr[j], (int64_t)ch * EPC,
+                                                         rv[j] && ch < a.total_chunks && update, a.D, wraw[j][c]);
+            }
+        // Keep every load of the rows issued before the first wait.
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < R; ++j) {
+            float s0 = 0.0f, s1 = 0.0f;
+#pragma unroll
+            for (int c = 0; c < C; ++c) {
+                float x[EPC];
+                decode(graw[j][c], x);
+#pragma unroll
+                for (int e = 0; e < EPC; ++e) {
+                    if (e & 1) s1 = fmaf(x[e], x[e], s1);
+                    else s0 = fmaf(x[e], x[e], s0);
+                }
+            }
+            const float sum = wave_sum(s0 + s1);
+            const float mean = (float)((double)sum * invD);
+            const float rnew = fmaf(a.beta2, rold[j], a.one_minus_beta2 * mean);
+#pragma unroll
+            for (int c = 0; c < C; ++c) launder(graw[j][c]);
+            if (!rv[j]) continue;
+            if (lane == 0) a.r[wrow[j]] = rnew;
+            if (!update) continue;
+            const float rc = __builtin_amdgcn_rcpf(fmaf(sqrtf(rnew * a.inv_bias), a.inv_alpha, a.eps_over_alpha));
+#pragma unroll
+            for (int c = 0; c < C; ++c) {
+                const int ch = lane + kWave * c;
+                if (!kExact && ch >= a.total_chunks) continue;
+                float g[EPC], w[EPC], o[EPC];
+                decode(graw[j][c], g);
+                decode(wraw[j][c], w);
+#pragma unroll
+                for (int e = 0; e < EPC; ++e) {
+                    const float upd = fmaf(g[e], rc, w[e]);
+                    o[e] = (g[e] == 0.0f) ? w[e] : upd;
+                }
+                if constexpr (kExact) buf_store<WT, EPC>(wb[j], ch * kWBytes, o);
+                else store_chunk<WT, EPC, EMBER_ROWONLY_NT>(wr[j], (int64_t)ch * EPC, a.D, o);
+            }
+        }
+    }
+}
+
+// Blocks nb.. of the sparse row-only step: beta2 r on every row outside idx,
+// and the row marks cleared (r is left alone when idx was rejected).
+__device__ __forceinline__ void rowonly_decay(const RowOnlyParams& a, int err) {
+    const int64_t i0 = (int64_t)(blockIdx.x - a.nb) * kDecayRows;
+    for (int64_t i = i0 + threadIdx.x; i < i0 + kDecayRows && i < a.V; i += blockDim.x) {
+        const int sl = a.slot[i];
+        if (sl != 0) a.slot[i] = 0;
+        else if (!err) a.r[i] = a.beta2 * a.r[i];
+    }
+}
+
+// Every block of the sparse step has read the error bits before it counts
+// itself; the last one clears them for the next step.
+__device__ __forceinline__ void rowonly_clear_flag(const RowOnlyParams& a, int* last) {
+    if (block_ticket(a.ticket, (int)gridDim.x, last) && threadIdx.x == 0) {
+        *a.flag = 0;
+        *a.ticket = 0;
+    }
+}
+
+// Dense: blocks [0, nb) over the V rows.  Sparse: the same over the n gradient
+// rows (mapped through idx), then the decay blocks.  kExact: D is a multiple
+// of the chunk width, so no chunk is partial.
+template <typename GT, typename WT, int C, bool kSparse, bool kExact>
+__global__ __launch_bounds__(kBlock) void ember_rowonly_wave(RowOnlyParams a) {
+    __shared__ int last;
+    if (!kSparse) {
+        if (blockIdx.x == 0 && threadIdx.x == 0) *a.status = 0;
+        rowonly_wave_rows<GT, WT, C, false, kExact>(a);
+        return;
+    }
+    const int err = *a.flag;
+    if (blockIdx.x == 0 && threadIdx.x == 0) *a.status = err;
+    if ((int)blockIdx.x >= a.nb) rowonly_decay(a, err);
+    else if (!err) rowonly_wave_rows<GT, WT, C, true, kExact>(a);
+    rowonly_clear_flag(a, &last);
+}
+
+// Longer rows: a block of waves per row (see rowonly_rows).
 template <typename GT, typename WT, int M, int S, bool kSparse, bool kResident>
 __global__ __launch_bounds__(kRowOnlyMaxWaves * kWave) void ember_rowonly(RowOnlyParams a) {
     __shared__ float part[kRowOnlyMaxWaves][kRowOnlyRows];
@@ -905,22 +1102,9 @@ __global__ __launch_bounds__(kRowOnlyMaxWaves * kWave) void ember_rowonly(RowOnl
     }
     const int err = *a.flag;
     if (blockIdx.x == 0 && threadIdx.x == 0) *a.status = err;
-    if ((int)blockIdx.x >= a.nb) {
-        const int64_t i0 = (int64_t)(blockIdx.x - a.nb) * kDecayRows;
-        for (int64_t i = i0 + threadIdx.x; i < i0 + kDecayRows && i < a.V; i += blockDim.x) {
-            const int sl = a.slot[i];
-            if (sl != 0) a.slot[i] = 0;
-            else if (!err) a.r[i] = a.beta2 * a.r[i];
-        }
-    } else if (!err) {
-        rowonly_rows<GT, WT, M, S, true, kResident>(a, part, rn_lds);
-    }
-    // Every block has read the error bits: the last one clears them for the
-    // next step.
-    if (block_ticket(a.ticket, (int)gridDim.x, &last) && threadIdx.x == 0) {
-        *a.flag = 0;
-        *a.ticket = 0;
-    }
+    if ((int)blockIdx.x >= a.nb) rowonly_decay(a, err);
+    else if (!err) rowonly_rows<GT, WT, M, S, true, kResident>(a, part, rn_lds);
+    rowonly_clear_flag(a, &last);
 }
 
 // Sparse row-only step, first launch: validates idx and marks the touched rows
@@ -983,6 +1167,36 @@ hipError_t rowonly_dispatch(const RowOnlyParams& p, int m, int spw, bool residen
     else if (m == 2 && spw == 2) ember_rowonly<GT, WT, 2, 2, kSparse, true><<<grid, threads, 0, s>>>(p);
     else return hipErrorInvalidValue;
     return hipGetLastError();
+}
+
+template <typename GT, typename WT, bool kSparse, bool kExact>
+hipError_t rowonly_wave_dispatch_c(const RowOnlyParams& p, int c, dim3 grid, hipStream_t s) {
+    switch (c) {
+    case 1: ember_rowonly_wave<GT, WT, 1, kSparse, kExact><<<grid, kBlock, 0, s>>>(p); break;
+    case 2: ember_rowonly_wave<GT, WT, 2, kSparse, kExact><<<grid, kBlock, 0, s>>>(p); break;
+    case 4: ember_rowonly_wave<GT, WT, 4, kSparse, kExact><<<grid, kBlock, 0, s>>>(p); break;
+    case 8: ember_rowonly_wave<GT, WT, 8, kSparse, kExact><<<grid, kBlock, 0, s>>>(p); break;
+    case 16: ember_rowonly_wave<GT, WT, 16, kSparse, kExact><<<grid, kBlock, 0, s>>>(p); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+template <typename GT, typename WT, bool kSparse>
+hipError_t rowonly_wave_dispatch(const RowOnlyParams& p, int c, dim3 grid, hipStream_t s) {
+    constexpr int EPC = 16 / (int)sizeof(GT);
+    return p.D % EPC == 0 ? rowonly_wave_dispatch_c<GT, WT, kSparse, true>(p, c, grid, s)
+                          : rowonly_wave_dispatch_c<GT, WT, kSparse, false>(p, c, grid, s);
+}
+
+template <bool kSparse>
+hipError_t rowonly_wave_dispatch_t(const RowOnlyParams& p, int g_dtype, int w_dtype, int c, dim3 grid,
+                                   hipStream_t s) {
+    if (g_dtype == 0)
+        return w_dtype == 0 ? rowonly_wave_dispatch<float, float, kSparse>(p, c, grid, s)
+                            : rowonly_wave_dispatch<float, uint16_t, kSparse>(p, c, grid, s);
+    return w_dtype == 0 ? rowonly_wave_dispatch<uint16_t, float, kSparse>(p, c, grid, s)
+                        : rowonly_wave_dispatch<uint16_t, uint16_t, kSparse>(p, c, grid, s);
 }
 
 template <bool kSparse>
@@ -1183,6 +1397,12 @@ hipError_t launch_rowonly(const StepArgs& a, hipStream_t s) {
     const int ndecay = a.sparse ? (int)((a.V + kDecayRows - 1) / kDecayRows) : 0;
     const dim3 grid((unsigned)(p.nb + ndecay));
     if (p.nb + ndecay == 0) return hipSuccess;
+    if (cp.total_chunks <= kRowOnlyWaveChunks) {
+        int c = 1;
+        while (c * kWave < cp.total_chunks) c *= 2;
+        return a.sparse ? rowonly_wave_dispatch_t<true>(p, a.g_dtype, a.w_dtype, c, grid, s)
+                        : rowonly_wave_dispatch_t<false>(p, a.g_dtype, a.w_dtype, c, grid, s);
+    }
     if (a.sparse)
         return rowonly_dispatch_t<true>(p, a.g_dtype, a.w_dtype, cp.m, spw, resident, grid, waves * kWave, s);
     return rowonly_dispatch_t<false>(p, a.g_dtype, a.w_dtype, cp.m, spw, resident, grid, waves * kWave, s);

@@ -54,6 +54,18 @@ constexpr int kWaves = kBlock / kWave;
 #ifndef EMBER_APPLY_WNT
 #define EMBER_APPLY_WNT 1           // non-temporal weight loads in apply
 #endif
+#ifndef EMBER_ROWONLY_ROWS
+#define EMBER_ROWONLY_ROWS 2     // row-only kernel: rows in flight per block
+#endif
+#ifndef EMBER_ROWONLY_RPB
+#define EMBER_ROWONLY_RPB 16     // row-only kernel: rows per block
+#endif
+#ifndef EMBER_ROWONLY_WAVE_ROWS
+#define EMBER_ROWONLY_WAVE_ROWS 2 // row-only kernel, one wave per row: rows in flight per wave
+#endif
+#ifndef EMBER_ROWONLY_NT
+#define EMBER_ROWONLY_NT 1       // row-only kernel: non-temporal G/W loads and W stores
+#endif
 #ifndef EMBER_MAX_BLOCKS
 #define EMBER_MAX_BLOCKS 384        // row blocks of the statistics pass
 #endif

@@ -138,3 +138,14 @@ def algorithmic_bytes(V: int, D: int, w_size: int, g_size: int, rows: int | None
     if rows != V:
         b += 8 * rows
     return b
+
+
+def rowonly_algorithmic_bytes(V: int, D: int, w_size: int, g_size: int, rows: int | None = None) -> int:
+    """HBM bytes one row-only step must move: each row's statistic depends on
+    that row alone, so G is read once; W read and written once on the rows with
+    gradient, r read and written, plus the sparse step's int64 index list."""
+    rows = V if rows is None else rows
+    b = rows * D * (g_size + 2 * w_size) + 8 * V
+    if rows != V:
+        b += 8 * rows
+    return b

@@ -7,7 +7,8 @@ beta2), fp32 W within 1e-5 of max(|oracle|, |W before|), bf16 W within 1 ulp
 or the cancellation bound, W rows outside idx bit-identical.  The shapes cover
 each launch form of the fused kernel: rows held in registers with one or two
 2 KiB slabs per wave (one or two 16-byte chunks per lane), and rows too long to
-hold, which are read twice.
+hold, which are read twice; and rows of up to 1024 chunks handled by one wave
+each (D a multiple of the chunk width or not).
 """
 import numpy as np
 import pytest
@@ -115,6 +116,9 @@ def sparse_lockstep(em, cfg, seed=0, steps=None, shuffle=False):
     (70, 12000, torch.bfloat16, torch.bfloat16, 1),    # twelve slabs: two per wave
     (19, 8200, torch.float32, torch.float32, 0),       # 17 slabs: rows read twice
     (21, 20000, torch.bfloat16, torch.float32, 0),     # 40 slabs: rows read twice
+    (45, 8192, torch.bfloat16, torch.bfloat16, 0),     # one wave per row, 16 chunks per lane
+    (33, 4096, torch.float32, torch.float32, 1),       # the same in fp32
+    (100, 1500, torch.bfloat16, torch.bfloat16, 1),    # one wave per row, ragged, 4 chunks per lane
     (1, 4096, torch.bfloat16, torch.bfloat16, 0),      # one row
     (17, 1, torch.float32, torch.float32, 3),          # one column, odd row count
     (9, 8, torch.bfloat16, torch.bfloat16, 0),         # one partial row block
@@ -177,6 +181,13 @@ def test_rowonly_sparse_every_row(em):
     cfg = wl.Config("ro_sparse", 5000, 320, torch.bfloat16, torch.bfloat16, 4, "sparse_zipf",
                     batch_tokens=3000)
     sparse_lockstep(em, cfg, seed=5, shuffle=True)
+
+
+def test_rowonly_sparse_long_rows(em):
+    # rows too long for one wave: the block form of the fused kernel
+    cfg = wl.Config("ro_sparse_long", 3000, 9000, torch.bfloat16, torch.bfloat16, 2, "sparse_zipf",
+                    batch_tokens=1500)
+    sparse_lockstep(em, cfg, seed=8, shuffle=True)
 
 
 def test_rowonly_sparse_fp32_and_empty_index_list(em):
