@@ -29,6 +29,7 @@ PEAK_GBPS = 8000.0
 V, D = 128256, 4096
 KERNEL_SRC = os.path.join(ROOT, "paper_2607_01455_amd", "csrc", "ember_kernels.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ember_apply_lmhead128k_traffic.txt")
+ROWONLY_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ember_rowonly_lmhead128k_traffic.txt")
 
 
 def parse():
@@ -48,12 +49,12 @@ def kernel_source_hash() -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def traffic_for_current_kernel():
-    """HBM bytes per dense apply launch from the committed PMC summary, if it was
-    taken on the current kernel source (else None)."""
+def traffic_for_current_kernel(path=TRAFFIC_FILE):
+    """HBM bytes per launch of the dense kernel a committed PMC summary covers,
+    if it was taken on the current kernel source (else None)."""
     rec = {}
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(path) as f:
             for line in f:
                 if "=" in line and not line.lstrip().startswith("#"):
                     k, v = line.split("=", 1)
@@ -196,7 +197,9 @@ def row_only_section(ember, wl, torch, dev, K, Wm, W_head, W_emb, grads, batches
         },
         "roofline": {"kernel": "ember_rowonly (dense LM-head step)", "bound": "hbm",
                      "achieved": round(fused_gbps, 1), "peak": PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(fused_gbps / PEAK_GBPS, 4), "avg_launch_ms": round(fused_avg_ms, 5),
+                     "frac": round(fused_gbps / PEAK_GBPS, 4),
+                     "traffic": traffic_for_current_kernel(ROWONLY_TRAFFIC_FILE),
+                     "avg_launch_ms": round(fused_avg_ms, 5),
                      "algorithmic_bytes_per_launch": dense_bytes},
     }
 
