@@ -53,6 +53,8 @@ def _load():
     lib.ember_oracle_f64_to_bf16.restype = ctypes.c_uint16
     lib.ember_oracle_state_bytes.argtypes = [i64, i64]
     lib.ember_oracle_state_bytes.restype = i64
+    lib.ember_oracle_coalesce.argtypes = [vp, i64, vp, i32, i64, i64, i64, vp, vp, i32, i64, vp]
+    lib.ember_oracle_coalesce.restype = i32
     _lib = lib
     return lib
 
@@ -116,6 +118,30 @@ def step(W: np.ndarray, G: np.ndarray, r: np.ndarray, c: np.ndarray | None, t: i
                                  r.ctypes.data, c_ptr, V, D, int(t),
                                  float(lr), float(beta2), float(eps), int(bool(maximize)),
                                  wr_ptr, n_wr, int(bool(row_only)))
+
+
+def coalesce(tok: np.ndarray, U: np.ndarray, V: int, out_dtype=None):
+    """Distinct token ids (ascending) and the float64 sum of their per-position
+    gradient rows in ascending position order, rounded once to ``out_dtype``
+    (``np.float32`` or ``np.uint16`` for bf16 bits; default: U's).  Returns
+    (status, idx int64[n], G [n, D])."""
+    lib = _load()
+    tok = np.ascontiguousarray(tok, dtype=np.int64)
+    P = tok.shape[0]
+    if U.ndim != 2 or U.shape[0] != P:
+        raise ValueError("U must be [len(tok), D]")
+    D = U.shape[1]
+    out_dtype = U.dtype if out_dtype is None else np.dtype(out_dtype)
+    idx = np.zeros(max(P, 1), np.int64)
+    G = np.zeros((max(P, 1), D), out_dtype)
+    n = ctypes.c_int64(-1)
+    u_ptr = U.ctypes.data if U.size else None
+    st = lib.ember_oracle_coalesce(tok.ctypes.data if P else None, P, u_ptr, _dtype_code(U),
+                                   _ld(U) if P else D, int(V), D, idx.ctypes.data, G.ctypes.data,
+                                   _dtype_code(G), _ld(G), ctypes.byref(n))
+    if st != OK:
+        return st, None, None
+    return st, idx[:n.value].copy(), G[:n.value].copy()
 
 
 def bf16_to_f64(bits: int) -> float:

@@ -38,6 +38,10 @@
  *   - idx must hold unique values in [0, V); otherwise the call fails and
  *     modifies nothing.
  *
+ * Gradient coalescing (ember_oracle_coalesce, at the end of this file): the
+ * per-position embedding gradients of a batch summed into one row per distinct
+ * token, the input of the sparse step.
+ *
  * Row-only Ember (row_only = 1).  Section 2.1 describes a variant that keeps
  * only the V row statistics, bias-corrects them and divides each row's
  * gradient by their square root (the ablation table lists it with state V);
@@ -254,5 +258,71 @@ int ember_oracle_step(void* W, int w_dtype, int64_t ldw,
 
     free(grow);
     free(colsum);
+    return ORACLE_OK;
+}
+
+/*
+ * Coalescing of per-position embedding gradients into distinct rows.
+ *
+ * The input-embedding gradient of one position is a one-hot row selector
+ * times the back-propagated signal (appendix "Decomposing the Squared
+ * Gradient"), so the gradient of row i over a batch is the sum of the signals
+ * of the K_i positions holding token i (appendix "The Fisher is Proportional to
+ * Inverse Frequency Squared", where the row gradient is that sum).  This
+ * produces the (idx, G_rows) pair the sparse step takes:
+ *
+ *   idx[0..n)   the distinct values of tok[0..P), ascending;
+ *   G[k][j]     sum over p = 0, 1, ..., P-1 with tok[p] == idx[k] of U[p][j],
+ *               accumulated in float64 in that (ascending position) order and
+ *               rounded once to G's storage type.
+ *
+ * tok[p] must lie in [0, V); otherwise nothing is written and the call
+ * returns ORACLE_BAD_INDEX.  *n_out receives n.  P = 0 gives n = 0.
+ */
+static int cmp_i64(const void* a, const void* b)
+{
+    int64_t x = *(const int64_t*)a, y = *(const int64_t*)b;
+    return (x > y) - (x < y);
+}
+
+int ember_oracle_coalesce(const int64_t* tok, int64_t P, const void* U, int u_dtype, int64_t ldu,
+                          int64_t V, int64_t D, int64_t* idx, void* G, int g_dtype, int64_t ldg,
+                          int64_t* n_out)
+{
+    if (P < 0 || V < 1 || D < 1 || !n_out || (P > 0 && (!tok || !U || !idx || !G)))
+        return ORACLE_BAD_ARG;
+    for (int64_t p = 0; p < P; ++p)
+        if (tok[p] < 0 || tok[p] >= V)
+            return ORACLE_BAD_INDEX;
+    /* distinct ids, ascending */
+    int64_t* ids = (int64_t*)malloc((size_t)(P > 0 ? P : 1) * sizeof(int64_t));
+    if (!ids)
+        return ORACLE_BAD_ARG;
+    memcpy(ids, tok, (size_t)P * sizeof(int64_t));
+    qsort(ids, (size_t)P, sizeof(int64_t), cmp_i64);
+    int64_t n = 0;
+    for (int64_t p = 0; p < P; ++p)
+        if (n == 0 || ids[p] != ids[n - 1])
+            ids[n++] = ids[p];
+    double* acc = (double*)calloc((size_t)(n > 0 ? n : 1) * (size_t)D, sizeof(double));
+    if (!acc) {
+        free(ids);
+        return ORACLE_BAD_ARG;
+    }
+    /* the sums, visiting positions in ascending order */
+    for (int64_t p = 0; p < P; ++p) {
+        const int64_t* hit = (const int64_t*)bsearch(&tok[p], ids, (size_t)n, sizeof(int64_t), cmp_i64);
+        int64_t k = hit - ids;
+        for (int64_t j = 0; j < D; ++j)
+            acc[k * D + j] += load_elem(U, u_dtype, p * ldu + j);
+    }
+    for (int64_t k = 0; k < n; ++k) {
+        idx[k] = ids[k];
+        for (int64_t j = 0; j < D; ++j)
+            store_elem(G, g_dtype, k * ldg + j, acc[k * D + j]);
+    }
+    *n_out = n;
+    free(acc);
+    free(ids);
     return ORACLE_OK;
 }
