@@ -69,9 +69,11 @@ typedef enum {
     EMBER_ERR_HIP = -7        /* a HIP runtime call failed */
 } ember_status;
 
-/* Largest supported V (row indices are kept in 31 bits) and D. */
+/* Largest supported V (row indices are kept in 31 bits) and D, and the
+ * largest token batch of ember_coalesce_rows. */
 #define EMBER_MAX_V ((int64_t)0x7FFFFFFE)
 #define EMBER_MAX_D ((int64_t)(1 << 22))
+#define EMBER_MAX_TOKENS ((int64_t)(1 << 26))
 
 /*
  * Workspace size for a V x D table, valid for every step (dense, sparse,
@@ -171,6 +173,45 @@ int ember_rowonly_step_sparse_rows(void* W, int w_dtype, int64_t ldw,
                                    float* r, int64_t V, int64_t D, int64_t t,
                                    float lr, float beta2, float eps, int maximize,
                                    void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Gradient coalescing: the step before ember_step_sparse_rows.  The gradient
+ * of an input embedding for one batch position is the one-hot selector of its
+ * token times the back-propagated signal (appendix "Decomposing the Squared
+ * Gradient"), so the gradient of row i is the sum of the signals of every
+ * position holding token i (appendix "The Fisher is Proportional to Inverse
+ * Frequency Squared").  Given n_tok token ids tok (device int64, each in
+ * [0, V)) and the per-position signals U (n_tok x D, row stride ldu, dtype
+ * u_dtype), this writes
+ *
+ *   *n_out           n, the number of distinct ids (device int64);
+ *   idx[0..n)        the distinct ids, ascending (device int64[n_tok]);
+ *   G_rows[k][0..D)  for k < n: the sum of U[p] over the positions p with
+ *                    tok[p] == idx[k], accumulated in float64 and rounded once
+ *                    (nearest-even) to g_dtype (device, n_tok x D, stride ldg).
+ *
+ * The sums have a fixed order, so results are reproducible bit for bit: the
+ * positions of one id are added in ascending order, within fixed chunks of the
+ * id-sorted positions, and chunk partials in chunk order.  idx and G_rows feed
+ * ember_step_sparse_rows directly once n is known on the host (read *n_out
+ * after synchronising the stream).  Ids outside [0, V) make the call report
+ * EMBER_ERR_INDEX through ember_get_error on this workspace, with n = 0 and
+ * idx / G_rows unspecified.  n_tok = 0 gives n = 0 (tok, U, idx, G_rows may
+ * then be NULL).  Layout and alignment rules of U and G_rows are those of W
+ * and G; tok, idx and n_out must be 8-byte aligned.
+ *
+ * The workspace (device, 256-byte aligned, ember_coalesce_workspace_bytes of
+ * at least n_tok tokens) needs no initialisation and may be reused by
+ * successive calls on one stream; its size grows with max_tokens (sort
+ * buffers) and with D (float64 partial rows of at most 2^25 elements).
+ */
+int ember_coalesce_workspace_bytes(int64_t max_tokens, int64_t V, int64_t D, size_t* bytes);
+
+int ember_coalesce_rows(const int64_t* tok, int64_t n_tok,
+                        const void* U, int u_dtype, int64_t ldu,
+                        int64_t V, int64_t D,
+                        int64_t* idx, void* G_rows, int g_dtype, int64_t ldg,
+                        int64_t* n_out, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * Device status of the most recent step enqueued with this workspace.

@@ -285,6 +285,48 @@ int ember_rowonly_step_sparse_rows(void* W, int w_dtype, int64_t ldw, const void
     return run_rowonly_step(a, lr, beta2, eps, t, maximize, stream);
 }
 
+int ember_coalesce_workspace_bytes(int64_t max_tokens, int64_t V, int64_t D, size_t* bytes) {
+    if (bytes == nullptr) return EMBER_ERR_ARG;
+    int st = check_shape(V, D);
+    if (st != EMBER_OK) return st;
+    if (max_tokens < 0 || max_tokens > EMBER_MAX_TOKENS) return EMBER_ERR_SHAPE;
+    *bytes = ember::coal_plan(max_tokens, V, D).total;
+    return EMBER_OK;
+}
+
+int ember_coalesce_rows(const int64_t* tok, int64_t n_tok, const void* U, int u_dtype, int64_t ldu,
+                        int64_t V, int64_t D, int64_t* idx, void* G_rows, int g_dtype, int64_t ldg,
+                        int64_t* n_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+    int st = check_shape(V, D);
+    if (st == EMBER_OK && (n_tok < 0 || n_tok > EMBER_MAX_TOKENS)) st = EMBER_ERR_SHAPE;
+    if (st == EMBER_OK) st = check_matrix(U, u_dtype, ldu, D, n_tok == 0);
+    if (st == EMBER_OK) st = check_matrix(G_rows, g_dtype, ldg, D, n_tok == 0);
+    if (st == EMBER_OK && n_tok > 0 && (tok == nullptr || idx == nullptr)) st = EMBER_ERR_ARG;
+    if (st == EMBER_OK && n_out == nullptr) st = EMBER_ERR_ARG;
+    if (st == EMBER_OK && ws == nullptr) st = EMBER_ERR_ARG;
+    if (st == EMBER_OK && ((tok != nullptr && !aligned(tok, 8)) || (idx != nullptr && !aligned(idx, 8)) ||
+                           !aligned(n_out, 8) || !aligned(ws, 256)))
+        st = EMBER_ERR_ALIGN;
+    if (st == EMBER_OK && ws_bytes < ember::coal_plan(n_tok, V, D).total) st = EMBER_ERR_WORKSPACE;
+    if (st != EMBER_OK) return st;
+    ember::CoalArgs a;
+    a.tok = tok;
+    a.P = n_tok;
+    a.U = U;
+    a.u_dtype = u_dtype;
+    a.ldu = ldu;
+    a.V = V;
+    a.D = D;
+    a.idx = idx;
+    a.G = G_rows;
+    a.g_dtype = g_dtype;
+    a.ldg = ldg;
+    a.n_out = n_out;
+    a.ws = static_cast<char*>(ws);
+    hipError_t e = timed("ember_coalesce", stream, [&] { return ember::launch_coalesce(a, stream); });
+    return e == hipSuccess ? EMBER_OK : EMBER_ERR_HIP;
+}
+
 int ember_get_error(const void* ws, hipStream_t stream, int* device_status) {
     if (ws == nullptr || device_status == nullptr) return EMBER_ERR_ARG;
     if (!aligned(ws, 256)) return EMBER_ERR_ALIGN;

@@ -1,0 +1,664 @@
+// Coalescing of per-position token gradients into the (idx, G_rows) input of the
+// sparse Ember step, on the GPU.
+//
+// The input-embedding gradient of one batch position is a one-hot row selector
+// times the back-propagated signal (appendix "Decomposing the Squared
+// Gradient"); the gradient of row i is the sum of the signals of the positions
+// holding token i (appendix "The Fisher is Proportional to Inverse Frequency
+// Squared").  Given token ids tok[P] and per-position rows U[P][D]:
+//
+//   idx[0..n)  the distinct ids, ascending;
+//   G[k][j]    the sum of U[p][j] over the positions p with tok[p] == idx[k],
+//              in float64, rounded once to G's type.
+//
+// Pipeline (all integer work is exact and order-independent; every floating
+// point sum has a fixed order):
+//   1. stable LSD radix sort of (id, position) pairs by id, 1-3 passes of up
+//      to 8 bits (digit histograms per tile, offsets, stable scatter ranked with
+//      wavefront ballots), so the positions of one id stay ascending;
+//   2. head flags of the sorted ids -> distinct ids, segment starts, and the
+//      segment number of every sorted entry;
+//   3. the sums: the sorted entries are cut into chunks of L positions; a
+//      wavefront sums one chunk for 256 columns in float64, position by
+//      position, and writes every segment that lies inside the chunk; the
+//      pieces of segments that cross chunk boundaries go to float64 partial
+//      rows, which a last launch adds in chunk order.
+// A segment inside one chunk is therefore summed exactly in ascending
+// position order; a longer one is summed in that order within each chunk and
+// then chunk by chunk.
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "ember_launch.h"
+
+namespace ember {
+namespace {
+
+constexpr int kCoalThreads = 256;                    // 4 wavefronts
+constexpr int kCoalWaves = kCoalThreads / kWave;
+constexpr int kCoalItems = EMBER_COAL_ITEMS;         // keys per thread per tile
+constexpr int kTile = kCoalThreads * kCoalItems;     // keys per tile
+constexpr int kMaxBins = 256;                        // digits of up to 8 bits
+constexpr int kInBlockOffsetTiles = 64;              // up to this many tiles the
+                                                     // scatter derives its own offsets
+constexpr int kRunRows = 32;                         // rows a wavefront holds at once
+constexpr int kMaxChunks = 4096;                     // bound on the chunks ...
+constexpr int64_t kMaxPartialElems = (int64_t)1 << 25; // ... and on chunks x D
+constexpr int kColsPerLane = 4;
+constexpr int kSlabCols = kWave * kColsPerLane;      // columns per wavefront
+
+struct SortPass {
+    const int64_t* tok;       // first pass: token ids (clamped into [0, V); tiles flag bad ones)
+    const uint32_t* keys_in;  // later passes
+    const uint32_t* vals_in;
+    uint32_t* keys_out;
+    uint32_t* vals_out;
+    int64_t P;
+    int64_t V;
+    int shift;
+    int bits;
+    int ntiles;
+    uint32_t* hist;           // [bins][ntiles] digit counts per tile
+    const uint32_t* offs;     // [bins][ntiles] exclusive offsets, or null (derived in the block)
+    uint32_t* tile_bad;       // first pass: 1 where the tile holds an id outside [0, V)
+};
+
+__device__ __forceinline__ uint32_t key_of(const SortPass& a, int64_t i, int& bad) {
+    if (a.tok == nullptr) return a.keys_in[i];
+    const int64_t id = a.tok[i];
+    if (id < 0) { bad = 1; return 0u; }
+    if (id >= a.V) { bad = 1; return (uint32_t)(a.V - 1); }
+    return (uint32_t)id;
+}
+
+// Digit histogram of one tile.  The first pass also records whether the tile
+// holds an invalid id (a plain store per tile: no flag to reset).
+__global__ __launch_bounds__(kCoalThreads) void coal_hist(SortPass a) {
+    __shared__ uint32_t h[kMaxBins];
+    __shared__ int any_bad;
+    const int bins = 1 << a.bits;
+    for (int b = threadIdx.x; b < bins; b += kCoalThreads) h[b] = 0;
+    if (threadIdx.x == 0) any_bad = 0;
+    __syncthreads();
+    const int64_t base = (int64_t)blockIdx.x * kTile;
+    int bad = 0;
+    for (int j = 0; j < kCoalItems; ++j) {
+        const int64_t i = base + (int64_t)j * kCoalThreads + threadIdx.x;
+        if (i < a.P) {
+            const uint32_t key = key_of(a, i, bad);
+            atomicAdd(&h[(key >> a.shift) & (uint32_t)(bins - 1)], 1u);
+        }
+    }
+    if (bad) any_bad = 1;
+    __syncthreads();
+    for (int b = threadIdx.x; b < bins; b += kCoalThreads)
+        a.hist[(int64_t)b * a.ntiles + blockIdx.x] = h[b];
+    if (a.tok != nullptr && threadIdx.x == 0) a.tile_bad[blockIdx.x] = (uint32_t)any_bad;
+}
+
+// Exclusive prefix sums of n counts with one block (integer: exact).
+__global__ __launch_bounds__(1024) void coal_scan(const uint32_t* in, uint32_t* out, int64_t n) {
+    __shared__ uint32_t part[1024];
+    const int t = threadIdx.x;
+    const int64_t per = (n + 1023) / 1024;
+    const int64_t b0 = min(n, (int64_t)t * per);
+    const int64_t b1 = min(n, b0 + per);
+    uint32_t s = 0;
+    for (int64_t i = b0; i < b1; ++i) s += in[i];
+    part[t] = s;
+    __syncthreads();
+    for (int off = 1; off < 1024; off <<= 1) {
+        const uint32_t v = t >= off ? part[t - off] : 0u;
+        __syncthreads();
+        part[t] += v;
+        __syncthreads();
+    }
+    uint32_t run = part[t] - s;
+    for (int64_t i = b0; i < b1; ++i) {
+        const uint32_t x = in[i];
+        out[i] = run;
+        run += x;
+    }
+}
+
+// Exclusive scan of one value per thread over the block (256 threads).
+__device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* lds, uint32_t* total) {
+    const int t = threadIdx.x;
+    lds[t] = v;
+    __syncthreads();
+    for (int off = 1; off < kCoalThreads; off <<= 1) {
+        const uint32_t x = t >= off ? lds[t - off] : 0u;
+        __syncthreads();
+        lds[t] += x;
+        __syncthreads();
+    }
+    const uint32_t incl = lds[t];
+    *total = lds[kCoalThreads - 1];
+    __syncthreads();
+    return incl - v;
+}
+
+// Stable scatter of one tile by the current digit.  Tile keys are taken in
+// position order (item j of thread t is key base + j * 256 + t); within each
+// group of 256 keys a key's rank among equal digits is the number of equal
+// digits in lower lanes of its wavefront (from one ballot per digit bit) plus
+// the counts of that digit in lower wavefronts and in earlier groups.
+__global__ __launch_bounds__(kCoalThreads) void coal_scatter(SortPass a) {
+    __shared__ uint32_t off[kMaxBins];
+    __shared__ uint32_t run[kMaxBins];
+    __shared__ uint32_t wcnt[kCoalWaves][kMaxBins];
+    __shared__ uint32_t wexcl[kCoalWaves][kMaxBins];
+    __shared__ uint32_t scan_lds[kCoalThreads];
+    const int bins = 1 << a.bits;
+    const int tile = blockIdx.x;
+    const int t = threadIdx.x;
+    const int lane = t & (kWave - 1);
+    const int wave = t / kWave;
+
+    if (a.offs != nullptr) {
+        for (int b = t; b < bins; b += kCoalThreads) off[b] = a.offs[(int64_t)b * a.ntiles + tile];
+    } else {
+        // offset of digit b in this tile = keys of smaller digits in every tile
+        // + keys of digit b in earlier tiles
+        uint32_t tot = 0, before = 0;
+        if (t < bins) {
+            for (int k = 0; k < a.ntiles; ++k) {
+                const uint32_t c = a.hist[(int64_t)t * a.ntiles + k];
+                tot += c;
+                if (k < tile) before += c;
+            }
+        }
+        uint32_t all;
+        const uint32_t excl = block_excl_scan(tot, scan_lds, &all);
+        if (t < bins) off[t] = excl + before;
+    }
+    for (int b = t; b < bins; b += kCoalThreads) {
+        run[b] = 0;
+#pragma unroll
+        for (int w = 0; w < kCoalWaves; ++w) wcnt[w][b] = 0;
+    }
+    __syncthreads();
+
+    const uint64_t below = lane == 0 ? 0ull : (~0ull >> (kWave - lane));
+    const int64_t base = (int64_t)tile * kTile;
+    for (int j = 0; j < kCoalItems; ++j) {
+        const int64_t i = base + (int64_t)j * kCoalThreads + t;
+        const bool valid = i < a.P;
+        uint32_t key = 0, val = 0;
+        int bad = 0;
+        if (valid) {
+            key = key_of(a, i, bad);
+            val = a.tok != nullptr ? (uint32_t)i : a.vals_in[i];
+        }
+        const uint32_t d = (key >> a.shift) & (uint32_t)(bins - 1);
+        uint64_t peers = __ballot(valid);
+        for (int b = 0; b < a.bits; ++b) {
+            const bool bit = (d >> b) & 1u;
+            const uint64_t m = __ballot(bit);
+            peers &= bit ? m : ~m;
+        }
+        const uint32_t rank = (uint32_t)__popcll(peers & below);
+        if (valid && rank == 0) wcnt[wave][d] = (uint32_t)__popcll(peers);
+        __syncthreads();
+        for (int b = t; b < bins; b += kCoalThreads) {
+            uint32_t r = run[b];
+#pragma unroll
+            for (int w = 0; w < kCoalWaves; ++w) {
+                wexcl[w][b] = r;
+                r += wcnt[w][b];
+                wcnt[w][b] = 0;
+            }
+            run[b] = r;
+        }
+        __syncthreads();
+        if (valid) {
+            const uint32_t dst = off[d] + wexcl[wave][d] + rank;
+            a.keys_out[dst] = key;
+            a.vals_out[dst] = val;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// distinct ids and segments of the sorted keys
+// ---------------------------------------------------------------------------
+
+struct HeadParams {
+    const uint32_t* K;        // sorted ids
+    int64_t P;
+    int ntiles;
+    uint32_t* tilecnt;        // heads per tile
+    const uint32_t* tileoff;  // exclusive offsets, or null (derived in the block)
+    uint32_t* uid;            // [P] segment number of every sorted entry
+    uint32_t* seg_start;      // [n + 1]
+    int64_t* idx;             // [n] the distinct ids
+    int64_t* n_out;
+};
+
+__device__ __forceinline__ bool is_head(const uint32_t* K, int64_t k) { return k == 0 || K[k] != K[k - 1]; }
+
+// Tiles here are kTile consecutive sorted entries, kCoalItems per thread.
+__global__ __launch_bounds__(kCoalThreads) void coal_heads_count(HeadParams a) {
+    __shared__ uint32_t lds[kCoalThreads];
+    const int64_t k0 = (int64_t)blockIdx.x * kTile + (int64_t)threadIdx.x * kCoalItems;
+    uint32_t c = 0;
+    for (int e = 0; e < kCoalItems; ++e)
+        if (k0 + e < a.P && is_head(a.K, k0 + e)) ++c;
+    uint32_t total;
+    (void)block_excl_scan(c, lds, &total);
+    if (threadIdx.x == 0) a.tilecnt[blockIdx.x] = total;
+}
+
+__global__ __launch_bounds__(kCoalThreads) void coal_heads_write(HeadParams a) {
+    __shared__ uint32_t lds[kCoalThreads];
+    __shared__ uint32_t tile_base;
+    if (a.tileoff != nullptr) {
+        if (threadIdx.x == 0) tile_base = a.tileoff[blockIdx.x];
+    } else {
+        uint32_t s = 0;
+        for (int k = threadIdx.x; k < (int)blockIdx.x; k += kCoalThreads) s += a.tilecnt[k];
+        uint32_t total;
+        (void)block_excl_scan(s, lds, &total);
+        if (threadIdx.x == 0) tile_base = total;
+    }
+    __syncthreads();
+    const int64_t k0 = (int64_t)blockIdx.x * kTile + (int64_t)threadIdx.x * kCoalItems;
+    uint32_t c = 0;
+    for (int e = 0; e < kCoalItems; ++e)
+        if (k0 + e < a.P && is_head(a.K, k0 + e)) ++c;
+    uint32_t total;
+    const uint32_t excl = block_excl_scan(c, lds, &total);
+    uint32_t u = tile_base + excl;   // segment number of the next head
+    for (int e = 0; e < kCoalItems; ++e) {
+        const int64_t k = k0 + e;
+        if (k >= a.P) break;
+        if (is_head(a.K, k)) {
+            a.idx[u] = (int64_t)a.K[k];
+            a.seg_start[u] = (uint32_t)k;
+            ++u;
+        }
+        a.uid[k] = u - 1;
+    }
+    if (blockIdx.x == a.ntiles - 1 && threadIdx.x == 0) {
+        const uint32_t n = tile_base + total;
+        a.seg_start[n] = (uint32_t)a.P;
+        *a.n_out = (int64_t)n;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// the sums
+// ---------------------------------------------------------------------------
+
+struct SumParams {
+    const uint32_t* K;
+    const uint32_t* pos;      // sorted positions
+    const uint32_t* uid;
+    const uint32_t* seg_start;
+    const void* U;
+    int64_t ldu;
+    void* G;
+    int64_t ldg;
+    int64_t P;
+    int64_t D;
+    int64_t L;                // chunk length (a multiple of kRunRows)
+    int nchunks;
+    int nslabs;
+    double* partA;            // [nchunks][D]: the first segment of a chunk, begun in an earlier chunk
+    double* partB;            // [nchunks][D]: the last segment, continued in a later chunk
+    const uint32_t* tile_bad;
+    int ntiles;
+    int* status;
+    int64_t* n_out;
+};
+
+template <typename T> struct Cols;
+template <> struct Cols<float> {
+    using raw = uint32_t __attribute__((ext_vector_type(4)));
+    static __device__ __forceinline__ void widen(const raw& r, double (&x)[kColsPerLane]) {
+        x[0] = (double)__uint_as_float(r.x); x[1] = (double)__uint_as_float(r.y);
+        x[2] = (double)__uint_as_float(r.z); x[3] = (double)__uint_as_float(r.w);
+    }
+    static __device__ __forceinline__ float elem(const float* p) { return *p; }
+};
+template <> struct Cols<uint16_t> {
+    using raw = uint32_t __attribute__((ext_vector_type(2)));
+    static __device__ __forceinline__ void widen(const raw& r, double (&x)[kColsPerLane]) {
+        x[0] = (double)__uint_as_float(r.x << 16); x[1] = (double)__uint_as_float(r.x & 0xFFFF0000u);
+        x[2] = (double)__uint_as_float(r.y << 16); x[3] = (double)__uint_as_float(r.y & 0xFFFF0000u);
+    }
+    static __device__ __forceinline__ float elem(const uint16_t* p) { return __uint_as_float((uint32_t)*p << 16); }
+};
+
+// float64 -> bf16, one round-to-nearest-even: round to fp32 with round-to-odd
+// (the truncation, with its last bit set when inexact), then to bf16 with
+// round-to-nearest-even; fp32 keeps 16 more bits than bf16, so the result is
+// the correctly rounded one (Boldo and Melquiond, "When double rounding is
+// odd", 2005).
+__device__ __forceinline__ uint16_t f64_to_bf16(double x) {
+    float f = (float)x;
+    uint32_t b = __float_as_uint(f);
+    if ((double)f != x && x == x) {
+        if (fabs((double)f) > fabs(x)) b -= 1;   // rounded away from zero: step back
+        b |= 1u;
+        f = __uint_as_float(b);
+    }
+    if ((b & 0x7F800000u) == 0x7F800000u && (b & 0x007FFFFFu) != 0u) return (uint16_t)((b >> 16) | 0x0040u);
+    return (uint16_t)((b + 0x7FFFu + ((b >> 16) & 1u)) >> 16);
+}
+
+template <typename GT>
+__device__ __forceinline__ void store_cols(void* G, int64_t ldg, uint32_t u, int64_t col, int64_t D,
+                                           const double (&x)[kColsPerLane]) {
+    GT* row = static_cast<GT*>(G) + (int64_t)u * ldg;
+#pragma unroll
+    for (int e = 0; e < kColsPerLane; ++e) {
+        if (col + e < D) {
+            if constexpr (sizeof(GT) == 4) row[col + e] = (float)x[e];
+            else row[col + e] = f64_to_bf16(x[e]);
+        }
+    }
+}
+
+template <typename UT>
+__device__ __forceinline__ void load_cols(const UT* row, int64_t col, int64_t D, bool valid,
+                                          typename Cols<UT>::raw& r) {
+    using raw = typename Cols<UT>::raw;
+    r = raw{};
+    if (!valid) return;
+    if (col + kColsPerLane <= D) {
+        r = *reinterpret_cast<const raw*>(row + col);
+    } else {
+        UT tmp[kColsPerLane] = {};
+        for (int e = 0; e < kColsPerLane; ++e)
+            if (col + e < D) tmp[e] = row[col + e];
+        r = *reinterpret_cast<const raw*>(tmp);
+    }
+}
+
+// One wavefront per (chunk, 256-column slab); slabs of a chunk are adjacent.
+// kExact (D a multiple of 4): the wavefront loads kRunRows rows at a time into
+// registers before adding them; otherwise one row at a time.
+template <typename UT, typename GT, bool kExact>
+__global__ __launch_bounds__(kCoalThreads) void coal_segsum(SumParams a) {
+    using raw = typename Cols<UT>::raw;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int item = blockIdx.x * kCoalWaves + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int c = item / a.nslabs;
+    if (c >= a.nchunks) return;
+    const int slab = item - c * a.nslabs;
+    const int64_t col = (int64_t)slab * kSlabCols + (int64_t)lane * kColsPerLane;
+    const bool col_ok = col < a.D;
+    const int64_t k0 = (int64_t)c * a.L;
+    const int64_t k1 = min(a.P, k0 + a.L);
+    const UT* U = static_cast<const UT*>(a.U);
+    const bool began_before = k0 > 0 && a.K[k0] == a.K[k0 - 1];
+    const bool ends_after = k1 < a.P && a.K[k1] == a.K[k1 - 1];
+
+    double acc[kColsPerLane] = {0.0, 0.0, 0.0, 0.0};
+    int64_t run0 = k0;
+    auto flush = [&](int64_t rs, int64_t re) {
+        const bool first = rs == k0 && began_before;
+        const bool last = re == k1 && ends_after;
+        if (!col_ok) return;
+        if (!first && !last) {
+            store_cols<GT>(a.G, a.ldg, a.uid[rs], col, a.D, acc);
+        } else {
+            double* dst = (first ? a.partA : a.partB) + (int64_t)c * a.D;
+#pragma unroll
+            for (int e = 0; e < kColsPerLane; ++e)
+                if (col + e < a.D) dst[col + e] = acc[e];
+        }
+    };
+    auto add_row = [&](int64_t k, const raw& r) {
+        if (k > run0 && a.K[k] != a.K[k - 1]) {
+            flush(run0, k);
+#pragma unroll
+            for (int e = 0; e < kColsPerLane; ++e) acc[e] = 0.0;
+            run0 = k;
+        }
+        double x[kColsPerLane];
+        Cols<UT>::widen(r, x);
+#pragma unroll
+        for (int e = 0; e < kColsPerLane; ++e) acc[e] += x[e];
+    };
+    if constexpr (kExact) {
+        for (int64_t s0 = k0; s0 < k1; s0 += kRunRows) {
+            raw rows[kRunRows];
+#pragma unroll
+            for (int r = 0; r < kRunRows; ++r) {
+                const int64_t k = s0 + r;
+                rows[r] = raw{};
+                if (k < k1 && col_ok)
+                    rows[r] = *reinterpret_cast<const raw*>(U + (int64_t)a.pos[k] * a.ldu + col);
+            }
+#pragma unroll
+            for (int r = 0; r < kRunRows; ++r)
+                if (s0 + r < k1) add_row(s0 + r, rows[r]);
+        }
+    } else {
+        for (int64_t k = k0; k < k1; ++k) {
+            raw r;
+            load_cols<UT>(U + (int64_t)a.pos[k] * a.ldu, col, a.D, col_ok, r);
+            add_row(k, r);
+        }
+    }
+    flush(run0, k1);
+}
+
+// Segments that cross chunk boundaries: the wavefront of the chunk where such
+// a segment ends adds its pieces in chunk order.  Block 0 also turns the
+// tiles' index-error marks into the status word (n = 0 on error).
+template <typename GT>
+__global__ __launch_bounds__(kCoalThreads) void coal_fixup(SumParams a) {
+    if (blockIdx.x == 0) {
+        __shared__ uint32_t bad_lds[kCoalThreads];
+        uint32_t bad = 0;
+        for (int k = threadIdx.x; k < a.ntiles; k += kCoalThreads) bad |= a.tile_bad[k];
+        bad_lds[threadIdx.x] = bad;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            uint32_t any = 0;
+            for (int k = 0; k < kCoalThreads; ++k) any |= bad_lds[k];
+            *a.status = any ? 1 : 0;
+            if (any) *a.n_out = 0;
+        }
+    }
+    const int lane = threadIdx.x & (kWave - 1);
+    const int item = blockIdx.x * kCoalWaves + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int c = item / a.nslabs;
+    if (c >= a.nchunks) return;
+    const int slab = item - c * a.nslabs;
+    const int64_t k0 = (int64_t)c * a.L;
+    if (k0 == 0 || a.K[k0] != a.K[k0 - 1]) return;          // first segment begins here
+    const int64_t k1 = min(a.P, k0 + a.L);
+    if (k1 < a.P && a.K[k1] == a.K[k0]) return;              // it continues past this chunk
+    const int64_t col = (int64_t)slab * kSlabCols + (int64_t)lane * kColsPerLane;
+    if (col >= a.D) return;
+    const uint32_t u = a.uid[k0];
+    const int c0 = (int)(a.seg_start[u] / a.L);
+    double acc[kColsPerLane];
+    const double* b = a.partB + (int64_t)c0 * a.D;
+#pragma unroll
+    for (int e = 0; e < kColsPerLane; ++e) acc[e] = col + e < a.D ? b[col + e] : 0.0;
+    for (int cc = c0 + 1; cc <= c; ++cc) {
+        const double* p = a.partA + (int64_t)cc * a.D;
+#pragma unroll
+        for (int e = 0; e < kColsPerLane; ++e)
+            if (col + e < a.D) acc[e] += p[col + e];
+    }
+    store_cols<GT>(a.G, a.ldg, u, col, a.D, acc);
+}
+
+// P == 0: no rows, no error.
+__global__ void coal_empty(int* status, int64_t* n_out) {
+    *status = 0;
+    *n_out = 0;
+}
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+int bits_for(int64_t V) {
+    int b = 0;
+    while (b < 31 && ((int64_t)1 << b) < V) ++b;
+    return b < 1 ? 1 : b;
+}
+
+} // namespace
+
+CoalPlan coal_plan(int64_t P, int64_t V, int64_t D) {
+    CoalPlan c;
+    c.ntiles = (int)((P + kTile - 1) / kTile);
+    const int bits = bits_for(V);
+    c.passes = (bits + 7) / 8;
+    c.digit_bits = (bits + c.passes - 1) / c.passes;
+    int64_t maxc = kMaxPartialElems / (D > 0 ? D : 1);
+    maxc = maxc < 1 ? 1 : (maxc > kMaxChunks ? kMaxChunks : maxc);
+    const int64_t m = (P + (int64_t)kRunRows * maxc - 1) / ((int64_t)kRunRows * maxc);
+    c.L = (int64_t)kRunRows * (m < 1 ? 1 : m);
+    c.nchunks = (int)((P + c.L - 1) / c.L);
+    c.nslabs = (int)((D + kSlabCols - 1) / kSlabCols);
+    size_t off = 256;   // status words, shared layout with the step workspace
+    const size_t nt = (size_t)(c.ntiles > 0 ? c.ntiles : 1);
+    const size_t np = (size_t)(P > 0 ? P : 1);
+    c.keys_a = off; off = align256(off + np * 4);
+    c.vals_a = off; off = align256(off + np * 4);
+    c.keys_b = off; off = align256(off + np * 4);
+    c.vals_b = off; off = align256(off + np * 4);
+    c.hist = off; off = align256(off + (size_t)kMaxBins * nt * 4);
+    c.offs = off; off = align256(off + (size_t)kMaxBins * nt * 4);
+    c.tile_bad = off; off = align256(off + nt * 4);
+    c.tilecnt = off; off = align256(off + nt * 4);
+    c.tileoff = off; off = align256(off + nt * 4);
+    c.uid = off; off = align256(off + np * 4);
+    c.seg_start = off; off = align256(off + (np + 1) * 4);
+    const size_t nc = (size_t)(c.nchunks > 0 ? c.nchunks : 1);
+    c.part_a = off; off = align256(off + nc * (size_t)D * 8);
+    c.part_b = off; off = align256(off + nc * (size_t)D * 8);
+    c.total = off;
+    return c;
+}
+
+hipError_t launch_coalesce(const CoalArgs& a, hipStream_t s) {
+    const CoalPlan c = coal_plan(a.P, a.V, a.D);
+    char* ws = a.ws;
+    int* status = reinterpret_cast<int*>(ws + 4);
+    if (a.P == 0) {
+        coal_empty<<<1, 1, 0, s>>>(status, a.n_out);
+        return hipGetLastError();
+    }
+    uint32_t* ka = reinterpret_cast<uint32_t*>(ws + c.keys_a);
+    uint32_t* va = reinterpret_cast<uint32_t*>(ws + c.vals_a);
+    uint32_t* kb = reinterpret_cast<uint32_t*>(ws + c.keys_b);
+    uint32_t* vb = reinterpret_cast<uint32_t*>(ws + c.vals_b);
+    uint32_t* hist = reinterpret_cast<uint32_t*>(ws + c.hist);
+    uint32_t* offs = reinterpret_cast<uint32_t*>(ws + c.offs);
+    uint32_t* tile_bad = reinterpret_cast<uint32_t*>(ws + c.tile_bad);
+    const bool in_block = c.ntiles <= kInBlockOffsetTiles;
+
+    // 1. sort
+    const uint32_t* kin = nullptr;
+    const uint32_t* vin = nullptr;
+    for (int q = 0; q < c.passes; ++q) {
+        SortPass p;
+        p.tok = q == 0 ? a.tok : nullptr;
+        p.keys_in = kin;
+        p.vals_in = vin;
+        p.keys_out = (q & 1) ? kb : ka;
+        p.vals_out = (q & 1) ? vb : va;
+        p.P = a.P;
+        p.V = a.V;
+        p.shift = q * c.digit_bits;
+        p.bits = c.digit_bits;
+        p.ntiles = c.ntiles;
+        p.hist = hist;
+        p.offs = in_block ? nullptr : offs;
+        p.tile_bad = tile_bad;
+        coal_hist<<<c.ntiles, kCoalThreads, 0, s>>>(p);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        if (!in_block) {
+            coal_scan<<<1, 1024, 0, s>>>(hist, offs, (int64_t)c.ntiles << p.bits);
+            e = hipGetLastError();
+            if (e != hipSuccess) return e;
+        }
+        coal_scatter<<<c.ntiles, kCoalThreads, 0, s>>>(p);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        kin = p.keys_out;
+        vin = p.vals_out;
+    }
+
+    // 2. distinct ids and segments
+    HeadParams h;
+    h.K = kin;
+    h.P = a.P;
+    h.ntiles = c.ntiles;
+    h.tilecnt = reinterpret_cast<uint32_t*>(ws + c.tilecnt);
+    h.tileoff = in_block ? nullptr : reinterpret_cast<uint32_t*>(ws + c.tileoff);
+    h.uid = reinterpret_cast<uint32_t*>(ws + c.uid);
+    h.seg_start = reinterpret_cast<uint32_t*>(ws + c.seg_start);
+    h.idx = a.idx;
+    h.n_out = a.n_out;
+    coal_heads_count<<<c.ntiles, kCoalThreads, 0, s>>>(h);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (!in_block) {
+        coal_scan<<<1, 1024, 0, s>>>(h.tilecnt, reinterpret_cast<uint32_t*>(ws + c.tileoff), c.ntiles);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    coal_heads_write<<<c.ntiles, kCoalThreads, 0, s>>>(h);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+
+    // 3. sums
+    SumParams m;
+    m.K = kin;
+    m.pos = vin;
+    m.uid = h.uid;
+    m.seg_start = h.seg_start;
+    m.U = a.U;
+    m.ldu = a.ldu;
+    m.G = a.G;
+    m.ldg = a.ldg;
+    m.P = a.P;
+    m.D = a.D;
+    m.L = c.L;
+    m.nchunks = c.nchunks;
+    m.nslabs = c.nslabs;
+    m.partA = reinterpret_cast<double*>(ws + c.part_a);
+    m.partB = reinterpret_cast<double*>(ws + c.part_b);
+    m.tile_bad = tile_bad;
+    m.ntiles = c.ntiles;
+    m.status = status;
+    m.n_out = a.n_out;
+    const int64_t items = (int64_t)c.nchunks * c.nslabs;
+    const unsigned grid = (unsigned)((items + kCoalWaves - 1) / kCoalWaves);
+    const bool exact = a.D % kColsPerLane == 0;
+    if (a.u_dtype == 0) {
+        if (a.g_dtype == 0) {
+            if (exact) coal_segsum<float, float, true><<<grid, kCoalThreads, 0, s>>>(m);
+            else coal_segsum<float, float, false><<<grid, kCoalThreads, 0, s>>>(m);
+        } else {
+            if (exact) coal_segsum<float, uint16_t, true><<<grid, kCoalThreads, 0, s>>>(m);
+            else coal_segsum<float, uint16_t, false><<<grid, kCoalThreads, 0, s>>>(m);
+        }
+    } else {
+        if (a.g_dtype == 0) {
+            if (exact) coal_segsum<uint16_t, float, true><<<grid, kCoalThreads, 0, s>>>(m);
+            else coal_segsum<uint16_t, float, false><<<grid, kCoalThreads, 0, s>>>(m);
+        } else {
+            if (exact) coal_segsum<uint16_t, uint16_t, true><<<grid, kCoalThreads, 0, s>>>(m);
+            else coal_segsum<uint16_t, uint16_t, false><<<grid, kCoalThreads, 0, s>>>(m);
+        }
+    }
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (a.g_dtype == 0) coal_fixup<float><<<grid, kCoalThreads, 0, s>>>(m);
+    else coal_fixup<uint16_t><<<grid, kCoalThreads, 0, s>>>(m);
+    return hipGetLastError();
+}
+
+} // namespace ember

@@ -66,6 +66,9 @@ constexpr int kWaves = kBlock / kWave;
 #ifndef EMBER_ROWONLY_NT
 #define EMBER_ROWONLY_NT 1       // row-only kernel: non-temporal G/W loads and W stores
 #endif
+#ifndef EMBER_COAL_ITEMS
+#define EMBER_COAL_ITEMS 4       // gradient coalescing: keys per thread per sort tile
+#endif
 #ifndef EMBER_MAX_BLOCKS
 #define EMBER_MAX_BLOCKS 384        // row blocks of the statistics pass
 #endif
@@ -166,5 +169,37 @@ hipError_t launch_apply(const StepArgs& a, hipStream_t s);
 // validates idx and marks the touched rows).
 hipError_t launch_rowonly_validate(const StepArgs& a, hipStream_t s);
 hipError_t launch_rowonly(const StepArgs& a, hipStream_t s);
+
+// Gradient coalescing (ember_coalesce.hip): token ids and per-position rows
+// -> distinct ids and summed rows.
+struct CoalArgs {
+    const int64_t* tok;
+    int64_t P;
+    const void* U;
+    int u_dtype;
+    int64_t ldu;
+    int64_t V;
+    int64_t D;
+    int64_t* idx;
+    void* G;
+    int g_dtype;
+    int64_t ldg;
+    int64_t* n_out;
+    char* ws;
+};
+
+struct CoalPlan {
+    int ntiles;        // sort tiles
+    int passes;        // radix passes
+    int digit_bits;
+    int64_t L;         // chunk length of the sums
+    int nchunks;
+    int nslabs;
+    size_t keys_a, vals_a, keys_b, vals_b, hist, offs, tile_bad, tilecnt, tileoff, uid, seg_start;
+    size_t part_a, part_b;
+    size_t total;      // workspace bytes
+};
+CoalPlan coal_plan(int64_t P, int64_t V, int64_t D);
+hipError_t launch_coalesce(const CoalArgs& a, hipStream_t s);
 
 } // namespace ember

@@ -30,7 +30,8 @@ EMBER_ERR_HIP = -7
 # Every function the C header declares, checked by the CPU test suite.
 EXPORTED = ("ember_workspace_bytes", "ember_init_state", "ember_step_dense",
             "ember_step_sparse_rows", "ember_rowonly_init_state", "ember_rowonly_step_dense",
-            "ember_rowonly_step_sparse_rows", "ember_get_error", "ember_strerror",
+            "ember_rowonly_step_sparse_rows", "ember_coalesce_workspace_bytes", "ember_coalesce_rows",
+            "ember_get_error", "ember_strerror",
             "ember_profile_enable", "ember_profile_collect")
 
 
@@ -60,6 +61,8 @@ def _load(path: str = _LIB_PATH) -> ctypes.CDLL:
                                              f32, f32, f32, i32, vp, sz, vp]
     lib.ember_rowonly_step_sparse_rows.argtypes = [vp, i32, i64, vp, i32, i64, vp, i64, vp, i64, i64, i64,
                                                    f32, f32, f32, i32, vp, sz, vp]
+    lib.ember_coalesce_workspace_bytes.argtypes = [i64, i64, i64, ctypes.POINTER(sz)]
+    lib.ember_coalesce_rows.argtypes = [vp, i64, vp, i32, i64, i64, i64, vp, vp, i32, i64, vp, vp, sz, vp]
     lib.ember_get_error.argtypes = [vp, vp, ctypes.POINTER(i32)]
     lib.ember_strerror.argtypes = [i32]
     lib.ember_strerror.restype = ctypes.c_char_p
@@ -85,7 +88,12 @@ def _dtype(t: torch.Tensor) -> int:
 def _ld(t: torch.Tensor) -> int:
     if t.dim() != 2 or (t.size(1) > 1 and t.stride(1) != 1):
         raise TypeError("a 2-D tensor with unit column stride is required")
-    return t.stride(0) if t.size(0) > 1 else t.size(1)
+    if t.size(0) > 1:
+        return t.stride(0)
+    # one row: the stride is never used to address a second row; give the
+    # smallest one that keeps the library's 16-byte row rule
+    q = max(1, 16 // t.element_size())
+    return (t.size(1) + q - 1) // q * q
 
 
 def _ptr(t):
@@ -172,6 +180,54 @@ def ember_rowonly_step_sparse_rows(W: torch.Tensor, G_rows: torch.Tensor, idx: t
                                               float(beta2), float(eps), int(bool(maximize)), _ptr(ws),
                                               ws.numel() * ws.element_size(), _stream(W)),
            "ember_rowonly_step_sparse_rows")
+
+
+def ember_coalesce_workspace_bytes(max_tokens: int, V: int, D: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(LIB.ember_coalesce_workspace_bytes(int(max_tokens), int(V), int(D), ctypes.byref(out)),
+           "ember_coalesce_workspace_bytes")
+    return out.value
+
+
+def ember_coalesce_rows(tok: torch.Tensor, U: torch.Tensor, V: int, idx: torch.Tensor, G_rows: torch.Tensor,
+                        n_out: torch.Tensor, ws: torch.Tensor) -> None:
+    """Enqueue the coalescing of (tok, U) into (idx, G_rows, n_out) on the current
+    stream; n_out is a device int64 tensor of one element."""
+    if tok.dtype != torch.int64 or idx.dtype != torch.int64 or n_out.dtype != torch.int64:
+        raise TypeError("tok, idx and n_out must be int64")
+    P = tok.numel()
+    D = U.shape[1]
+    ldu = _ld(U) if P else D
+    ldg = _ld(G_rows) if G_rows.numel() else D
+    _check(LIB.ember_coalesce_rows(_ptr(tok), P, _ptr(U), _dtype(U), ldu, int(V), D, _ptr(idx),
+                                   _ptr(G_rows), _dtype(G_rows), ldg, n_out.data_ptr(), _ptr(ws),
+                                   ws.numel() * ws.element_size(), _stream(n_out)), "ember_coalesce_rows")
+
+
+class Coalescer:
+    """Workspace and outputs for coalescing batches of up to max_tokens token
+    gradients of a V-row, D-column table."""
+
+    def __init__(self, max_tokens: int, V: int, D: int, dtype=torch.bfloat16, device="cuda"):
+        self.max_tokens, self.V, self.D = int(max_tokens), int(V), int(D)
+        n = max(self.max_tokens, 1)
+        q = 16 // torch.empty(0, dtype=dtype).element_size()
+        ld = (self.D + q - 1) // q * q   # rows start on 16-byte boundaries
+        self.idx = torch.empty(n, dtype=torch.int64, device=device)
+        self.G_rows = torch.empty(n, ld, dtype=dtype, device=device)[:, :self.D]
+        self.n_out = torch.zeros(1, dtype=torch.int64, device=device)
+        nbytes = ember_coalesce_workspace_bytes(self.max_tokens, self.V, self.D)
+        self.ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+    def __call__(self, tok: torch.Tensor, U: torch.Tensor):
+        """Coalesce one batch; synchronises to read n.  Returns (idx, G_rows)
+        views of the first n rows."""
+        if tok.numel() > self.max_tokens:
+            raise ValueError("batch larger than max_tokens")
+        ember_coalesce_rows(tok, U, self.V, self.idx, self.G_rows, self.n_out, self.ws)
+        _check(ember_get_error(self.ws), "ember_coalesce_rows (device)")
+        n = int(self.n_out.item())
+        return self.idx[:n], self.G_rows[:n]
 
 
 def ember_get_error(ws: torch.Tensor) -> int:

@@ -129,6 +129,31 @@ def make_sparse_batch(cfg: Config, step: int, seed: int = 0, device="cuda", shuf
     return uniq.to(device=device, dtype=torch.int64).contiguous(), x.to(cfg.g_dtype)
 
 
+def make_token_batch(cfg: Config, step: int, seed: int = 0, device="cuda", dtype=None, ld: int | None = None):
+    """(tok int64 [P], U [P, D]) for one step of the embedding table before
+    coalescing: batch_tokens ids drawn with replacement from Zipf(1.1) over the
+    V rows, in batch order, and one back-propagated signal N(0, g_std) per
+    position (the per-position gradient rows whose per-id sums the sparse step
+    takes)."""
+    gc = _gen("cpu", seed, 2000 + step)
+    p = zipf_probs(cfg.V).float()
+    tok = torch.multinomial(p, cfg.batch_tokens, replacement=True, generator=gc)
+    ld = cfg.D if ld is None else ld
+    dtype = cfg.g_dtype if dtype is None else dtype
+    g = _gen(device, seed, 2000 + step)
+    U = torch.empty(cfg.batch_tokens, ld, dtype=dtype, device=device)
+    for r0 in range(0, cfg.batch_tokens, 16384):
+        r1 = min(cfg.batch_tokens, r0 + 16384)
+        U[r0:r1] = (torch.randn(r1 - r0, ld, generator=g, device=device) * cfg.g_std).to(dtype)
+    return tok.to(device=device, dtype=torch.int64).contiguous(), U[:, :cfg.D]
+
+
+def coalesce_bytes(P: int, n: int, D: int, u_size: int, g_size: int) -> int:
+    """HBM bytes coalescing must move: the token ids and per-position rows read
+    once, the distinct ids and summed rows written once."""
+    return 8 * P + P * D * u_size + 8 * n + n * D * g_size
+
+
 def algorithmic_bytes(V: int, D: int, w_size: int, g_size: int, rows: int | None = None) -> int:
     """HBM bytes one step must move: G read twice, W read and written once on
     the `rows` rows that carry gradient (all V if dense), r read and written,

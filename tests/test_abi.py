@@ -169,6 +169,45 @@ def test_rowonly_sparse_step_rejects_bad_arguments_on_host(em, kw, status):
     assert _rowonly_sparse(em, **kw) == getattr(em, "EMBER_ERR_" + status)
 
 
+def _coalesce(em, **kw):
+    a = dict(tok=IDX_, P=100, U=G_, ud=1, ldu=64, V=1000, D=64, idx=IDX_ + A, G=W_, gd=1, ldg=64,
+             n=R_, ws=WS_, wsb=None)
+    a.update(kw)
+    if a["wsb"] is None:
+        out = ctypes.c_size_t(0)
+        em.LIB.ember_coalesce_workspace_bytes(max(a["P"], 0), max(a["V"], 1), max(a["D"], 1), ctypes.byref(out))
+        a["wsb"] = out.value
+    return em.LIB.ember_coalesce_rows(a["tok"], a["P"], a["U"], a["ud"], a["ldu"], a["V"], a["D"], a["idx"],
+                                      a["G"], a["gd"], a["ldg"], a["n"], a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(P=-1), "SHAPE"), (dict(P=2 ** 26 + 1), "SHAPE"), (dict(V=0), "SHAPE"), (dict(D=0), "SHAPE"),
+    (dict(ldu=32), "SHAPE"), (dict(ldg=63), "SHAPE"),
+    (dict(tok=None), "ARG"), (dict(U=None), "ARG"), (dict(idx=None), "ARG"), (dict(G=None), "ARG"),
+    (dict(n=None), "ARG"), (dict(ws=None), "ARG"),
+    (dict(tok=IDX_ + 4), "ALIGN"), (dict(idx=IDX_ + A + 2), "ALIGN"), (dict(n=R_ + 4), "ALIGN"),
+    (dict(U=G_ + 2), "ALIGN"), (dict(ws=WS_ + 64), "ALIGN"), (dict(ud=5), "DTYPE"), (dict(gd=-1), "DTYPE"),
+    (dict(wsb=256), "WORKSPACE"),
+])
+def test_coalesce_rejects_bad_arguments_on_host(em, kw, status):
+    assert _coalesce(em, **kw) == getattr(em, "EMBER_ERR_" + status)
+
+
+def test_coalesce_workspace_bytes(em):
+    out = ctypes.c_size_t(0)
+    assert em.LIB.ember_coalesce_workspace_bytes(-1, 10, 10, ctypes.byref(out)) == em.EMBER_ERR_SHAPE
+    assert em.LIB.ember_coalesce_workspace_bytes(10, 10, 10, None) == em.EMBER_ERR_ARG
+    sizes = []
+    for P in (0, 1, 16384, 1 << 20):
+        assert em.LIB.ember_coalesce_workspace_bytes(P, 128256, 4096, ctypes.byref(out)) == em.EMBER_OK
+        assert out.value % 256 == 0
+        sizes.append(out.value)
+    assert sizes == sorted(sizes)
+    # sort buffers grow with the batch; the float64 partial rows stay bounded
+    assert sizes[-1] < 2 * (1 << 25) * 8 + 64 * (1 << 20)
+
+
 def test_init_state_and_get_error_reject_bad_arguments(em):
     wsb = _ws_bytes(em, 10, 64)
     assert em.LIB.ember_init_state(R_, C_, 0, 64, WS_, wsb, None) == em.EMBER_ERR_SHAPE
@@ -192,5 +231,9 @@ def test_binding_marshals_dtypes_and_strides(em):
     assert em._dtype(torch.zeros(1, dtype=torch.float16)) not in (em.EMBER_F32, em.EMBER_BF16)
     x = torch.zeros(5, 72)[:, :64]
     assert em._ld(x) == 72
+    # one row: a stride that keeps rows 16-byte aligned (never used to step rows)
+    assert em._ld(torch.zeros(1, 5)) == 8
+    assert em._ld(torch.zeros(1, 5, dtype=torch.bfloat16)) == 8
+    assert em._ld(torch.zeros(1, 4096, dtype=torch.bfloat16)) == 4096
     with pytest.raises(TypeError):
         em._ld(torch.zeros(5, 8).t())
