@@ -41,6 +41,7 @@ def parse():
     p.add_argument("--cpu-rows", type=int, default=65536, help="rows of the oracle's sample")
     p.add_argument("--no-other-configs", action="store_true")
     p.add_argument("--no-row-only", action="store_true")
+    p.add_argument("--no-coalesce", action="store_true")
     return p.parse_args()
 
 
@@ -204,6 +205,61 @@ def row_only_section(ember, wl, torch, dev, K, Wm, W_head, W_emb, grads, batches
     }
 
 
+def coalesce_section(ember, wl, torch, dev, K, Wm):
+    """Coalescing of the embedding batch (8 x 2048 token ids, one 4096-wide bf16
+    signal row per position) into distinct ids and summed rows: time per call
+    with inputs resident (no host read of n inside the timed region), and the
+    whole tokens -> sparse step path, which reads n on the host each step."""
+    cfg = wl.CONFIGS["embed128k"]
+    P, V_, D_ = cfg.batch_tokens, cfg.V, cfg.D
+    nb = 4
+    batches = [wl.make_token_batch(cfg, t + 1, seed=33, device=dev) for t in range(nb)]
+    co = ember.Coalescer(P, V_, D_, device=dev)
+    ns = []
+    for tok, U in batches:
+        idx, G = co(tok, U)
+        ns.append(int(idx.numel()))
+    stream = torch.cuda.current_stream()
+    for k in range(Wm):
+        tok, U = batches[k % nb]
+        ember.ember_coalesce_rows(tok, U, V_, co.idx, co.G_rows, co.n_out, co.ws)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for k in range(K):
+        tok, U = batches[k % nb]
+        ember.ember_coalesce_rows(tok, U, V_, co.idx, co.G_rows, co.n_out, co.ws)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / K
+    if ember.ember_get_error(co.ws) != ember.EMBER_OK:
+        raise RuntimeError("coalescing reported an index error")
+    n_avg = sum(ns[k % nb] for k in range(K)) / K
+    nbytes = sum(wl.coalesce_bytes(P, ns[k % nb], D_, 2, 2) for k in range(K)) / K
+    # tokens -> coalesce -> sparse step, n read on the host every step
+    W_emb = wl.make_weights(cfg, seed=34, device=dev)
+    emb = ember.EmberTable(V_, D_, device=dev)
+    for k in range(Wm):
+        tok, U = batches[k % nb]
+        idx, G = co(tok, U)
+        emb.step_sparse_rows(W_emb, G, idx)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(K):
+        tok, U = batches[k % nb]
+        idx, G = co(tok, U)
+        emb.step_sparse_rows(W_emb, G, idx)
+    torch.cuda.synchronize()
+    e2e_ms = (time.perf_counter() - t0) * 1e3 / K
+    gbps = nbytes / (ms * 1e-3) / 1e9
+    return {"workload": f"embed128k batch: {P} token ids over V={V_}, D={D_} bf16 signal rows, "
+                        f"{n_avg:.0f} distinct ids on average",
+            "ms": round(ms, 4), "bytes": int(nbytes), "GBps": round(gbps, 1),
+            "pct_of_peak": round(100.0 * gbps / PEAK_GBPS, 2),
+            "tokens_to_sparse_step_ms": round(e2e_ms, 4)}
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -365,12 +421,15 @@ def main():
         },
         "torch_device_copy_GBps": round(copy_gbps, 1),
         "row_only": None,
+        "coalesce": None,
         "other_configs": None,
         "cpu_baseline": None,
     }
     del head, emb
     if not args.no_row_only:
         out["row_only"] = row_only_section(ember, wl, torch, dev, K, Wm, W_head, W_emb, grads, batches)
+    if not args.no_coalesce:
+        out["coalesce"] = coalesce_section(ember, wl, torch, dev, K, Wm)
     if not args.no_other_configs:
         del W_head, W_emb, grads, batches
         torch.cuda.empty_cache()

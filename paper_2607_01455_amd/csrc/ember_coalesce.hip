@@ -13,19 +13,21 @@
 //
 // Pipeline (all integer work is exact and order-independent; every floating
 // point sum has a fixed order):
-//   1. stable LSD radix sort of (id, position) pairs by id, 1-3 passes of up
-//      to 8 bits (digit histograms per tile, offsets, stable scatter ranked with
+//   1. stable LSD radix sort of (id, position) pairs by id, 1-4 passes of up
+//      to 10 bits (digit histograms per tile, offsets, stable scatter ranked with
 //      wavefront ballots), so the positions of one id stay ascending;
 //   2. head flags of the sorted ids -> distinct ids, segment starts, and the
 //      segment number of every sorted entry;
-//   3. the sums: the sorted entries are cut into chunks of L positions; a
-//      wavefront sums one chunk for 256 columns in float64, position by
-//      position, and writes every segment that lies inside the chunk; the
-//      pieces of segments that cross chunk boundaries go to float64 partial
-//      rows, which a last launch adds in chunk order.
-// A segment inside one chunk is therefore summed exactly in ascending
-// position order; a longer one is summed in that order within each chunk and
-// then chunk by chunk.
+//   3. the sums: the sorted entries are cut into chunks of about L positions
+//      (boundaries at multiples of L, moved back to a segment head unless the
+//      segment is longer than L); a wavefront sums one chunk for 256 columns
+//      in float64, position by position, and writes every segment that lies
+//      inside the chunk; the pieces of the segments longer than L go to
+//      float64 partial rows; the chunks where such segments end are listed,
+//      and a last launch adds each one's pieces in chunk order.
+// A segment of at most L positions is therefore summed exactly in ascending
+// position order; a longer one is summed in that order within each piece of L
+// positions and then piece by piece.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -39,10 +41,11 @@ constexpr int kCoalThreads = 256;                    // 4 wavefronts
 constexpr int kCoalWaves = kCoalThreads / kWave;
 constexpr int kCoalItems = EMBER_COAL_ITEMS;         // keys per thread per tile
 constexpr int kTile = kCoalThreads * kCoalItems;     // keys per tile
-constexpr int kMaxBins = 256;                        // digits of up to 8 bits
+constexpr int kMaxDigitBits = 10;
+constexpr int kMaxBins = 1 << kMaxDigitBits;         // digits of up to 10 bits
 constexpr int kInBlockOffsetTiles = 64;              // up to this many tiles the
                                                      // scatter derives its own offsets
-constexpr int kRunRows = 32;                         // rows a wavefront holds at once
+constexpr int kRunRows = EMBER_COAL_RUN_ROWS;        // rows a wavefront holds at once
 constexpr int kMaxChunks = 4096;                     // bound on the chunks ...
 constexpr int64_t kMaxPartialElems = (int64_t)1 << 25; // ... and on chunks x D
 constexpr int kColsPerLane = 4;
@@ -160,18 +163,31 @@ __global__ __launch_bounds__(kCoalThreads) void coal_scatter(SortPass a) {
         for (int b = t; b < bins; b += kCoalThreads) off[b] = a.offs[(int64_t)b * a.ntiles + tile];
     } else {
         // offset of digit b in this tile = keys of smaller digits in every tile
-        // + keys of digit b in earlier tiles
-        uint32_t tot = 0, before = 0;
-        if (t < bins) {
-            for (int k = 0; k < a.ntiles; ++k) {
-                const uint32_t c = a.hist[(int64_t)t * a.ntiles + k];
-                tot += c;
-                if (k < tile) before += c;
+        // + keys of digit b in earlier tiles; thread t owns digits
+        // [t * per, (t + 1) * per)
+        const int per = bins > kCoalThreads ? bins / kCoalThreads : 1;
+        uint32_t tot[kMaxBins / kCoalThreads], before[kMaxBins / kCoalThreads];
+        uint32_t mine = 0;
+        for (int q = 0; q < per; ++q) {
+            const int b = t * per + q;
+            tot[q] = 0;
+            before[q] = 0;
+            if (b < bins) {
+                for (int k = 0; k < a.ntiles; ++k) {
+                    const uint32_t c = a.hist[(int64_t)b * a.ntiles + k];
+                    tot[q] += c;
+                    if (k < tile) before[q] += c;
+                }
             }
+            mine += tot[q];
         }
         uint32_t all;
-        const uint32_t excl = block_excl_scan(tot, scan_lds, &all);
-        if (t < bins) off[t] = excl + before;
+        uint32_t excl = block_excl_scan(mine, scan_lds, &all);
+        for (int q = 0; q < per; ++q) {
+            const int b = t * per + q;
+            if (b < bins) off[b] = excl + before[q];
+            excl += tot[q];
+        }
     }
     for (int b = t; b < bins; b += kCoalThreads) {
         run[b] = 0;
@@ -234,13 +250,18 @@ struct HeadParams {
     uint32_t* seg_start;      // [n + 1]
     int64_t* idx;             // [n] the distinct ids
     int64_t* n_out;
+    uint32_t* fix_count;      // cleared here for the sums
+    const uint32_t* tile_bad; // index errors found by the first sort pass
+    int* status;
 };
 
 __device__ __forceinline__ bool is_head(const uint32_t* K, int64_t k) { return k == 0 || K[k] != K[k - 1]; }
 
 // Tiles here are kTile consecutive sorted entries, kCoalItems per thread.
+// This launch also clears the count of chunks listed for the fixup.
 __global__ __launch_bounds__(kCoalThreads) void coal_heads_count(HeadParams a) {
     __shared__ uint32_t lds[kCoalThreads];
+    if (blockIdx.x == 0 && threadIdx.x == 0) *a.fix_count = 0;
     const int64_t k0 = (int64_t)blockIdx.x * kTile + (int64_t)threadIdx.x * kCoalItems;
     uint32_t c = 0;
     for (int e = 0; e < kCoalItems; ++e)
@@ -280,10 +301,18 @@ __global__ __launch_bounds__(kCoalThreads) void coal_heads_write(HeadParams a) {
         }
         a.uid[k] = u - 1;
     }
-    if (blockIdx.x == a.ntiles - 1 && threadIdx.x == 0) {
-        const uint32_t n = tile_base + total;
-        a.seg_start[n] = (uint32_t)a.P;
-        *a.n_out = (int64_t)n;
+    if (blockIdx.x == a.ntiles - 1) {
+        // index errors (marked per tile by the first sort pass) -> status, n = 0
+        uint32_t bad = 0;
+        for (int k = threadIdx.x; k < a.ntiles; k += kCoalThreads) bad |= a.tile_bad[k];
+        uint32_t nbad;
+        (void)block_excl_scan(bad, lds, &nbad);
+        if (threadIdx.x == 0) {
+            const uint32_t n = tile_base + total;
+            a.seg_start[n] = (uint32_t)a.P;
+            *a.n_out = nbad ? 0 : (int64_t)n;
+            *a.status = nbad ? 1 : 0;
+        }
     }
 }
 
@@ -307,10 +336,8 @@ struct SumParams {
     int nslabs;
     double* partA;            // [nchunks][D]: the first segment of a chunk, begun in an earlier chunk
     double* partB;            // [nchunks][D]: the last segment, continued in a later chunk
-    const uint32_t* tile_bad;
-    int ntiles;
-    int* status;
-    int64_t* n_out;
+    uint32_t* fix_list;       // chunks where a segment that began in an earlier chunk ends
+    uint32_t* fix_count;      // entries of fix_list (cleared by the heads launch)
 };
 
 template <typename T> struct Cols;
@@ -337,15 +364,14 @@ template <> struct Cols<uint16_t> {
 // the correctly rounded one (Boldo and Melquiond, "When double rounding is
 // odd", 2005).
 __device__ __forceinline__ uint16_t f64_to_bf16(double x) {
-    float f = (float)x;
-    uint32_t b = __float_as_uint(f);
-    if ((double)f != x && x == x) {
-        if (fabs((double)f) > fabs(x)) b -= 1;   // rounded away from zero: step back
-        b |= 1u;
-        f = __uint_as_float(b);
-    }
-    if ((b & 0x7F800000u) == 0x7F800000u && (b & 0x007FFFFFu) != 0u) return (uint16_t)((b >> 16) | 0x0040u);
-    return (uint16_t)((b + 0x7FFFu + ((b >> 16) & 1u)) >> 16);
+    const float f = (float)x;
+    const uint32_t b0 = __float_as_uint(f);
+    const bool inexact = (double)f != x;                        // also true for NaN
+    const uint32_t toward_zero = b0 - (fabs((double)f) > fabs(x) ? 1u : 0u);
+    const uint32_t b = inexact ? (toward_zero | 1u) : b0;     // round-to-odd fp32
+    const uint32_t rne = (b + 0x7FFFu + ((b >> 16) & 1u)) >> 16;
+    const bool nan = x != x;
+    return (uint16_t)(nan ? ((b0 >> 16) | 0x0040u) : rne);
 }
 
 template <typename GT>
@@ -377,9 +403,58 @@ __device__ __forceinline__ void load_cols(const UT* row, int64_t col, int64_t D,
     }
 }
 
+// Stores of one lane's 4 columns through a buffer resource whose length is the
+// row's D columns: the hardware drops the stores of lanes past the end (D is a
+// multiple of 4 where these are used), so no lane-divergent branch is needed.
+constexpr int kBufferWord3 = 0x00020000;  // raw 32-bit data format, gfx9 family
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(void* row, int64_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(row, 0, (int)bytes, kBufferWord3);
+}
+
+template <typename GT>
+__device__ __forceinline__ void buf_store_cols(void* G, int64_t ldg, uint32_t u, int col, int64_t D,
+                                               const double (&x)[kColsPerLane]) {
+    GT* row = static_cast<GT*>(G) + (int64_t)u * ldg;
+    const __amdgpu_buffer_rsrc_t rs = row_rsrc(row, D * (int64_t)sizeof(GT));
+    if constexpr (sizeof(GT) == 4) {
+        using v4 = decltype(__builtin_amdgcn_raw_buffer_load_b128(rs, 0, 0, 0));
+        const uint32_t w0 = __float_as_uint((float)x[0]), w1 = __float_as_uint((float)x[1]);
+        const uint32_t w2 = __float_as_uint((float)x[2]), w3 = __float_as_uint((float)x[3]);
+        __builtin_amdgcn_raw_buffer_store_b128(v4{w0, w1, w2, w3}, rs, col * 4, 0, 0);
+    } else {
+        using v2 = decltype(__builtin_amdgcn_raw_buffer_load_b64(rs, 0, 0, 0));
+        const uint32_t w0 = (uint32_t)f64_to_bf16(x[0]) | ((uint32_t)f64_to_bf16(x[1]) << 16);
+        const uint32_t w1 = (uint32_t)f64_to_bf16(x[2]) | ((uint32_t)f64_to_bf16(x[3]) << 16);
+        __builtin_amdgcn_raw_buffer_store_b64(v2{w0, w1}, rs, col * 2, 0, 0);
+    }
+}
+
+__device__ __forceinline__ void store_partial(double* row, int64_t col, int64_t D, const double (&x)[kColsPerLane]) {
+#pragma unroll
+    for (int e = 0; e < kColsPerLane; ++e)
+        if (col + e < D) row[col + e] = x[e];
+}
+
+// Start of chunk c: the position c * L, moved back to the head of its segment
+// when that segment is not longer than L.  Only segments longer than L are then
+// cut by chunk boundaries (always at multiples of L); a chunk holds between 1
+// and 2L - 1 positions.
+__device__ __forceinline__ int64_t chunk_start(const SumParams& a, int64_t c) {
+    const int64_t x = c * a.L;
+    if (x >= a.P) return a.P;
+    const uint32_t u = a.uid[x];
+    const int64_t s = a.seg_start[u];
+    const int64_t e = a.seg_start[u + 1];
+    return e - s > a.L ? x : s;
+}
+
 // One wavefront per (chunk, 256-column slab); slabs of a chunk are adjacent.
 // kExact (D a multiple of 4): the wavefront loads kRunRows rows at a time into
-// registers before adding them; otherwise one row at a time.
+// registers (lanes past D read column 0 and store nothing), then walks them in
+// order; a row that starts a segment resets the sum, a row that ends one
+// stores it.  Segment boundaries depend only on the sorted ids, so every branch
+// is uniform across the wavefront.  Otherwise one row at a time.
 template <typename UT, typename GT, bool kExact>
 __global__ __launch_bounds__(kCoalThreads) void coal_segsum(SumParams a) {
     using raw = typename Cols<UT>::raw;
@@ -390,105 +465,131 @@ __global__ __launch_bounds__(kCoalThreads) void coal_segsum(SumParams a) {
     const int slab = item - c * a.nslabs;
     const int64_t col = (int64_t)slab * kSlabCols + (int64_t)lane * kColsPerLane;
     const bool col_ok = col < a.D;
-    const int64_t k0 = (int64_t)c * a.L;
-    const int64_t k1 = min(a.P, k0 + a.L);
+    const int64_t k0 = chunk_start(a, c);
+    const int64_t k1 = chunk_start(a, (int64_t)c + 1);
     const UT* U = static_cast<const UT*>(a.U);
     const bool began_before = k0 > 0 && a.K[k0] == a.K[k0 - 1];
     const bool ends_after = k1 < a.P && a.K[k1] == a.K[k1 - 1];
 
     double acc[kColsPerLane] = {0.0, 0.0, 0.0, 0.0};
     int64_t run0 = k0;
-    auto flush = [&](int64_t rs, int64_t re) {
-        const bool first = rs == k0 && began_before;
-        const bool last = re == k1 && ends_after;
-        if (!col_ok) return;
-        if (!first && !last) {
-            store_cols<GT>(a.G, a.ldg, a.uid[rs], col, a.D, acc);
-        } else {
-            double* dst = (first ? a.partA : a.partB) + (int64_t)c * a.D;
-#pragma unroll
-            for (int e = 0; e < kColsPerLane; ++e)
-                if (col + e < a.D) dst[col + e] = acc[e];
-        }
-    };
-    auto add_row = [&](int64_t k, const raw& r) {
-        if (k > run0 && a.K[k] != a.K[k - 1]) {
-            flush(run0, k);
-#pragma unroll
-            for (int e = 0; e < kColsPerLane; ++e) acc[e] = 0.0;
-            run0 = k;
-        }
-        double x[kColsPerLane];
-        Cols<UT>::widen(r, x);
-#pragma unroll
-        for (int e = 0; e < kColsPerLane; ++e) acc[e] += x[e];
-    };
+    // the chunk's first segment began earlier and ends here: list the chunk
+    // for the launch that adds the pieces (once, from the first slab)
+    bool ends_crossing = false;
     if constexpr (kExact) {
+        const int64_t colc = col_ok ? col : 0;
         for (int64_t s0 = k0; s0 < k1; s0 += kRunRows) {
+            const int nr = (int)min((int64_t)kRunRows, k1 - s0);
+            // ids, positions and segment numbers of the batch, one per lane (lane
+            // nr holds the id after the batch, if any); read back per row with
+            // lane reads instead of a memory round trip per row
+            const int64_t kl = s0 + min(lane, nr);
+            const bool have = lane <= nr && kl < a.P;
+            const uint32_t kv = have ? a.K[kl] : 0xFFFFFFFFu;
+            const uint32_t pv = lane < nr ? a.pos[kl] : 0u;
+            const uint32_t uv = lane < nr ? a.uid[kl] : 0u;
             raw rows[kRunRows];
 #pragma unroll
             for (int r = 0; r < kRunRows; ++r) {
-                const int64_t k = s0 + r;
-                rows[r] = raw{};
-                if (k < k1 && col_ok)
-                    rows[r] = *reinterpret_cast<const raw*>(U + (int64_t)a.pos[k] * a.ldu + col);
+                const uint32_t p = (uint32_t)__builtin_amdgcn_readlane((int)pv, r < nr ? r : 0);
+                rows[r] = *reinterpret_cast<const raw*>(U + (int64_t)p * a.ldu + colc);
             }
 #pragma unroll
-            for (int r = 0; r < kRunRows; ++r)
-                if (s0 + r < k1) add_row(s0 + r, rows[r]);
+            for (int r = 0; r < kRunRows; ++r) {
+                const int64_t k = s0 + r;
+                if (r < nr) {
+                    const uint32_t kr = (uint32_t)__builtin_amdgcn_readlane((int)kv, r);
+                    if (k > run0 && (r == 0 ? a.K[k - 1] != kr
+                                            : (uint32_t)__builtin_amdgcn_readlane((int)kv, r - 1) != kr)) {
+                        run0 = k;
+#pragma unroll
+                        for (int e = 0; e < kColsPerLane; ++e) acc[e] = 0.0;
+                    }
+                    double x[kColsPerLane];
+                    Cols<UT>::widen(rows[r], x);
+#pragma unroll
+                    for (int e = 0; e < kColsPerLane; ++e) acc[e] += x[e];
+                    const bool chunk_end = k + 1 == k1;
+                    if (chunk_end || (uint32_t)__builtin_amdgcn_readlane((int)kv, r + 1) != kr) {
+                        const bool first = run0 == k0 && began_before;
+                        const uint32_t u = (uint32_t)__builtin_amdgcn_readlane((int)uv, r);
+                        if (first || (chunk_end && ends_after)) {
+                            store_partial((first ? a.partA : a.partB) + (int64_t)c * a.D, col, a.D, acc);
+                            ends_crossing |= first && !(chunk_end && ends_after);
+                        } else {
+                            buf_store_cols<GT>(a.G, a.ldg, u, (int)col, a.D, acc);
+                        }
+                    }
+                }
+            }
         }
     } else {
         for (int64_t k = k0; k < k1; ++k) {
+            if (k > run0 && a.K[k] != a.K[k - 1]) {
+                run0 = k;
+                for (int e = 0; e < kColsPerLane; ++e) acc[e] = 0.0;
+            }
             raw r;
             load_cols<UT>(U + (int64_t)a.pos[k] * a.ldu, col, a.D, col_ok, r);
-            add_row(k, r);
+            double x[kColsPerLane];
+            Cols<UT>::widen(r, x);
+            for (int e = 0; e < kColsPerLane; ++e) acc[e] += x[e];
+            const bool chunk_end = k + 1 == k1;
+            if (chunk_end || a.K[k + 1] != a.K[k]) {
+                const bool first = run0 == k0 && began_before;
+                if (first || (chunk_end && ends_after)) {
+                    store_partial((first ? a.partA : a.partB) + (int64_t)c * a.D, col, a.D, acc);
+                    ends_crossing |= first && !(chunk_end && ends_after);
+                } else if (col_ok) {
+                    store_cols<GT>(a.G, a.ldg, a.uid[k], col, a.D, acc);
+                }
+            }
         }
     }
-    flush(run0, k1);
+    if (ends_crossing && slab == 0 && lane == 0) a.fix_list[atomicAdd(a.fix_count, 1u)] = (uint32_t)c;
 }
 
-// Segments that cross chunk boundaries: the wavefront of the chunk where such
-// a segment ends adds its pieces in chunk order.  Block 0 also turns the
-// tiles' index-error marks into the status word (n = 0 on error).
+// Segments that cross chunk boundaries: for each listed chunk (where such a
+// segment ends), add the segment's pieces in chunk order: the start chunk's
+// last-segment partial, then the first-segment partials of the later chunks.
+// One column per lane, 64 columns per wavefront, kFixBatch partial rows loaded
+// at a time; the grid walks the (listed chunk, column slab) items.  The
+// list order varies from run to run; each item's result does not.
+constexpr int kFixBatch = 64;
+
 template <typename GT>
 __global__ __launch_bounds__(kCoalThreads) void coal_fixup(SumParams a) {
-    if (blockIdx.x == 0) {
-        __shared__ uint32_t bad_lds[kCoalThreads];
-        uint32_t bad = 0;
-        for (int k = threadIdx.x; k < a.ntiles; k += kCoalThreads) bad |= a.tile_bad[k];
-        bad_lds[threadIdx.x] = bad;
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            uint32_t any = 0;
-            for (int k = 0; k < kCoalThreads; ++k) any |= bad_lds[k];
-            *a.status = any ? 1 : 0;
-            if (any) *a.n_out = 0;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int nslabs = (int)((a.D + kWave - 1) / kWave);
+    const int64_t items = (int64_t)(*a.fix_count) * nslabs;
+    const int64_t wave0 = (int64_t)blockIdx.x * kCoalWaves + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    for (int64_t item = wave0; item < items; item += (int64_t)gridDim.x * kCoalWaves) {
+        const int c = (int)a.fix_list[item / nslabs];
+        const int slab = (int)(item % nslabs);
+        const int64_t k0 = (int64_t)c * a.L;
+        const int64_t col = (int64_t)slab * kWave + lane;
+        const bool ok = col < a.D;
+        const int64_t colc = ok ? col : 0;
+        const uint32_t u = a.uid[k0];
+        const int c0 = (int)(a.seg_start[u] / a.L);
+        double acc = a.partB[(int64_t)c0 * a.D + colc];
+        for (int cc = c0 + 1; cc <= c; cc += kFixBatch) {
+            double x[kFixBatch];
+#pragma unroll
+            for (int q = 0; q < kFixBatch; ++q) {
+                const int ccq = cc + q <= c ? cc + q : c;
+                x[q] = a.partA[(int64_t)ccq * a.D + colc];
+            }
+#pragma unroll
+            for (int q = 0; q < kFixBatch; ++q)
+                if (cc + q <= c) acc += x[q];
+        }
+        if (ok) {
+            GT* row = static_cast<GT*>(a.G) + (int64_t)u * a.ldg;
+            if constexpr (sizeof(GT) == 4) row[col] = (float)acc;
+            else row[col] = f64_to_bf16(acc);
         }
     }
-    const int lane = threadIdx.x & (kWave - 1);
-    const int item = blockIdx.x * kCoalWaves + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-    const int c = item / a.nslabs;
-    if (c >= a.nchunks) return;
-    const int slab = item - c * a.nslabs;
-    const int64_t k0 = (int64_t)c * a.L;
-    if (k0 == 0 || a.K[k0] != a.K[k0 - 1]) return;          // first segment begins here
-    const int64_t k1 = min(a.P, k0 + a.L);
-    if (k1 < a.P && a.K[k1] == a.K[k0]) return;              // it continues past this chunk
-    const int64_t col = (int64_t)slab * kSlabCols + (int64_t)lane * kColsPerLane;
-    if (col >= a.D) return;
-    const uint32_t u = a.uid[k0];
-    const int c0 = (int)(a.seg_start[u] / a.L);
-    double acc[kColsPerLane];
-    const double* b = a.partB + (int64_t)c0 * a.D;
-#pragma unroll
-    for (int e = 0; e < kColsPerLane; ++e) acc[e] = col + e < a.D ? b[col + e] : 0.0;
-    for (int cc = c0 + 1; cc <= c; ++cc) {
-        const double* p = a.partA + (int64_t)cc * a.D;
-#pragma unroll
-        for (int e = 0; e < kColsPerLane; ++e)
-            if (col + e < a.D) acc[e] += p[col + e];
-    }
-    store_cols<GT>(a.G, a.ldg, u, col, a.D, acc);
 }
 
 // P == 0: no rows, no error.
@@ -511,7 +612,7 @@ CoalPlan coal_plan(int64_t P, int64_t V, int64_t D) {
     CoalPlan c;
     c.ntiles = (int)((P + kTile - 1) / kTile);
     const int bits = bits_for(V);
-    c.passes = (bits + 7) / 8;
+    c.passes = (bits + kMaxDigitBits - 1) / kMaxDigitBits;
     c.digit_bits = (bits + c.passes - 1) / c.passes;
     int64_t maxc = kMaxPartialElems / (D > 0 ? D : 1);
     maxc = maxc < 1 ? 1 : (maxc > kMaxChunks ? kMaxChunks : maxc);
@@ -536,6 +637,8 @@ CoalPlan coal_plan(int64_t P, int64_t V, int64_t D) {
     const size_t nc = (size_t)(c.nchunks > 0 ? c.nchunks : 1);
     c.part_a = off; off = align256(off + nc * (size_t)D * 8);
     c.part_b = off; off = align256(off + nc * (size_t)D * 8);
+    c.fix_list = off; off = align256(off + nc * 4);
+    c.fix_count = off; off = align256(off + 4);
     c.total = off;
     return c;
 }
@@ -601,6 +704,9 @@ hipError_t launch_coalesce(const CoalArgs& a, hipStream_t s) {
     h.seg_start = reinterpret_cast<uint32_t*>(ws + c.seg_start);
     h.idx = a.idx;
     h.n_out = a.n_out;
+    h.fix_count = reinterpret_cast<uint32_t*>(ws + c.fix_count);
+    h.tile_bad = tile_bad;
+    h.status = status;
     coal_heads_count<<<c.ntiles, kCoalThreads, 0, s>>>(h);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -630,10 +736,8 @@ hipError_t launch_coalesce(const CoalArgs& a, hipStream_t s) {
     m.nslabs = c.nslabs;
     m.partA = reinterpret_cast<double*>(ws + c.part_a);
     m.partB = reinterpret_cast<double*>(ws + c.part_b);
-    m.tile_bad = tile_bad;
-    m.ntiles = c.ntiles;
-    m.status = status;
-    m.n_out = a.n_out;
+    m.fix_list = reinterpret_cast<uint32_t*>(ws + c.fix_list);
+    m.fix_count = h.fix_count;
     const int64_t items = (int64_t)c.nchunks * c.nslabs;
     const unsigned grid = (unsigned)((items + kCoalWaves - 1) / kCoalWaves);
     const bool exact = a.D % kColsPerLane == 0;
@@ -656,8 +760,11 @@ hipError_t launch_coalesce(const CoalArgs& a, hipStream_t s) {
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if (a.g_dtype == 0) coal_fixup<float><<<grid, kCoalThreads, 0, s>>>(m);
-    else coal_fixup<uint16_t><<<grid, kCoalThreads, 0, s>>>(m);
+    // one (listed chunk, 64-column slab) item per wavefront in the worst case
+    const int64_t fix_items = (int64_t)c.nchunks * ((a.D + kWave - 1) / kWave);
+    const unsigned fix_blocks = (unsigned)min((fix_items + kCoalWaves - 1) / kCoalWaves, (int64_t)16384);
+    if (a.g_dtype == 0) coal_fixup<float><<<fix_blocks, kCoalThreads, 0, s>>>(m);
+    else coal_fixup<uint16_t><<<fix_blocks, kCoalThreads, 0, s>>>(m);
     return hipGetLastError();
 }
 

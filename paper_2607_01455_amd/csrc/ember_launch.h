@@ -69,6 +69,9 @@ constexpr int kWaves = kBlock / kWave;
 #ifndef EMBER_COAL_ITEMS
 #define EMBER_COAL_ITEMS 4       // gradient coalescing: keys per thread per sort tile
 #endif
+#ifndef EMBER_COAL_RUN_ROWS
+#define EMBER_COAL_RUN_ROWS 32   // gradient coalescing: rows a wavefront sums per batch of loads
+#endif
 #ifndef EMBER_MAX_BLOCKS
 #define EMBER_MAX_BLOCKS 384        // row blocks of the statistics pass
 #endif
@@ -196,7 +199,7 @@ struct CoalPlan {
     int nchunks;
     int nslabs;
     size_t keys_a, vals_a, keys_b, vals_b, hist, offs, tile_bad, tilecnt, tileoff, uid, seg_start;
-    size_t part_a, part_b;
+    size_t part_a, part_b, fix_list, fix_count;
     size_t total;      // workspace bytes
 };
 CoalPlan coal_plan(int64_t P, int64_t V, int64_t D);
