@@ -375,7 +375,13 @@ __device__ __forceinline__ RowSet stats_rows(int64_t rows, int nb, int b) {
 // last are the first it reads again: rows >= cached_from are loaded through
 // the caches (and can be served from the last-level cache later), the others
 // with non-temporal loads.
-template <typename GT, int M, int R, bool kSparse>
+// kWide (more than kWideRowsPerWave rows per wavefront, i.e. very tall
+// tables): the per-lane column sums are kept in fp32 over kWideRowsPerWave
+// rows at a time and gathered in float64, so their error does not grow with
+// the row count.
+constexpr int64_t kWideRowsPerWave = 1024;
+
+template <typename GT, int M, int R, bool kSparse, bool kWide>
 __global__ __launch_bounds__(kBlock) void ember_stats(StatsParams a) {
     constexpr int EPC = 16 / (int)sizeof(GT);
     const int lane = threadIdx.x & (kWave - 1);
@@ -388,10 +394,28 @@ __global__ __launch_bounds__(kBlock) void ember_stats(StatsParams a) {
     const GT* G = static_cast<const GT*>(a.G);
 
     float acc[M][EPC];
+    double wide[kWide ? M : 1][kWide ? EPC : 1];
 #pragma unroll
     for (int m = 0; m < M; ++m)
 #pragma unroll
         for (int e = 0; e < EPC; ++e) acc[m][e] = 0.0f;
+    if constexpr (kWide) {
+#pragma unroll
+        for (int m = 0; m < M; ++m)
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) wide[m][e] = 0.0;
+    }
+    auto gather = [&]() {
+        if constexpr (kWide) {
+#pragma unroll
+            for (int m = 0; m < M; ++m)
+#pragma unroll
+                for (int e = 0; e < EPC; ++e) {
+                    wide[m][e] += (double)acc[m][e];
+                    acc[m][e] = 0.0f;
+                }
+        }
+    };
 
     // this wave's rows: the block's rows wave, wave + 4, wave + 8, ...
     const int64_t span = rset.count - wave;
@@ -453,6 +477,14 @@ __global__ __launch_bounds__(kBlock) void ember_stats(StatsParams a) {
             }
         }
         if (!EMBER_STATS_PIPE && k0 + R < nk) load_batch(k0 + R);
+        if (kWide && (k0 / R + 1) % (kWideRowsPerWave / R) == 0) gather();
+    }
+    if constexpr (kWide) {
+        gather();
+#pragma unroll
+        for (int m = 0; m < M; ++m)
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) acc[m][e] = (float)wide[m][e];
     }
 
     // Combine the 4 waves' column sums in a fixed order, one chunk column at a time.
@@ -629,9 +661,9 @@ __device__ __forceinline__ void finalize_body(const FinParams& a, int err, float
         if (err) continue;
         float rn;
         if (touched) {
-            float sum = 0.0f;
-            for (int sb = 0; sb < a.nslab; ++sb) sum += a.rowpart[(int64_t)sb * a.rows + k];
-            const float mean = (float)((double)sum * invD);
+            double sum = 0.0;
+            for (int sb = 0; sb < a.nslab; ++sb) sum += (double)a.rowpart[(int64_t)sb * a.rows + k];
+            const float mean = (float)(sum * invD);
             rn = fmaf(a.beta2, a.r[i], a.one_minus_beta2 * mean);
         } else {
             rn = a.beta2 * a.r[i];
@@ -679,67 +711,72 @@ __global__ __launch_bounds__(kBlock) void ember_apply(ApplyParams a) {
     }
     if (a.inv_alpha == 0.0) return;   // lr == 0: every weight keeps its bits
 
-    const int slab = (int)(blockIdx.x % (unsigned)a.nslab);
-    // Row blocks in reverse order: the rows the statistics pass read last are
-    // the likeliest still to sit in the last-level cache.
-    const int b = a.nb - 1 - (int)(blockIdx.x / (unsigned)a.nslab);
-    const int cbeg = slab * a.slab_chunks;
-    const int cend = min(cbeg + a.slab_chunks, a.total_chunks);
+    // (row block, slab) pairs, slab-fastest; the grid is capped, so a block may
+    // take several pairs
+    const int64_t nvb = (int64_t)a.nb * a.nslab;
+    for (int64_t vb = blockIdx.x; vb < nvb; vb += gridDim.x) {
+        const int slab = (int)(vb % a.nslab);
+        // Row blocks in reverse order: the rows the statistics pass read last are
+        // the likeliest still to sit in the last-level cache.
+        const int b = a.nb - 1 - (int)(vb / a.nslab);
+        const int cbeg = slab * a.slab_chunks;
+        const int cend = min(cbeg + a.slab_chunks, a.total_chunks);
 
-    // Column factors sqrt(chat_j / s) / alpha_s of this lane's columns, derived
-    // once per step by the finalize pass.
-    float qa[M][EPC];
+        // Column factors sqrt(chat_j / s) / alpha_s of this lane's columns, derived
+        // once per step by the finalize pass.
+        float qa[M][EPC];
 #pragma unroll
-    for (int m = 0; m < M; ++m) {
-        const int ch = cbeg + lane + kWave * m;
-        load_chunk_f32<EPC>(a.qa, (int64_t)ch * EPC, ch < cend, a.D, qa[m]);
-    }
-    const float epsa = a.eps_over_alpha;
-    const float ibias = (float)a.inv_bias;
-
-    int64_t r0, r1;
-    row_range(a.rows, a.nb, b, r0, r1);
-    const GT* G = static_cast<const GT*>(a.G);
-    WT* W = static_cast<WT*>(a.W);
-
-    const int64_t span = r1 - r0 - wave;
-    const int64_t nk = span > 0 ? (span + kWaves - 1) / kWaves : 0;
-    for (int64_t k0 = 0; k0 < nk; k0 += R) {
-        Raw<GT, EPC> graw[R][M];
-        Raw<WT, EPC> wraw[R][M];
-        float ai[R];
-        WT* wr[R];
-#pragma unroll
-        for (int j = 0; j < R; ++j) {
-            const bool rv = k0 + j < nk;
-            const int64_t row = rv ? r0 + wave + kWaves * (k0 + j) : r0;
-            const int64_t wrow = kSparse ? a.idx[row] : row;
-            ai[j] = sqrtf(a.r[wrow] * ibias);
-            const GT* grow = G + row * a.ldg;
-            wr[j] = W + wrow * a.ldw;
-#pragma unroll
-            for (int m = 0; m < M; ++m) {
-                const int ch = cbeg + lane + kWave * m;
-                load_raw<GT, EPC, EMBER_APPLY_NT>(grow, (int64_t)ch * EPC, rv && ch < cend, a.D, graw[j][m]);
-                load_raw<WT, EPC, EMBER_APPLY_WNT>(wr[j], (int64_t)ch * EPC, rv && ch < cend, a.D, wraw[j][m]);
-            }
+        for (int m = 0; m < M; ++m) {
+            const int ch = cbeg + lane + kWave * m;
+            load_chunk_f32<EPC>(a.qa, (int64_t)ch * EPC, ch < cend, a.D, qa[m]);
         }
+        const float epsa = a.eps_over_alpha;
+        const float ibias = (float)a.inv_bias;
+
+        int64_t r0, r1;
+        row_range(a.rows, a.nb, b, r0, r1);
+        const GT* G = static_cast<const GT*>(a.G);
+        WT* W = static_cast<WT*>(a.W);
+
+        const int64_t span = r1 - r0 - wave;
+        const int64_t nk = span > 0 ? (span + kWaves - 1) / kWaves : 0;
+        for (int64_t k0 = 0; k0 < nk; k0 += R) {
+            Raw<GT, EPC> graw[R][M];
+            Raw<WT, EPC> wraw[R][M];
+            float ai[R];
+            WT* wr[R];
 #pragma unroll
-        for (int j = 0; j < R; ++j) {
-            if (k0 + j >= nk) break;
+            for (int j = 0; j < R; ++j) {
+                const bool rv = k0 + j < nk;
+                const int64_t row = rv ? r0 + wave + kWaves * (k0 + j) : r0;
+                const int64_t wrow = kSparse ? a.idx[row] : row;
+                ai[j] = sqrtf(a.r[wrow] * ibias);
+                const GT* grow = G + row * a.ldg;
+                wr[j] = W + wrow * a.ldw;
 #pragma unroll
-            for (int m = 0; m < M; ++m) {
-                const int ch = cbeg + lane + kWave * m;
-                float g[EPC], w[EPC], o[EPC];
-                decode(graw[j][m], g);
-                decode(wraw[j][m], w);
-#pragma unroll
-                for (int e = 0; e < EPC; ++e) {
-                    const float d = fmaf(ai[j], qa[m][e], epsa);
-                    const float upd = fmaf(g[e], __builtin_amdgcn_rcpf(d), w[e]);
-                    o[e] = (g[e] == 0.0f) ? w[e] : upd;
+                for (int m = 0; m < M; ++m) {
+                    const int ch = cbeg + lane + kWave * m;
+                    load_raw<GT, EPC, EMBER_APPLY_NT>(grow, (int64_t)ch * EPC, rv && ch < cend, a.D, graw[j][m]);
+                    load_raw<WT, EPC, EMBER_APPLY_WNT>(wr[j], (int64_t)ch * EPC, rv && ch < cend, a.D, wraw[j][m]);
                 }
-                if (ch < cend) store_chunk<WT, EPC, EMBER_APPLY_NT>(wr[j], (int64_t)ch * EPC, a.D, o);
+            }
+#pragma unroll
+            for (int j = 0; j < R; ++j) {
+                if (k0 + j >= nk) break;
+#pragma unroll
+                for (int m = 0; m < M; ++m) {
+                    const int ch = cbeg + lane + kWave * m;
+                    float g[EPC], w[EPC], o[EPC];
+                    decode(graw[j][m], g);
+                    decode(wraw[j][m], w);
+#pragma unroll
+                    for (int e = 0; e < EPC; ++e) {
+                        const float d = fmaf(ai[j], qa[m][e], epsa);
+                        const float upd = fmaf(g[e], __builtin_amdgcn_rcpf(d), w[e]);
+                        o[e] = (g[e] == 0.0f) ? w[e] : upd;
+                    }
+                    if (ch < cend) store_chunk<WT, EPC, EMBER_APPLY_NT>(wr[j], (int64_t)ch * EPC, a.D, o);
+                }
             }
         }
     }
@@ -766,7 +803,8 @@ struct RowOnlyParams {
     int total_chunks;
     int slab_chunks;
     int nslab;
-    int nb;                // row blocks
+    int64_t nb;            // row blocks
+    int64_t nvb;           // row blocks + decay blocks (sparse)
     const int64_t* idx;    // sparse only
     float* r;
     int64_t V;
@@ -787,7 +825,8 @@ struct RowOnlyParams {
 // (rows too long to hold) wave w takes slabs w, w + nw, ... and reads them
 // once for the row sum and again, with W, for the update.
 template <typename GT, typename WT, int M, int S, bool kSparse, bool kResident>
-__device__ __forceinline__ void rowonly_rows(const RowOnlyParams& a, float (*part)[kRowOnlyRows], float* rn_lds) {
+__device__ __forceinline__ void rowonly_rows(const RowOnlyParams& a, int64_t vb, float (*part)[kRowOnlyRows],
+                                             float* rn_lds) {
     constexpr int EPC = 16 / (int)sizeof(GT);
     constexpr int R = kRowOnlyRows;
     const int lane = threadIdx.x & (kWave - 1);
@@ -795,7 +834,7 @@ __device__ __forceinline__ void rowonly_rows(const RowOnlyParams& a, float (*par
     const int nw = blockDim.x / kWave;
     const bool update = a.inv_alpha != 0.0f;
 
-    const int64_t r0 = (int64_t)blockIdx.x * kRowOnlyRowsPerBlock;
+    const int64_t r0 = vb * kRowOnlyRowsPerBlock;
     const int64_t r1 = min(r0 + kRowOnlyRowsPerBlock, a.rows);
     const GT* G = static_cast<const GT*>(a.G);
     WT* W = static_cast<WT*>(a.W);
@@ -864,6 +903,10 @@ __device__ __forceinline__ void rowonly_rows(const RowOnlyParams& a, float (*par
 #pragma unroll
                     for (int m = 0; m < M; ++m) accumulate(graw[j][q][m], j);
         } else {
+            // long rows: each slab's fp32 sum is gathered in float64
+            double wsum[R];
+#pragma unroll
+            for (int j = 0; j < R; ++j) wsum[j] = 0.0;
             for (int slab = wave; slab < a.nslab; slab += nw) {
                 const int cbeg = slab * a.slab_chunks;
                 const int cend = min(cbeg + a.slab_chunks, a.total_chunks);
@@ -875,10 +918,15 @@ __device__ __forceinline__ void rowonly_rows(const RowOnlyParams& a, float (*par
                         load_raw<GT, EPC, false>(gr[j], (int64_t)ch * EPC, rv[j] && ch < cend, a.D, graw[j][0][m]);
                     }
 #pragma unroll
-                for (int j = 0; j < R; ++j)
+                for (int j = 0; j < R; ++j) {
 #pragma unroll
                     for (int m = 0; m < M; ++m) accumulate(graw[j][0][m], j);
+                    wsum[j] += (double)s0[j] + (double)s1[j];
+                    s0[j] = s1[j] = 0.0f;
+                }
             }
+#pragma unroll
+            for (int j = 0; j < R; ++j) s0[j] = (float)wsum[j];
         }
 
         // Row sums of g^2: this wave's part, then the waves in order.
@@ -954,14 +1002,14 @@ __device__ __forceinline__ void rowonly_rows(const RowOnlyParams& a, float (*par
 // wave takes kRowOnlyWaveRows adjacent rows at a time; the waves of a block
 // interleave over the block's rows.
 template <typename GT, typename WT, int C, bool kSparse, bool kExact>
-__device__ __forceinline__ void rowonly_wave_rows(const RowOnlyParams& a) {
+__device__ __forceinline__ void rowonly_wave_rows(const RowOnlyParams& a, int64_t vb) {
     constexpr int EPC = 16 / (int)sizeof(GT);
     constexpr int R = kRowOnlyWaveRows;
     constexpr int kWBytes = EPC * (int)sizeof(WT);   // bytes of W per chunk
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const bool update = a.inv_alpha != 0.0f;
-    const int64_t r0 = (int64_t)blockIdx.x * kRowOnlyRowsPerBlock;
+    const int64_t r0 = vb * kRowOnlyRowsPerBlock;
     const int64_t r1 = min(r0 + kRowOnlyRowsPerBlock, a.rows);
     const GT* G = static_cast<const GT*>(a.G);
     WT* W = static_cast<WT*>(a.W);
@@ -1053,8 +1101,8 @@ __device__ __forceinline__ void rowonly_wave_rows(const RowOnlyParams& a) {
 
 // Blocks nb.. of the sparse row-only step: beta2 r on every row outside idx,
 // and the row marks cleared (r is left alone when idx was rejected).
-__device__ __forceinline__ void rowonly_decay(const RowOnlyParams& a, int err) {
-    const int64_t i0 = (int64_t)(blockIdx.x - a.nb) * kDecayRows;
+__device__ __forceinline__ void rowonly_decay(const RowOnlyParams& a, int err, int64_t db) {
+    const int64_t i0 = db * kDecayRows;
     for (int64_t i = i0 + threadIdx.x; i < i0 + kDecayRows && i < a.V; i += blockDim.x) {
         const int sl = a.slot[i];
         if (sl != 0) a.slot[i] = 0;
@@ -1079,13 +1127,15 @@ __global__ __launch_bounds__(kBlock) void ember_rowonly_wave(RowOnlyParams a) {
     __shared__ int last;
     if (!kSparse) {
         if (blockIdx.x == 0 && threadIdx.x == 0) *a.status = 0;
-        rowonly_wave_rows<GT, WT, C, false, kExact>(a);
+        for (int64_t vb = blockIdx.x; vb < a.nb; vb += gridDim.x) rowonly_wave_rows<GT, WT, C, false, kExact>(a, vb);
         return;
     }
     const int err = *a.flag;
     if (blockIdx.x == 0 && threadIdx.x == 0) *a.status = err;
-    if ((int)blockIdx.x >= a.nb) rowonly_decay(a, err);
-    else if (!err) rowonly_wave_rows<GT, WT, C, true, kExact>(a);
+    for (int64_t vb = blockIdx.x; vb < a.nvb; vb += gridDim.x) {
+        if (vb >= a.nb) rowonly_decay(a, err, vb - a.nb);
+        else if (!err) rowonly_wave_rows<GT, WT, C, true, kExact>(a, vb);
+    }
     rowonly_clear_flag(a, &last);
 }
 
@@ -1097,13 +1147,16 @@ __global__ __launch_bounds__(kRowOnlyMaxWaves * kWave) void ember_rowonly(RowOnl
     __shared__ int last;
     if (!kSparse) {
         if (blockIdx.x == 0 && threadIdx.x == 0) *a.status = 0;
-        rowonly_rows<GT, WT, M, S, false, kResident>(a, part, rn_lds);
+        for (int64_t vb = blockIdx.x; vb < a.nb; vb += gridDim.x)
+            rowonly_rows<GT, WT, M, S, false, kResident>(a, vb, part, rn_lds);
         return;
     }
     const int err = *a.flag;
     if (blockIdx.x == 0 && threadIdx.x == 0) *a.status = err;
-    if ((int)blockIdx.x >= a.nb) rowonly_decay(a, err);
-    else if (!err) rowonly_rows<GT, WT, M, S, true, kResident>(a, part, rn_lds);
+    for (int64_t vb = blockIdx.x; vb < a.nvb; vb += gridDim.x) {
+        if (vb >= a.nb) rowonly_decay(a, err, vb - a.nb);
+        else if (!err) rowonly_rows<GT, WT, M, S, true, kResident>(a, vb, part, rn_lds);
+    }
     rowonly_clear_flag(a, &last);
 }
 
@@ -1136,8 +1189,11 @@ __global__ __launch_bounds__(kBlock) void ember_zero(uint32_t* p, int64_t words)
 
 template <typename GT, bool kSparse>
 hipError_t stats_dispatch(const StatsParams& p, int m, dim3 grid, hipStream_t s) {
-    if (m == 1) ember_stats<GT, 1, kStatsRows, kSparse><<<grid, kBlock, 0, s>>>(p);
-    else if (m == 2) ember_stats<GT, 2, kStatsRows, kSparse><<<grid, kBlock, 0, s>>>(p);
+    const bool wide = (p.rows + (int64_t)p.nb * kWaves - 1) / ((int64_t)p.nb * kWaves) > kWideRowsPerWave;
+    if (m == 1 && !wide) ember_stats<GT, 1, kStatsRows, kSparse, false><<<grid, kBlock, 0, s>>>(p);
+    else if (m == 2 && !wide) ember_stats<GT, 2, kStatsRows, kSparse, false><<<grid, kBlock, 0, s>>>(p);
+    else if (m == 1) ember_stats<GT, 1, kStatsRows, kSparse, true><<<grid, kBlock, 0, s>>>(p);
+    else if (m == 2) ember_stats<GT, 2, kStatsRows, kSparse, true><<<grid, kBlock, 0, s>>>(p);
     else return hipErrorInvalidValue;
     return hipGetLastError();
 }
@@ -1211,6 +1267,11 @@ hipError_t rowonly_dispatch_t(const RowOnlyParams& p, int g_dtype, int w_dtype, 
 
 } // namespace
 
+// A launch's work-item count is 32 bits wide in the dispatch packet, so grids
+// stay far below 2^32 threads: kernels whose natural block count can exceed
+// kMaxGridBlocks loop over their virtual blocks.
+int64_t capped_blocks(int64_t blocks) { return blocks < kMaxGridBlocks ? blocks : kMaxGridBlocks; }
+
 ColPlan col_plan(int64_t D, int g_dtype) {
     static_assert(kSlabChunks == 64 || kSlabChunks == 128, "one or two chunks per lane");
     ColPlan cp;
@@ -1283,7 +1344,8 @@ hipError_t launch_stats(const StepArgs& a, hipStream_t s) {
     p.V = a.V;
     p.slot = reinterpret_cast<int*>(a.ws + L.slot);
     p.flag = reinterpret_cast<int*>(a.ws + L.flag);
-    const dim3 grid((unsigned)(p.nb * cp.nslab));
+    // at most 384 row blocks x D / 512 slabs: far below the 2^32-thread limit
+    const dim3 grid((unsigned)((int64_t)p.nb * cp.nslab));
     const bool sparse = a.sparse;
     if (a.g_dtype == 0)
         return sparse ? stats_dispatch<float, true>(p, cp.m, grid, s) : stats_dispatch<float, false>(p, cp.m, grid, s);
@@ -1346,7 +1408,7 @@ hipError_t launch_apply(const StepArgs& a, hipStream_t s) {
     p.eps_over_alpha = a.eps_over_alpha;
     p.status = reinterpret_cast<const int*>(a.ws + L.status);
     p.flag = reinterpret_cast<int*>(a.ws + L.flag);
-    const dim3 grid((unsigned)(p.nb * cp.nslab));
+    const dim3 grid((unsigned)capped_blocks((int64_t)p.nb * cp.nslab));
     const bool sparse = a.sparse;
     if (a.g_dtype == 0)
         return sparse ? apply_dispatch_w<float, true>(p, a.w_dtype, cp.m, grid, s)
@@ -1381,7 +1443,7 @@ hipError_t launch_rowonly(const StepArgs& a, hipStream_t s) {
     p.total_chunks = cp.total_chunks;
     p.slab_chunks = cp.slab_chunks;
     p.nslab = cp.nslab;
-    p.nb = (int)((a.rows + kRowOnlyRowsPerBlock - 1) / kRowOnlyRowsPerBlock);
+    p.nb = (a.rows + kRowOnlyRowsPerBlock - 1) / kRowOnlyRowsPerBlock;
     p.idx = a.idx;
     p.r = a.r;
     p.V = a.V;
@@ -1394,9 +1456,10 @@ hipError_t launch_rowonly(const StepArgs& a, hipStream_t s) {
     p.flag = reinterpret_cast<int*>(a.ws + L.flag);
     p.ticket = reinterpret_cast<int*>(a.ws + L.ticket);
     p.status = reinterpret_cast<int*>(a.ws + L.status);
-    const int ndecay = a.sparse ? (int)((a.V + kDecayRows - 1) / kDecayRows) : 0;
-    const dim3 grid((unsigned)(p.nb + ndecay));
-    if (p.nb + ndecay == 0) return hipSuccess;
+    const int64_t ndecay = a.sparse ? (a.V + kDecayRows - 1) / kDecayRows : 0;
+    p.nvb = p.nb + ndecay;
+    if (p.nvb == 0) return hipSuccess;
+    const dim3 grid((unsigned)capped_blocks(p.nvb));
     if (cp.total_chunks <= kRowOnlyWaveChunks) {
         int c = 1;
         while (c * kWave < cp.total_chunks) c *= 2;

@@ -84,6 +84,8 @@ constexpr int kMaxBlocks = EMBER_MAX_BLOCKS;
 constexpr int kRowsPerBlockMin = 8; // fewer rows than this per block: fewer blocks
 constexpr int kVRowsPerThread = 4;  // rows per thread in the r pass
 constexpr int kDecayRows = 1024;    // rows per decay block of the row-only sparse step
+constexpr int64_t kMaxGridBlocks = (int64_t)1 << 20;  // launched blocks per kernel at most
+int64_t capped_blocks(int64_t blocks);
 
 // Status bits written by the sparse statistics pass.
 constexpr int kFlagRange = 1;

@@ -20,7 +20,7 @@ import torch
 
 import oracle
 from paper_2607_01455_amd import workloads as wl
-from parity_checks import DEV, host_bits
+from parity_checks import DEV, as_f64 as _as_f64, check_coalesced_rows as check_rows, host_bits
 
 pytestmark = pytest.mark.gpu
 
@@ -29,43 +29,6 @@ pytestmark = pytest.mark.gpu
 def em():
     from paper_2607_01455_amd import ember
     return ember
-
-
-def _as_f64(bits: np.ndarray) -> np.ndarray:
-    if bits.dtype == np.uint16:
-        return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
-    return bits.astype(np.float64)
-
-
-def _ordered(bits: np.ndarray) -> np.ndarray:
-    if bits.dtype == np.uint16:
-        b = bits.astype(np.int64)
-        return np.where(b & 0x8000, 0x8000 - (b & 0x7FFF), 0x8000 + b)
-    b = bits.view(np.uint32).astype(np.int64)
-    return np.where(b & 0x80000000, 0x80000000 - (b & 0x7FFFFFFF), 0x80000000 + b)
-
-
-def check_rows(got: np.ndarray, want: np.ndarray, tok: np.ndarray, U64: np.ndarray, what: str):
-    """got/want: [n, D] in the row dtype (fp32 values or bf16 bits); returns the
-    number of elements that differ (each at a rounding boundary)."""
-    if np.array_equal(got.view(np.uint32) if got.dtype == np.float32 else got,
-                      want.view(np.uint32) if want.dtype == np.float32 else want):
-        return 0
-    ids, inv, counts = np.unique(tok, return_inverse=True, return_counts=True)
-    S = np.zeros(want.shape, np.float64)
-    A = np.zeros(want.shape, np.float64)
-    np.add.at(S, inv, U64)
-    np.add.at(A, inv, np.abs(U64))
-    diff = (got.view(np.uint32) != want.view(np.uint32)) if got.dtype == np.float32 else (got != want)
-    rows, cols = np.nonzero(diff)
-    d_ulp = np.abs(_ordered(got[rows, cols]) - _ordered(want[rows, cols]))
-    assert (d_ulp == 1).all(), f"{what}: {int((d_ulp > 1).sum())} elements differ by more than 1 ulp"
-    assert (counts[rows] > 1).all(), f"{what}: a single-occurrence row is not a copy"
-    mid = 0.5 * (_as_f64(got[rows, cols]) + _as_f64(want[rows, cols]))
-    bound = 2.0 * (counts[rows] - 1) * 2.0 ** -53 * A[rows, cols]
-    ok = np.abs(S[rows, cols] - mid) <= bound
-    assert ok.all(), f"{what}: {int((~ok).sum())} elements differ away from a rounding boundary"
-    return int(diff.sum())
 
 
 def run_case(em, tok_h: np.ndarray, U: torch.Tensor, V: int, g_dtype, what: str):
