@@ -65,7 +65,8 @@ typedef enum {
     EMBER_ERR_DTYPE = -4,     /* dtype is not EMBER_F32 or EMBER_BF16 */
     EMBER_ERR_WORKSPACE = -5, /* ws_bytes smaller than ember_workspace_bytes(V, D) */
     EMBER_ERR_INDEX = -6,     /* sparse step: idx holds a value outside [0, V) or a
-                                 repeated value (reported by ember_get_error) */
+                                 repeated value, or a device row count is out of
+                                 range (reported by ember_get_error) */
     EMBER_ERR_HIP = -7        /* a HIP runtime call failed */
 } ember_status;
 
@@ -133,6 +134,26 @@ int ember_step_sparse_rows(void* W, int w_dtype, int64_t ldw,
                            void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * The sparse step with its row count in device memory, for callers whose
+ * count is produced on the device (ember_coalesce_rows writes it): nothing is
+ * read back to the host, so coalescing and the step can be enqueued together
+ * or captured in one HIP graph.  n_idx_dev points to one int64 in device
+ * memory, read when the step runs; max_rows (host) bounds it and sizes the
+ * launches; G_rows and idx must hold max_rows rows.  A device count outside
+ * [0, max_rows] is reported like an index error (EMBER_ERR_INDEX through
+ * ember_get_error; W, r and c untouched).  With *n_idx_dev == max_rows the
+ * result is the same, bit for bit, as ember_step_sparse_rows with n_idx =
+ * max_rows; other counts partition the rows differently and agree within the
+ * stated tolerances.  Everything else as for ember_step_sparse_rows.
+ */
+int ember_step_sparse_rows_devn(void* W, int w_dtype, int64_t ldw,
+                                const void* G_rows, int g_dtype, int64_t ldg,
+                                const int64_t* idx, const int64_t* n_idx_dev, int64_t max_rows,
+                                float* r, float* c, int64_t V, int64_t D, int64_t t,
+                                float lr, float beta2, float eps, int maximize,
+                                void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
  * Row-only Ember (Section 2.1, the variant the paper analyses most, listed in
  * its ablation table with V floats of state): only the row statistic r is
  * kept, and each row's gradient is divided by the square root of its own
@@ -174,6 +195,15 @@ int ember_rowonly_step_sparse_rows(void* W, int w_dtype, int64_t ldw,
                                    float lr, float beta2, float eps, int maximize,
                                    void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* The row-only sparse step with its row count in device memory (as for
+ * ember_step_sparse_rows_devn). */
+int ember_rowonly_step_sparse_rows_devn(void* W, int w_dtype, int64_t ldw,
+                                        const void* G_rows, int g_dtype, int64_t ldg,
+                                        const int64_t* idx, const int64_t* n_idx_dev, int64_t max_rows,
+                                        float* r, int64_t V, int64_t D, int64_t t,
+                                        float lr, float beta2, float eps, int maximize,
+                                        void* ws, size_t ws_bytes, hipStream_t stream);
+
 /*
  * Gradient coalescing: the step before ember_step_sparse_rows.  The gradient
  * of an input embedding for one batch position is the one-hot selector of its
@@ -194,9 +224,11 @@ int ember_rowonly_step_sparse_rows(void* W, int w_dtype, int64_t ldw,
  * positions of one id are added in ascending order, within fixed chunks of the
  * id-sorted positions, and chunk partials in chunk order.  idx and G_rows feed
  * ember_step_sparse_rows directly once n is known on the host (read *n_out
- * after synchronising the stream).  Ids outside [0, V) make the call report
- * EMBER_ERR_INDEX through ember_get_error on this workspace, with n = 0 and
- * idx / G_rows unspecified.  n_tok = 0 gives n = 0 (tok, U, idx, G_rows may
+ * after synchronising the stream), or feed ember_step_sparse_rows_devn with
+ * n_out itself.  Ids outside [0, V) make the call report EMBER_ERR_INDEX
+ * through ember_get_error on this workspace and write n = -1 (which a
+ * device-count step refuses, leaving its table untouched); idx and G_rows are
+ * then unspecified.  n_tok = 0 gives n = 0 (tok, U, idx, G_rows may
  * then be NULL).  Layout and alignment rules of U and G_rows are those of W
  * and G; tok, idx and n_out must be 8-byte aligned.
  *

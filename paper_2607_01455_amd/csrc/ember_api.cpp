@@ -123,6 +123,18 @@ int run_rowonly_step(StepArgs& a, float lr, float beta2, float eps, int64_t t, i
     return e == hipSuccess ? EMBER_OK : EMBER_ERR_HIP;
 }
 
+// Arguments of the sparse steps whose row count is in device memory.
+int check_devn(const void* W, int w_dtype, int64_t ldw, const void* G_rows, int g_dtype, int64_t ldg,
+               const int64_t* idx, const int64_t* n_dev, int64_t max_rows, int64_t V, int64_t D) {
+    int st = check_shape(V, D);
+    if (st == EMBER_OK && (max_rows < 0 || max_rows > V)) st = EMBER_ERR_SHAPE;
+    if (st == EMBER_OK) st = check_matrix(W, w_dtype, ldw, D, false);
+    if (st == EMBER_OK) st = check_matrix(G_rows, g_dtype, ldg, D, max_rows == 0);
+    if (st == EMBER_OK && ((max_rows > 0 && idx == nullptr) || n_dev == nullptr)) st = EMBER_ERR_ARG;
+    if (st == EMBER_OK && ((idx != nullptr && !aligned(idx, 8)) || !aligned(n_dev, 8))) st = EMBER_ERR_ALIGN;
+    return st;
+}
+
 int check_rowonly_state(const float* r, const void* ws, size_t ws_bytes, int64_t V, int64_t D) {
     if (r == nullptr || ws == nullptr) return EMBER_ERR_ARG;
     if (!aligned(r, 4) || !aligned(ws, 256)) return EMBER_ERR_ALIGN;
@@ -277,6 +289,62 @@ int ember_rowonly_step_sparse_rows(void* W, int w_dtype, int64_t ldw, const void
     a.ldg = ldg;
     a.idx = idx;
     a.rows = n_idx;
+    a.r = r;
+    a.c = nullptr;
+    a.V = V;
+    a.D = D;
+    a.ws = static_cast<char*>(ws);
+    return run_rowonly_step(a, lr, beta2, eps, t, maximize, stream);
+}
+
+int ember_step_sparse_rows_devn(void* W, int w_dtype, int64_t ldw, const void* G_rows, int g_dtype, int64_t ldg,
+                                const int64_t* idx, const int64_t* n_idx_dev, int64_t max_rows,
+                                float* r, float* c, int64_t V, int64_t D, int64_t t,
+                                float lr, float beta2, float eps, int maximize,
+                                void* ws, size_t ws_bytes, hipStream_t stream) {
+    int st = check_devn(W, w_dtype, ldw, G_rows, g_dtype, ldg, idx, n_idx_dev, max_rows, V, D);
+    if (st == EMBER_OK) st = check_state(r, c, ws, ws_bytes, V, D);
+    if (st == EMBER_OK) st = check_scalars(t, lr, beta2, eps);
+    if (st != EMBER_OK) return st;
+    StepArgs a{};
+    a.sparse = true;
+    a.W = W;
+    a.w_dtype = w_dtype;
+    a.ldw = ldw;
+    a.G = G_rows;
+    a.g_dtype = g_dtype;
+    a.ldg = ldg;
+    a.idx = idx;
+    a.n_dev = n_idx_dev;
+    a.rows = max_rows;
+    a.r = r;
+    a.c = c;
+    a.V = V;
+    a.D = D;
+    a.ws = static_cast<char*>(ws);
+    return run_step(a, lr, beta2, eps, t, maximize, stream);
+}
+
+int ember_rowonly_step_sparse_rows_devn(void* W, int w_dtype, int64_t ldw, const void* G_rows, int g_dtype,
+                                        int64_t ldg, const int64_t* idx, const int64_t* n_idx_dev,
+                                        int64_t max_rows, float* r, int64_t V, int64_t D, int64_t t,
+                                        float lr, float beta2, float eps, int maximize,
+                                        void* ws, size_t ws_bytes, hipStream_t stream) {
+    int st = check_devn(W, w_dtype, ldw, G_rows, g_dtype, ldg, idx, n_idx_dev, max_rows, V, D);
+    if (st == EMBER_OK) st = check_rowonly_state(r, ws, ws_bytes, V, D);
+    if (st == EMBER_OK) st = check_scalars(t, lr, beta2, eps);
+    if (st != EMBER_OK) return st;
+    StepArgs a{};
+    a.sparse = true;
+    a.W = W;
+    a.w_dtype = w_dtype;
+    a.ldw = ldw;
+    a.G = G_rows;
+    a.g_dtype = g_dtype;
+    a.ldg = ldg;
+    a.idx = idx;
+    a.n_dev = n_idx_dev;
+    a.rows = max_rows;
     a.r = r;
     a.c = nullptr;
     a.V = V;

@@ -302,7 +302,7 @@ __global__ __launch_bounds__(kCoalThreads) void coal_heads_write(HeadParams a) {
         a.uid[k] = u - 1;
     }
     if (blockIdx.x == a.ntiles - 1) {
-        // index errors (marked per tile by the first sort pass) -> status, n = 0
+        // index errors (marked per tile by the first sort pass) -> status, n = -1
         uint32_t bad = 0;
         for (int k = threadIdx.x; k < a.ntiles; k += kCoalThreads) bad |= a.tile_bad[k];
         uint32_t nbad;
@@ -310,7 +310,7 @@ __global__ __launch_bounds__(kCoalThreads) void coal_heads_write(HeadParams a) {
         if (threadIdx.x == 0) {
             const uint32_t n = tile_base + total;
             a.seg_start[n] = (uint32_t)a.P;
-            *a.n_out = nbad ? 0 : (int64_t)n;
+            *a.n_out = nbad ? -1 : (int64_t)n;   // -1: a device-count step refuses it
             *a.status = nbad ? 1 : 0;
         }
     }

@@ -312,6 +312,7 @@ struct StatsParams {
     float* rowpart;      // [nslab][rows]
     float* P;            // [nb][D]
     const int64_t* idx;  // sparse only
+    const int64_t* n_dev; // sparse only: device row count, or null
     int64_t V;
     int* slot;
     int* flag;
@@ -347,6 +348,17 @@ template <int R>
 __device__ __forceinline__ float rows_sum(const float (&v)[R], int lane) {
     static_assert(R == 1 || R == 2 || R == 4 || R == 8 || R == 16, "rows per batch");
     return rows_sum_step<R, kWave / 2>(v, lane);
+}
+
+// Row count of a sparse step: the host's, or the one in device memory (then
+// a.rows is its maximum, which sizes the grids and the row-sum stride).  An
+// out-of-range device count gives no rows and sets `bad`.
+__device__ __forceinline__ int64_t active_rows(const int64_t* n_dev, int64_t rows_max, bool& bad) {
+    bad = false;
+    if (n_dev == nullptr) return rows_max;
+    const int64_t n = *n_dev;
+    bad = n < 0 || n > rows_max;
+    return bad ? 0 : n;
 }
 
 // Rows of row block b: b, b + nb, b + 2 nb, ... (interleaved: all blocks sweep
@@ -388,7 +400,10 @@ __global__ __launch_bounds__(kBlock) void ember_stats(StatsParams a) {
     const int wave = threadIdx.x / kWave;
     const int slab = (int)(blockIdx.x % (unsigned)a.nslab);
     const int b = (int)(blockIdx.x / (unsigned)a.nslab);
-    const RowSet rset = stats_rows(a.rows, a.nb, b);
+    bool bad_count = false;
+    const int64_t nrows = kSparse ? active_rows(a.n_dev, a.rows, bad_count) : a.rows;
+    if (kSparse && bad_count && blockIdx.x == 0 && threadIdx.x == 0) atomicOr(a.flag, kFlagCount);
+    const RowSet rset = stats_rows(nrows, a.nb, b);
     const int cbeg = slab * a.slab_chunks;
     const int cend = min(cbeg + a.slab_chunks, a.total_chunks);
     const GT* G = static_cast<const GT*>(a.G);
@@ -691,6 +706,7 @@ struct ApplyParams {
     int nslab;
     int nb;
     const int64_t* idx;   // sparse only
+    const int64_t* n_dev; // sparse only: device row count, or null
     const float* r;
     const float* qa;      // [D] column factors sqrt(chat_j / s) / alpha_s
     double inv_bias;
@@ -710,6 +726,8 @@ __global__ __launch_bounds__(kBlock) void ember_apply(ApplyParams a) {
         if (*a.status != 0) return;
     }
     if (a.inv_alpha == 0.0) return;   // lr == 0: every weight keeps its bits
+    bool bad_count = false;
+    const int64_t nrows = kSparse ? active_rows(a.n_dev, a.rows, bad_count) : a.rows;
 
     // (row block, slab) pairs, slab-fastest; the grid is capped, so a block may
     // take several pairs
@@ -734,7 +752,7 @@ __global__ __launch_bounds__(kBlock) void ember_apply(ApplyParams a) {
         const float ibias = (float)a.inv_bias;
 
         int64_t r0, r1;
-        row_range(a.rows, a.nb, b, r0, r1);
+        row_range(nrows, a.nb, b, r0, r1);
         const GT* G = static_cast<const GT*>(a.G);
         WT* W = static_cast<WT*>(a.W);
 
@@ -806,6 +824,7 @@ struct RowOnlyParams {
     int64_t nb;            // row blocks
     int64_t nvb;           // row blocks + decay blocks (sparse)
     const int64_t* idx;    // sparse only
+    const int64_t* n_dev;  // sparse only: device row count, or null
     float* r;
     int64_t V;
     float beta2;
@@ -825,8 +844,8 @@ struct RowOnlyParams {
 // (rows too long to hold) wave w takes slabs w, w + nw, ... and reads them
 // once for the row sum and again, with W, for the update.
 template <typename GT, typename WT, int M, int S, bool kSparse, bool kResident>
-__device__ __forceinline__ void rowonly_rows(const RowOnlyParams& a, int64_t vb, float (*part)[kRowOnlyRows],
-                                             float* rn_lds) {
+__device__ __forceinline__ void rowonly_rows(const RowOnlyParams& a, int64_t nrows, int64_t vb,
+                                             float (*part)[kRowOnlyRows], float* rn_lds) {
     constexpr int EPC = 16 / (int)sizeof(GT);
     constexpr int R = kRowOnlyRows;
     const int lane = threadIdx.x & (kWave - 1);
@@ -835,7 +854,7 @@ __device__ __forceinline__ void rowonly_rows(const RowOnlyParams& a, int64_t vb,
     const bool update = a.inv_alpha != 0.0f;
 
     const int64_t r0 = vb * kRowOnlyRowsPerBlock;
-    const int64_t r1 = min(r0 + kRowOnlyRowsPerBlock, a.rows);
+    const int64_t r1 = min(r0 + kRowOnlyRowsPerBlock, nrows);
     const GT* G = static_cast<const GT*>(a.G);
     WT* W = static_cast<WT*>(a.W);
     const double invD = 1.0 / (double)a.D;
@@ -1002,7 +1021,7 @@ __device__ __forceinline__ void rowonly_rows(const RowOnlyParams& a, int64_t vb,
 // wave takes kRowOnlyWaveRows adjacent rows at a time; the waves of a block
 // interleave over the block's rows.
 template <typename GT, typename WT, int C, bool kSparse, bool kExact>
-__device__ __forceinline__ void rowonly_wave_rows(const RowOnlyParams& a, int64_t vb) {
+__device__ __forceinline__ void rowonly_wave_rows(const RowOnlyParams& a, int64_t nrows, int64_t vb) {
     constexpr int EPC = 16 / (int)sizeof(GT);
     constexpr int R = kRowOnlyWaveRows;
     constexpr int kWBytes = EPC * (int)sizeof(WT);   // bytes of W per chunk
@@ -1010,7 +1029,7 @@ __device__ __forceinline__ void rowonly_wave_rows(const RowOnlyParams& a, int64_
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const bool update = a.inv_alpha != 0.0f;
     const int64_t r0 = vb * kRowOnlyRowsPerBlock;
-    const int64_t r1 = min(r0 + kRowOnlyRowsPerBlock, a.rows);
+    const int64_t r1 = min(r0 + kRowOnlyRowsPerBlock, nrows);
     const GT* G = static_cast<const GT*>(a.G);
     WT* W = static_cast<WT*>(a.W);
     const double invD = 1.0 / (double)a.D;
@@ -1127,14 +1146,17 @@ __global__ __launch_bounds__(kBlock) void ember_rowonly_wave(RowOnlyParams a) {
     __shared__ int last;
     if (!kSparse) {
         if (blockIdx.x == 0 && threadIdx.x == 0) *a.status = 0;
-        for (int64_t vb = blockIdx.x; vb < a.nb; vb += gridDim.x) rowonly_wave_rows<GT, WT, C, false, kExact>(a, vb);
+        for (int64_t vb = blockIdx.x; vb < a.nb; vb += gridDim.x)
+            rowonly_wave_rows<GT, WT, C, false, kExact>(a, a.rows, vb);
         return;
     }
     const int err = *a.flag;
     if (blockIdx.x == 0 && threadIdx.x == 0) *a.status = err;
+    bool bad_count = false;
+    const int64_t nrows = active_rows(a.n_dev, a.rows, bad_count);
     for (int64_t vb = blockIdx.x; vb < a.nvb; vb += gridDim.x) {
         if (vb >= a.nb) rowonly_decay(a, err, vb - a.nb);
-        else if (!err) rowonly_wave_rows<GT, WT, C, true, kExact>(a, vb);
+        else if (!err) rowonly_wave_rows<GT, WT, C, true, kExact>(a, nrows, vb);
     }
     rowonly_clear_flag(a, &last);
 }
@@ -1148,14 +1170,16 @@ __global__ __launch_bounds__(kRowOnlyMaxWaves * kWave) void ember_rowonly(RowOnl
     if (!kSparse) {
         if (blockIdx.x == 0 && threadIdx.x == 0) *a.status = 0;
         for (int64_t vb = blockIdx.x; vb < a.nb; vb += gridDim.x)
-            rowonly_rows<GT, WT, M, S, false, kResident>(a, vb, part, rn_lds);
+            rowonly_rows<GT, WT, M, S, false, kResident>(a, a.rows, vb, part, rn_lds);
         return;
     }
     const int err = *a.flag;
     if (blockIdx.x == 0 && threadIdx.x == 0) *a.status = err;
+    bool bad_count = false;
+    const int64_t nrows = active_rows(a.n_dev, a.rows, bad_count);
     for (int64_t vb = blockIdx.x; vb < a.nvb; vb += gridDim.x) {
         if (vb >= a.nb) rowonly_decay(a, err, vb - a.nb);
-        else if (!err) rowonly_rows<GT, WT, M, S, true, kResident>(a, vb, part, rn_lds);
+        else if (!err) rowonly_rows<GT, WT, M, S, true, kResident>(a, nrows, vb, part, rn_lds);
     }
     rowonly_clear_flag(a, &last);
 }
@@ -1163,8 +1187,12 @@ __global__ __launch_bounds__(kRowOnlyMaxWaves * kWave) void ember_rowonly(RowOnl
 // Sparse row-only step, first launch: validates idx and marks the touched rows
 // (slot = 1 + position in idx).  Error bits are ORed into the flag, which the
 // fused launch reads and clears.
-__global__ __launch_bounds__(kBlock) void ember_rowonly_validate(const int64_t* idx, int64_t n, int64_t V,
-                                                                int* slot, int* flag) {
+__global__ __launch_bounds__(kBlock) void ember_rowonly_validate(const int64_t* idx, int64_t n_max,
+                                                                const int64_t* n_dev, int64_t V, int* slot,
+                                                                int* flag) {
+    bool bad_count = false;
+    const int64_t n = active_rows(n_dev, n_max, bad_count);
+    if (bad_count && blockIdx.x == 0 && threadIdx.x == 0) atomicOr(flag, kFlagCount);
     const int64_t k = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     if (k >= n) return;
     const int64_t i = idx[k];
@@ -1341,6 +1369,7 @@ hipError_t launch_stats(const StepArgs& a, hipStream_t s) {
     p.rowpart = reinterpret_cast<float*>(a.ws + L.rowpart);
     p.P = reinterpret_cast<float*>(a.ws + L.p);
     p.idx = a.idx;
+    p.n_dev = a.n_dev;
     p.V = a.V;
     p.slot = reinterpret_cast<int*>(a.ws + L.slot);
     p.flag = reinterpret_cast<int*>(a.ws + L.flag);
@@ -1401,6 +1430,7 @@ hipError_t launch_apply(const StepArgs& a, hipStream_t s) {
     p.nslab = cp.nslab;
     p.nb = apply_blocks(a.rows, a.sparse);
     p.idx = a.idx;
+    p.n_dev = a.n_dev;
     p.r = a.r;
     p.qa = reinterpret_cast<const float*>(a.ws + L.qa);
     p.inv_bias = a.inv_bias;
@@ -1419,9 +1449,9 @@ hipError_t launch_apply(const StepArgs& a, hipStream_t s) {
 
 hipError_t launch_rowonly_validate(const StepArgs& a, hipStream_t s) {
     const WsLayout L = ws_layout(a.V, a.D);
-    if (a.rows == 0) return hipSuccess;
-    const unsigned nblk = (unsigned)((a.rows + kBlock - 1) / kBlock);
-    ember_rowonly_validate<<<nblk, kBlock, 0, s>>>(a.idx, a.rows, a.V, reinterpret_cast<int*>(a.ws + L.slot),
+    if (a.rows == 0 && a.n_dev == nullptr) return hipSuccess;
+    const unsigned nblk = (unsigned)(a.rows > 0 ? (a.rows + kBlock - 1) / kBlock : 1);
+    ember_rowonly_validate<<<nblk, kBlock, 0, s>>>(a.idx, a.rows, a.n_dev, a.V, reinterpret_cast<int*>(a.ws + L.slot),
                                                    reinterpret_cast<int*>(a.ws + L.flag));
     return hipGetLastError();
 }
@@ -1445,6 +1475,7 @@ hipError_t launch_rowonly(const StepArgs& a, hipStream_t s) {
     p.nslab = cp.nslab;
     p.nb = (a.rows + kRowOnlyRowsPerBlock - 1) / kRowOnlyRowsPerBlock;
     p.idx = a.idx;
+    p.n_dev = a.n_dev;
     p.r = a.r;
     p.V = a.V;
     p.beta2 = a.beta2;

@@ -90,6 +90,7 @@ int64_t capped_blocks(int64_t blocks);
 // Status bits written by the sparse statistics pass.
 constexpr int kFlagRange = 1;
 constexpr int kFlagDuplicate = 2;
+constexpr int kFlagCount = 4;       // a device-side row count outside [0, max rows]
 
 // Column tiling of one launch for a given gradient dtype (16-byte chunks).
 struct ColPlan {
@@ -150,7 +151,8 @@ struct StepArgs {
     int g_dtype;
     int64_t ldg;
     bool sparse;        // sparse-row step: G holds `rows` rows mapped through idx
-    const int64_t* idx; // device array of `rows` row indices (sparse only)
+    const int64_t* idx;
+    const int64_t* n_dev;  // sparse steps: row count in device memory (rows is then its maximum), or null // device array of `rows` row indices (sparse only)
     int64_t rows;       // V (dense) or n_idx (sparse)
     float* r;
     float* c;

@@ -30,7 +30,8 @@ EMBER_ERR_HIP = -7
 # Every function the C header declares, checked by the CPU test suite.
 EXPORTED = ("ember_workspace_bytes", "ember_init_state", "ember_step_dense",
             "ember_step_sparse_rows", "ember_rowonly_init_state", "ember_rowonly_step_dense",
-            "ember_rowonly_step_sparse_rows", "ember_coalesce_workspace_bytes", "ember_coalesce_rows",
+            "ember_rowonly_step_sparse_rows", "ember_step_sparse_rows_devn",
+            "ember_rowonly_step_sparse_rows_devn", "ember_coalesce_workspace_bytes", "ember_coalesce_rows",
             "ember_get_error", "ember_strerror",
             "ember_profile_enable", "ember_profile_collect")
 
@@ -61,6 +62,10 @@ def _load(path: str = _LIB_PATH) -> ctypes.CDLL:
                                              f32, f32, f32, i32, vp, sz, vp]
     lib.ember_rowonly_step_sparse_rows.argtypes = [vp, i32, i64, vp, i32, i64, vp, i64, vp, i64, i64, i64,
                                                    f32, f32, f32, i32, vp, sz, vp]
+    lib.ember_step_sparse_rows_devn.argtypes = [vp, i32, i64, vp, i32, i64, vp, vp, i64, vp, vp, i64, i64, i64,
+                                                f32, f32, f32, i32, vp, sz, vp]
+    lib.ember_rowonly_step_sparse_rows_devn.argtypes = [vp, i32, i64, vp, i32, i64, vp, vp, i64, vp, i64, i64,
+                                                        i64, f32, f32, f32, i32, vp, sz, vp]
     lib.ember_coalesce_workspace_bytes.argtypes = [i64, i64, i64, ctypes.POINTER(sz)]
     lib.ember_coalesce_rows.argtypes = [vp, i64, vp, i32, i64, i64, i64, vp, vp, i32, i64, vp, vp, sz, vp]
     lib.ember_get_error.argtypes = [vp, vp, ctypes.POINTER(i32)]
@@ -182,6 +187,30 @@ def ember_rowonly_step_sparse_rows(W: torch.Tensor, G_rows: torch.Tensor, idx: t
            "ember_rowonly_step_sparse_rows")
 
 
+def ember_step_sparse_rows_devn(W: torch.Tensor, G_rows: torch.Tensor, idx: torch.Tensor, n_dev: torch.Tensor,
+                                r: torch.Tensor, c, t: int, lr: float = 1e-3, beta2: float = 0.999,
+                                eps: float = 1e-8, maximize: bool = False, ws: torch.Tensor | None = None,
+                                row_only: bool = False) -> None:
+    """Sparse step whose row count n is the int64 in device tensor n_dev; G_rows
+    and idx hold the maximum count of rows (their first dimension)."""
+    V, D = W.shape
+    if idx.dtype != torch.int64 or n_dev.dtype != torch.int64:
+        raise TypeError("idx and n_dev must be int64")
+    max_rows = idx.numel()
+    ldg = _ld(G_rows) if G_rows.numel() else D
+    if row_only:
+        st = LIB.ember_rowonly_step_sparse_rows_devn(
+            _ptr(W), _dtype(W), _ld(W), _ptr(G_rows), _dtype(G_rows), ldg, _ptr(idx), n_dev.data_ptr(), max_rows,
+            _ptr(r), V, D, int(t), float(lr), float(beta2), float(eps), int(bool(maximize)), _ptr(ws),
+            ws.numel() * ws.element_size(), _stream(W))
+    else:
+        st = LIB.ember_step_sparse_rows_devn(
+            _ptr(W), _dtype(W), _ld(W), _ptr(G_rows), _dtype(G_rows), ldg, _ptr(idx), n_dev.data_ptr(), max_rows,
+            _ptr(r), _ptr(c), V, D, int(t), float(lr), float(beta2), float(eps), int(bool(maximize)), _ptr(ws),
+            ws.numel() * ws.element_size(), _stream(W))
+    _check(st, "ember_step_sparse_rows_devn")
+
+
 def ember_coalesce_workspace_bytes(max_tokens: int, V: int, D: int) -> int:
     out = ctypes.c_size_t(0)
     _check(LIB.ember_coalesce_workspace_bytes(int(max_tokens), int(V), int(D), ctypes.byref(out)),
@@ -218,6 +247,14 @@ class Coalescer:
         self.n_out = torch.zeros(1, dtype=torch.int64, device=device)
         nbytes = ember_coalesce_workspace_bytes(self.max_tokens, self.V, self.D)
         self.ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+    def enqueue(self, tok: torch.Tensor, U: torch.Tensor) -> None:
+        """Coalesce one batch on the current stream without reading n back:
+        self.idx, self.G_rows and self.n_out then feed a step with a device
+        row count (EmberTable.step_tokens)."""
+        if tok.numel() > self.max_tokens:
+            raise ValueError("batch larger than max_tokens")
+        ember_coalesce_rows(tok, U, self.V, self.idx, self.G_rows, self.n_out, self.ws)
 
     def __call__(self, tok: torch.Tensor, U: torch.Tensor):
         """Coalesce one batch; synchronises to read n.  Returns (idx, G_rows)
@@ -279,6 +316,17 @@ class EmberTable:
         else:
             ember_step_dense(W, G, self.r, self.c, self.t + 1, self.lr, self.beta2, self.eps,
                              self.maximize, self.ws)
+        self.t += 1
+
+    def step_tokens(self, W: torch.Tensor, tok: torch.Tensor, U: torch.Tensor, coalescer: "Coalescer") -> None:
+        """Sparse step from token ids and per-position gradient rows: coalescing
+        and the step are enqueued back to back with the row count kept in
+        device memory (no host synchronisation; capturable in a HIP graph).
+        Index errors of either call show in ember_get_error of its workspace."""
+        coalescer.enqueue(tok, U)
+        ember_step_sparse_rows_devn(W, coalescer.G_rows, coalescer.idx, coalescer.n_out, self.r, self.c,
+                                    self.t + 1, self.lr, self.beta2, self.eps, self.maximize, self.ws,
+                                    row_only=self.row_only)
         self.t += 1
 
     def step_sparse_rows(self, W: torch.Tensor, G_rows: torch.Tensor, idx: torch.Tensor,

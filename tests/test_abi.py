@@ -208,6 +208,32 @@ def test_coalesce_workspace_bytes(em):
     assert sizes[-1] < 2 * (1 << 25) * 8 + 64 * (1 << 20)
 
 
+def _devn(em, row_only=False, **kw):
+    a = dict(W=W_, wd=1, ldw=64, G=G_, gd=1, ldg=64, idx=IDX_, ndev=IDX_ + A, mx_rows=3, r=R_, c=C_, V=10, D=64,
+             t=1, lr=1e-3, b2=0.999, eps=1e-8, mx=0, ws=WS_, wsb=None)
+    a.update(kw)
+    if a["wsb"] is None:
+        a["wsb"] = _ws_bytes(em, max(a["V"], 1), max(a["D"], 1))
+    if row_only:
+        return em.LIB.ember_rowonly_step_sparse_rows_devn(
+            a["W"], a["wd"], a["ldw"], a["G"], a["gd"], a["ldg"], a["idx"], a["ndev"], a["mx_rows"], a["r"],
+            a["V"], a["D"], a["t"], a["lr"], a["b2"], a["eps"], a["mx"], a["ws"], a["wsb"], None)
+    return em.LIB.ember_step_sparse_rows_devn(
+        a["W"], a["wd"], a["ldw"], a["G"], a["gd"], a["ldg"], a["idx"], a["ndev"], a["mx_rows"], a["r"], a["c"],
+        a["V"], a["D"], a["t"], a["lr"], a["b2"], a["eps"], a["mx"], a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("row_only", [False, True])
+@pytest.mark.parametrize("kw,status", [
+    (dict(mx_rows=-1), "SHAPE"), (dict(mx_rows=11), "SHAPE"), (dict(ndev=None), "ARG"),
+    (dict(idx=None), "ARG"), (dict(ndev=IDX_ + A + 4), "ALIGN"), (dict(idx=IDX_ + 2), "ALIGN"),
+    (dict(G=None), "ARG"), (dict(W=None), "ARG"), (dict(r=None), "ARG"), (dict(gd=7), "DTYPE"),
+    (dict(t=0), "ARG"), (dict(wsb=0), "WORKSPACE"), (dict(V=0), "SHAPE"),
+])
+def test_device_count_steps_reject_bad_arguments_on_host(em, row_only, kw, status):
+    assert _devn(em, row_only=row_only, **kw) == getattr(em, "EMBER_ERR_" + status)
+
+
 def test_init_state_and_get_error_reject_bad_arguments(em):
     wsb = _ws_bytes(em, 10, 64)
     assert em.LIB.ember_init_state(R_, C_, 0, 64, WS_, wsb, None) == em.EMBER_ERR_SHAPE

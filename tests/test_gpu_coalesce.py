@@ -89,7 +89,7 @@ def test_coalesce_index_errors_empty_batch_and_reuse(em):
         tok = torch.tensor(bad + [1] * 7, dtype=torch.int64, device=DEV)
         em.ember_coalesce_rows(tok, U, V, co.idx, co.G_rows, co.n_out, co.ws)
         assert em.ember_get_error(co.ws) == em.EMBER_ERR_INDEX
-        assert int(co.n_out.item()) == 0
+        assert int(co.n_out.item()) == -1
     empty = torch.zeros(0, dtype=torch.int64, device=DEV)
     idx, G = co(empty, U[:0])
     assert idx.numel() == 0 and G.shape[0] == 0
