@@ -546,17 +546,20 @@ struct FinParams {
     float one_minus_beta2;
     float* rsum;           // [ceil(V / kFinRowsPerBlock)]
     float* csum;           // [ncolblocks]
-    int* ticket;           // finished blocks; the last one derives the column factors
-    float* qa;             // [D] column factors sqrt(chat_j / s) / alpha_s
+    int* ticket;           // finished blocks; the last one derives the step scale
+    float* qa;             // [D rounded up to 8] column factors sqrt(c_j)
+    float* scale;          // sqrt(1 / (bias s)) / alpha_s
     double inv_bias;
     double inv_alpha;
 };
 
 // Run by the last block of the finalize pass, once every r, c and partial sum
 // of this step is stored: s = sqrt(mean(rhat) mean(chat)) from the per-block
-// sums in a fixed order, then the column factors qa_j = sqrt(chat_j / s) / alpha_s
-// that the apply pass multiplies by the row factor sqrt(rhat_i).
-__device__ void column_factors(const FinParams& a, int nrsum, double* s_lds) {
+// sums in a fixed order, and the step scale sqrt(1 / (bias s)) / alpha_s.  The
+// preconditioner's root sqrt(rhat_i chat_j / s) / alpha_s is applied as
+// [sqrt(r_i / bias) * scale] * sqrt(c_j): a row factor times the column factor
+// the column blocks stored, which needs no pass over the columns here.
+__device__ void step_scale(const FinParams& a, int nrsum) {
     const int lane = threadIdx.x & (kWave - 1);
     if (threadIdx.x < kWave) {
         double sr = 0.0, sc = 0.0;
@@ -567,27 +570,8 @@ __device__ void column_factors(const FinParams& a, int nrsum, double* s_lds) {
         if (lane == 0) {
             const double mean_rhat = sr / (double)a.V * a.inv_bias;
             const double mean_chat = sc / (double)a.D * a.inv_bias;
-            *s_lds = sqrt(mean_rhat * mean_chat);
-        }
-    }
-    __syncthreads();
-    const double s = *s_lds;
-    const double kq = s > 0.0 ? a.inv_bias / s : 0.0;
-    // all loads of a thread first (they are coherent, i.e. uncached, loads),
-    // then sqrt(c_j * kq) / alpha_s, kq = 1 / (bias s): the product in f64
-    // (kq alone may exceed the fp32 range for tiny gradients), the root in fp32
-    const float ia = (float)a.inv_alpha;
-    for (int64_t j0 = 0; j0 < a.D; j0 += 4 * kFinThreads) {
-        float cv[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int64_t j = j0 + u * kFinThreads + threadIdx.x;
-            cv[u] = j < a.D ? ld_agent(a.c + j) : 0.0f;
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int64_t j = j0 + u * kFinThreads + threadIdx.x;
-            if (j < a.D) a.qa[j] = sqrtf((float)((double)cv[u] * kq)) * ia;
+            const double s = sqrt(mean_rhat * mean_chat);
+            *a.scale = s > 0.0 ? (float)(sqrt(a.inv_bias / s) * a.inv_alpha) : 0.0f;
         }
     }
 }
@@ -613,16 +597,15 @@ __global__ __launch_bounds__(kFinThreads) void ember_finalize(FinParams a) {
     __shared__ float part[kFinWaves][kWave];
     __shared__ float lds16[kFinWaves];
     __shared__ int last;
-    __shared__ double s_lds;
     const int err = kSparse ? *a.flag : 0;
     if (blockIdx.x == 0 && threadIdx.x == 0) *a.status = err;
     finalize_body<kSparse>(a, err, part, lds16);
 
-    // The block that finishes last derives the column factors from the stored
-    // state (c and the per-block sums are written with agent-scope stores).
+    // The block that finishes last derives the step scale from the per-block
+    // sums (written with agent-scope stores).
     if (!block_ticket(a.ticket, (int)gridDim.x, &last)) return;
     const int nrsum = (int)((a.V + kFinRowsPerBlock - 1) / kFinRowsPerBlock);
-    if (!err) column_factors(a, nrsum, &s_lds);
+    if (!err) step_scale(a, nrsum);
     if (threadIdx.x == 0) *a.ticket = 0;
 }
 
@@ -651,6 +634,7 @@ __device__ __forceinline__ void finalize_body(const FinParams& a, int err, float
                 const float mean = (float)((double)colsum / (double)a.V);
                 cn = fmaf(a.beta2, a.c[j], a.one_minus_beta2 * mean);
                 st_agent(a.c + j, cn);
+                a.qa[j] = sqrtf(cn);
             }
             cn = wave_sum(cn);
             if (lane == 0) st_agent(a.csum + blockIdx.x, cn);
@@ -708,7 +692,8 @@ struct ApplyParams {
     const int64_t* idx;   // sparse only
     const int64_t* n_dev; // sparse only: device row count, or null
     const float* r;
-    const float* qa;      // [D] column factors sqrt(chat_j / s) / alpha_s
+    const float* qa;      // [D rounded up to 8] column factors sqrt(c_j)
+    const float* scale;   // sqrt(1 / (bias s)) / alpha_s
     double inv_bias;
     double inv_alpha;     // 1 / alpha_s, alpha_s = -lr (descent) or +lr (ascent)
     float eps_over_alpha; // eps / alpha_s
@@ -740,8 +725,8 @@ __global__ __launch_bounds__(kBlock) void ember_apply(ApplyParams a) {
         const int cbeg = slab * a.slab_chunks;
         const int cend = min(cbeg + a.slab_chunks, a.total_chunks);
 
-        // Column factors sqrt(chat_j / s) / alpha_s of this lane's columns, derived
-        // once per step by the finalize pass.
+        // Column factors sqrt(c_j) of this lane's columns, stored by the finalize
+        // pass; the row factor carries sqrt(1 / bias) and the step scale.
         float qa[M][EPC];
 #pragma unroll
         for (int m = 0; m < M; ++m) {
@@ -750,6 +735,7 @@ __global__ __launch_bounds__(kBlock) void ember_apply(ApplyParams a) {
         }
         const float epsa = a.eps_over_alpha;
         const float ibias = (float)a.inv_bias;
+        const float scale = *a.scale;
 
         int64_t r0, r1;
         row_range(nrows, a.nb, b, r0, r1);
@@ -768,7 +754,7 @@ __global__ __launch_bounds__(kBlock) void ember_apply(ApplyParams a) {
                 const bool rv = k0 + j < nk;
                 const int64_t row = rv ? r0 + wave + kWaves * (k0 + j) : r0;
                 const int64_t wrow = kSparse ? a.idx[row] : row;
-                ai[j] = sqrtf(a.r[wrow] * ibias);
+                ai[j] = sqrtf(a.r[wrow] * ibias) * scale;
                 const GT* grow = G + row * a.ldg;
                 wr[j] = W + wrow * a.ldw;
 #pragma unroll
@@ -1320,6 +1306,7 @@ WsLayout ws_layout(int64_t V, int64_t D) {
     L.flag = off;
     L.status = off + 4;
     L.ticket = off + 8;
+    L.scale = off + 12;
     off = align256(12);
     L.slot = off;
     off = align256(off + (size_t)V * 4);
@@ -1404,6 +1391,7 @@ hipError_t launch_finalize(const StepArgs& a, hipStream_t s) {
     p.csum = reinterpret_cast<float*>(a.ws + L.csum);
     p.ticket = reinterpret_cast<int*>(a.ws + L.ticket);
     p.qa = reinterpret_cast<float*>(a.ws + L.qa);
+    p.scale = reinterpret_cast<float*>(a.ws + L.scale);
     p.inv_bias = a.inv_bias;
     p.inv_alpha = a.inv_alpha;
     const int nvb = (int)((a.V + kFinRowsPerBlock - 1) / kFinRowsPerBlock);
@@ -1433,6 +1421,7 @@ hipError_t launch_apply(const StepArgs& a, hipStream_t s) {
     p.n_dev = a.n_dev;
     p.r = a.r;
     p.qa = reinterpret_cast<const float*>(a.ws + L.qa);
+    p.scale = reinterpret_cast<const float*>(a.ws + L.scale);
     p.inv_bias = a.inv_bias;
     p.inv_alpha = a.inv_alpha;
     p.eps_over_alpha = a.eps_over_alpha;

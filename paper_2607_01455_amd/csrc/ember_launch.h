@@ -132,9 +132,10 @@ struct WsLayout {
     size_t flag;    // int32: index-error bits set by the sparse statistics pass
     size_t status;  // int32: status of the last step (read by ember_get_error)
     size_t ticket;  // int32: blocks of the finalize pass that have finished
+    size_t scale;   // float: sqrt(1 / (bias s)) / alpha_s of the last step
     size_t slot;    // int32[V]: 1 + position in idx of a touched row, else 0
     size_t zero_end;// [0, zero_end) must be zero before the first step
-    size_t qa;      // float[D rounded up to 8]: sqrt(chat_j / s) / alpha_s
+    size_t qa;      // float[D rounded up to 8]: column factors sqrt(c_j)
     size_t rowpart; // float[nslab][V]: per-slab row sums of g^2
     size_t rsum;    // float[ceil(V / 4096)]: per-block sums of the new r
     size_t csum;    // float[ceil(D / 64)]: per-block sums of the new c
