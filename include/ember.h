@@ -75,6 +75,11 @@ typedef enum {
 #define EMBER_MAX_V ((int64_t)0x7FFFFFFE)
 #define EMBER_MAX_D ((int64_t)(1 << 22))
 #define EMBER_MAX_TOKENS ((int64_t)(1 << 26))
+/* ember_lmhead_step: row strides of dY and H below 2^24 elements (a 64-token
+ * slice of either is then addressable with 32-bit offsets), and at most 2^30
+ * tokens. */
+#define EMBER_LMHEAD_MAX_LD ((int64_t)(1 << 24))
+#define EMBER_LMHEAD_MAX_T ((int64_t)(1 << 30))
 
 /*
  * Workspace size for a V x D table, valid for every step (dense, sparse,
@@ -244,6 +249,39 @@ int ember_coalesce_rows(const int64_t* tok, int64_t n_tok,
                         int64_t V, int64_t D,
                         int64_t* idx, void* G_rows, int g_dtype, int64_t ldg,
                         int64_t* n_out, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * LM-head step with the gradient statistics taken inside the weight-gradient
+ * GEMM.  For an LM head with logits z_m = W h_m, the cross-entropy gradient of
+ * row i is G_i = sum_m (q_mi - 1[y_m = i]) h_m (appendix "The LM Head
+ * Factorizes Like the Embedding Table"): G = dY^T H, with dY (T x V, row
+ * stride ldy) the gradient of the logits and H (T x D, row stride ldh) the
+ * hidden states, both bf16, token-major as a forward pass produces them.
+ *
+ * The call computes G with bf16 matrix instructions and fp32 accumulation,
+ * rounds it once (nearest-even) to g_dtype and stores it in G (V x D, row
+ * stride ldg; the caller keeps it, e.g. for clipping or logging), and takes
+ * the dense Ember step on W with that G.  The result is that of
+ * ember_step_dense(W, G, ...) on the stored G, up to the summation order of
+ * the row and column sums of g^2, which here are formed by the GEMM's
+ * epilogue from the stored values (fixed order, bit-reproducible), so the
+ * step does not read G a second time for its statistics.
+ *
+ * T = 0 is allowed (G = 0; dY and H may then be NULL).  W, G, r, c, t, the
+ * scalars, the workspace (ember_workspace_bytes(V, D), initialised by
+ * ember_init_state) and the error rules are those of ember_step_dense;
+ * additionally dY and H follow the layout rules of W and G, ldy and ldh must
+ * be below EMBER_LMHEAD_MAX_LD and T at most EMBER_LMHEAD_MAX_T
+ * (EMBER_ERR_SHAPE otherwise).  G must not overlap dY, H, W or the state.
+ * The row-stride padding of dY and H (columns V..ldy-1 and D..ldh-1) is read
+ * but never affects a stored value.
+ */
+int ember_lmhead_step(void* W, int w_dtype, int64_t ldw,
+                      const void* dY, int64_t ldy, const void* H, int64_t ldh, int64_t T,
+                      void* G, int g_dtype, int64_t ldg,
+                      float* r, float* c, int64_t V, int64_t D, int64_t t,
+                      float lr, float beta2, float eps, int maximize,
+                      void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * Device status of the most recent step enqueued with this workspace.

@@ -55,6 +55,8 @@ def _load():
     lib.ember_oracle_state_bytes.restype = i64
     lib.ember_oracle_coalesce.argtypes = [vp, i64, vp, i32, i64, i64, i64, vp, vp, i32, i64, vp]
     lib.ember_oracle_coalesce.restype = i32
+    lib.ember_oracle_lmhead_grad.argtypes = [vp, i64, vp, i64, i64, i64, i64, vp, i32, i64]
+    lib.ember_oracle_lmhead_grad.restype = i32
     _lib = lib
     return lib
 
@@ -142,6 +144,27 @@ def coalesce(tok: np.ndarray, U: np.ndarray, V: int, out_dtype=None):
     if st != OK:
         return st, None, None
     return st, idx[:n.value].copy(), G[:n.value].copy()
+
+
+def lmhead_grad(dY: np.ndarray, H: np.ndarray, out_dtype=np.uint16) -> np.ndarray:
+    """LM-head weight gradient G = dY^T H (appendix "The LM Head Factorizes
+    Like the Embedding Table"): dY [T, V] and H [T, D] as bf16 bits (uint16),
+    summed exactly in float64 in ascending token order and rounded once to
+    ``out_dtype`` (``np.uint16`` for bf16 bits, or ``np.float32``)."""
+    lib = _load()
+    if dY.dtype != np.uint16 or H.dtype != np.uint16:
+        raise TypeError("dY and H are bf16 bit arrays (uint16)")
+    if dY.ndim != 2 or H.ndim != 2 or dY.shape[0] != H.shape[0]:
+        raise ValueError("dY must be [T, V] and H [T, D]")
+    T, V = dY.shape
+    D = H.shape[1]
+    G = np.zeros((V, D), np.dtype(out_dtype))
+    st = lib.ember_oracle_lmhead_grad(dY.ctypes.data if T else None, _ld(dY) if T else V,
+                                      H.ctypes.data if T else None, _ld(H) if T else D, T, V, D,
+                                      G.ctypes.data, _dtype_code(G), D)
+    if st != OK:
+        raise ValueError("bad arguments for the LM-head gradient")
+    return G
 
 
 def bf16_to_f64(bits: int) -> float:

@@ -42,6 +42,10 @@
  * per-position embedding gradients of a batch summed into one row per distinct
  * token, the input of the sparse step.
  *
+ * LM-head weight gradient (ember_oracle_lmhead_grad, at the end of this file):
+ * G = dY^T H, the gradient whose statistics the LM-head step forms inside
+ * its matrix product.
+ *
  * Row-only Ember (row_only = 1).  Section 2.1 describes a variant that keeps
  * only the V row statistics, bias-corrects them and divides each row's
  * gradient by their square root (the ablation table lists it with state V);
@@ -325,4 +329,36 @@ int ember_oracle_coalesce(const int64_t* tok, int64_t P, const void* U, int u_dt
     free(acc);
     free(ids);
     return ORACLE_OK;
+}
+
+/*
+ * LM-head weight gradient.  For an LM head with logits z_m = W h_m and
+ * softmax probabilities q_m, the cross-entropy gradient of row i is
+ * G_i = sum_m (q_mi - 1[y_m = i]) h_m (appendix "The LM Head Factorizes Like
+ * the Embedding Table").  Given dY[m][i] = q_mi - 1[y_m = i] (T x V, bf16
+ * bits, row stride ldy) and the hidden states H (T x D, bf16 bits, row stride
+ * ldh), this writes G[i][j] = sum over m = 0 .. T-1 of dY[m][i] H[m][j]: the
+ * products of two bf16 values are exact in float64, the sum runs in float64
+ * in ascending m, and the result is rounded once to g_dtype (nearest-even).
+ * T = 0 gives G = 0.  Returns 0, or -1 for a bad argument.
+ */
+int ember_oracle_lmhead_grad(const uint16_t* dY, int64_t ldy, const uint16_t* H, int64_t ldh, int64_t T,
+                             int64_t V, int64_t D, void* G, int g_dtype, int64_t ldg)
+{
+    if (V < 1 || D < 1 || T < 0 || ldy < V || ldh < D || ldg < D || G == NULL) return -1;
+    if (T > 0 && (dY == NULL || H == NULL)) return -1;
+    if (g_dtype != ORACLE_F32 && g_dtype != ORACLE_BF16) return -1;
+    double* acc = (double*)malloc((size_t)D * sizeof(double));
+    if (acc == NULL) return -1;
+    for (int64_t i = 0; i < V; ++i) {
+        for (int64_t j = 0; j < D; ++j) acc[j] = 0.0;
+        for (int64_t m = 0; m < T; ++m) {
+            const double y = ember_oracle_bf16_to_f64(dY[m * ldy + i]);
+            const uint16_t* h = H + m * ldh;
+            for (int64_t j = 0; j < D; ++j) acc[j] += y * ember_oracle_bf16_to_f64(h[j]);
+        }
+        for (int64_t j = 0; j < D; ++j) store_elem(G, g_dtype, i * ldg + j, acc[j]);
+    }
+    free(acc);
+    return 0;
 }

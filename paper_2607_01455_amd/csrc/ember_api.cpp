@@ -115,6 +115,20 @@ void set_scalars(StepArgs& a, float lr, float beta2, float eps, int64_t t, int m
     a.eps_over_alpha = lr > 0.0f ? (float)((double)eps / alpha_s) : 0.0f;
 }
 
+// LM-head step: the weight-gradient GEMM writes G and the statistics
+// partials, then the finalize and apply passes of the dense step run on them.
+int run_lmhead_step(StepArgs& a, const ember::LmheadArgs& x, float lr, float beta2, float eps, int64_t t,
+                    int maximize, hipStream_t s) {
+    set_scalars(a, lr, beta2, eps, t, maximize);
+    const ember::LmheadPlan pl = ember::lmhead_plan(a.V, a.D);
+    a.fin_nb = pl.MT;
+    a.fin_nslab = pl.NT;
+    hipError_t e = timed("ember_lmhead_grad", s, [&] { return ember::launch_lmhead_grad(x, s); });
+    if (e == hipSuccess) e = timed("ember_finalize", s, [&] { return ember::launch_finalize(a, s); });
+    if (e == hipSuccess && lr > 0.0f) e = timed("ember_apply", s, [&] { return ember::launch_apply(a, s); });
+    return e == hipSuccess ? EMBER_OK : EMBER_ERR_HIP;
+}
+
 int run_rowonly_step(StepArgs& a, float lr, float beta2, float eps, int64_t t, int maximize, hipStream_t s) {
     set_scalars(a, lr, beta2, eps, t, maximize);
     hipError_t e = hipSuccess;
@@ -192,6 +206,54 @@ int ember_step_dense(void* W, int w_dtype, int64_t ldw, const void* G, int g_dty
     a.D = D;
     a.ws = static_cast<char*>(ws);
     return run_step(a, lr, beta2, eps, t, maximize, stream);
+}
+
+int ember_lmhead_step(void* W, int w_dtype, int64_t ldw,
+                      const void* dY, int64_t ldy, const void* H, int64_t ldh, int64_t T,
+                      void* G, int g_dtype, int64_t ldg,
+                      float* r, float* c, int64_t V, int64_t D, int64_t t,
+                      float lr, float beta2, float eps, int maximize,
+                      void* ws, size_t ws_bytes, hipStream_t stream) {
+    int st = check_shape(V, D);
+    if (st == EMBER_OK && (T < 0 || T > EMBER_LMHEAD_MAX_T)) st = EMBER_ERR_SHAPE;
+    if (st == EMBER_OK && (ldy >= EMBER_LMHEAD_MAX_LD || ldh >= EMBER_LMHEAD_MAX_LD)) st = EMBER_ERR_SHAPE;
+    if (st == EMBER_OK) st = check_matrix(W, w_dtype, ldw, D, false);
+    if (st == EMBER_OK) st = check_matrix(G, g_dtype, ldg, D, false);
+    if (st == EMBER_OK) st = check_matrix(dY, EMBER_BF16, ldy, V, T == 0);
+    if (st == EMBER_OK) st = check_matrix(H, EMBER_BF16, ldh, D, T == 0);
+    if (st == EMBER_OK) st = check_state(r, c, ws, ws_bytes, V, D);
+    if (st == EMBER_OK) st = check_scalars(t, lr, beta2, eps);
+    if (st != EMBER_OK) return st;
+    const WsLayout L = ember::ws_layout(V, D);
+    ember::LmheadArgs x{};
+    x.dY = dY;
+    x.ldy = ldy;
+    x.H = H;
+    x.ldh = ldh;
+    x.T = T;
+    x.V = V;
+    x.D = D;
+    x.G = G;
+    x.g_dtype = g_dtype;
+    x.ldg = ldg;
+    x.rowpart = reinterpret_cast<float*>(static_cast<char*>(ws) + L.rowpart);
+    x.P = reinterpret_cast<float*>(static_cast<char*>(ws) + L.p);
+    StepArgs a{};
+    a.sparse = false;
+    a.W = W;
+    a.w_dtype = w_dtype;
+    a.ldw = ldw;
+    a.G = G;
+    a.g_dtype = g_dtype;
+    a.ldg = ldg;
+    a.idx = nullptr;
+    a.rows = V;
+    a.r = r;
+    a.c = c;
+    a.V = V;
+    a.D = D;
+    a.ws = static_cast<char*>(ws);
+    return run_lmhead_step(a, x, lr, beta2, eps, t, maximize, stream);
 }
 
 int ember_step_sparse_rows(void* W, int w_dtype, int64_t ldw, const void* G_rows, int g_dtype, int64_t ldg,

@@ -1301,7 +1301,10 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 WsLayout ws_layout(int64_t V, int64_t D) {
     WsLayout L;
-    const int nb = row_blocks(V);
+    // the LM-head gradient GEMM writes its partials into the same regions
+    const LmheadPlan lp = lmhead_plan(V, D);
+    const int nb = row_blocks(V) > lp.MT ? row_blocks(V) : lp.MT;
+    const int nslab = nslab_for(D) > lp.NT ? nslab_for(D) : lp.NT;
     size_t off = 0;
     L.flag = off;
     L.status = off + 4;
@@ -1314,7 +1317,7 @@ WsLayout ws_layout(int64_t V, int64_t D) {
     L.qa = off;
     off = align256(off + (size_t)((D + 7) / 8 * 8) * 4);
     L.rowpart = off;
-    off = align256(off + (size_t)nslab_for(D) * (size_t)V * 4);
+    off = align256(off + (size_t)nslab * (size_t)V * 4);
     L.rsum = off;
     off = align256(off + (size_t)((V + kFinRowsPerBlock - 1) / kFinRowsPerBlock) * 4);
     L.csum = off;
@@ -1345,7 +1348,7 @@ hipError_t launch_stats(const StepArgs& a, hipStream_t s) {
     p.total_chunks = cp.total_chunks;
     p.slab_chunks = cp.slab_chunks;
     p.nslab = cp.nslab;
-    p.nb = row_blocks(a.rows, a.sparse);
+    p.nb = a.fin_nb > 0 ? a.fin_nb : row_blocks(a.rows, a.sparse);
     {
         const double row_bytes = (double)a.D * (a.g_dtype == 0 ? 4 : 2);
         const int64_t keep = (int64_t)((double)EMBER_STATS_KEEP_MB * 1048576.0 / row_bytes);
@@ -1372,11 +1375,11 @@ hipError_t launch_finalize(const StepArgs& a, hipStream_t s) {
     const WsLayout L = ws_layout(a.V, a.D);
     FinParams p;
     p.P = reinterpret_cast<const float*>(a.ws + L.p);
-    p.nb = row_blocks(a.rows, a.sparse);
+    p.nb = a.fin_nb > 0 ? a.fin_nb : row_blocks(a.rows, a.sparse);
     p.D = a.D;
     p.ncolblocks = (int)((a.D + kWave - 1) / kWave);
     p.rowpart = reinterpret_cast<const float*>(a.ws + L.rowpart);
-    p.nslab = col_plan(a.D, a.g_dtype).nslab;
+    p.nslab = a.fin_nslab > 0 ? a.fin_nslab : col_plan(a.D, a.g_dtype).nslab;
     p.rows = a.rows;
     p.V = a.V;
     p.r = a.r;

@@ -72,6 +72,12 @@ constexpr int kWaves = kBlock / kWave;
 #ifndef EMBER_COAL_RUN_ROWS
 #define EMBER_COAL_RUN_ROWS 32   // gradient coalescing: rows a wavefront sums per batch of loads
 #endif
+#ifndef EMBER_LMHEAD_PAD
+#define EMBER_LMHEAD_PAD 32      // LM-head gradient GEMM: bf16 elements of padding per LDS row
+#endif
+#ifndef EMBER_LMHEAD_GROUP_M
+#define EMBER_LMHEAD_GROUP_M 4   // LM-head gradient GEMM: row tiles per group of the tile order
+#endif
 #ifndef EMBER_MAX_BLOCKS
 #define EMBER_MAX_BLOCKS 384        // row blocks of the statistics pass
 #endif
@@ -86,6 +92,11 @@ constexpr int kVRowsPerThread = 4;  // rows per thread in the r pass
 constexpr int kDecayRows = 1024;    // rows per decay block of the row-only sparse step
 constexpr int64_t kMaxGridBlocks = (int64_t)1 << 20;  // launched blocks per kernel at most
 int64_t capped_blocks(int64_t blocks);
+
+// LM-head gradient GEMM tiles (ember_lmhead.hip): kLmheadTile x kLmheadTile
+// tiles of G, kLmheadK tokens per step.
+constexpr int kLmheadTile = 256;
+constexpr int kLmheadK = 64;
 
 // Status bits written by the sparse statistics pass.
 constexpr int kFlagRange = 1;
@@ -136,10 +147,10 @@ struct WsLayout {
     size_t slot;    // int32[V]: 1 + position in idx of a touched row, else 0
     size_t zero_end;// [0, zero_end) must be zero before the first step
     size_t qa;      // float[D rounded up to 8]: column factors sqrt(c_j)
-    size_t rowpart; // float[nslab][V]: per-slab row sums of g^2
+    size_t rowpart; // float[max(nslab, NT)][V]: per-slab (or per-column-tile) row sums of g^2
     size_t rsum;    // float[ceil(V / 4096)]: per-block sums of the new r
     size_t csum;    // float[ceil(D / 64)]: per-block sums of the new c
-    size_t p;       // float[row_blocks(V)][D]: per-block column sums of g^2
+    size_t p;       // float[max(row_blocks(V), MT)][D]: per-block (or per-row-tile) column sums of g^2
     size_t total;
 };
 WsLayout ws_layout(int64_t V, int64_t D);
@@ -165,6 +176,8 @@ struct StepArgs {
     double inv_alpha;   // 1 / (+lr or -lr); 0 when lr == 0 (no apply launch)
     float eps_over_alpha;
     char* ws;
+    int fin_nb;         // finalize: partial rows of P and row slabs of rowpart, when
+    int fin_nslab;      // they come from the LM-head gradient GEMM (0: the statistics pass's)
 };
 
 // Each launcher enqueues one kernel on `s` and returns hipGetLastError().
@@ -172,6 +185,29 @@ hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
 hipError_t launch_stats(const StepArgs& a, hipStream_t s);
 hipError_t launch_finalize(const StepArgs& a, hipStream_t s);
 hipError_t launch_apply(const StepArgs& a, hipStream_t s);
+
+// LM-head weight gradient G = dY^T H with the statistics partials in the
+// epilogue (ember_lmhead.hip): rowpart[NT][V] and P[MT][D] in the workspace.
+struct LmheadPlan {
+    int MT;   // row tiles: ceil(V / kLmheadTile)
+    int NT;   // column tiles: ceil(D / kLmheadTile)
+};
+LmheadPlan lmhead_plan(int64_t V, int64_t D);
+struct LmheadArgs {
+    const void* dY;    // [T][ldy] bf16
+    int64_t ldy;
+    const void* H;     // [T][ldh] bf16
+    int64_t ldh;
+    int64_t T;
+    int64_t V;
+    int64_t D;
+    void* G;           // [V][ldg]
+    int g_dtype;
+    int64_t ldg;
+    float* rowpart;
+    float* P;
+};
+hipError_t launch_lmhead_grad(const LmheadArgs& a, hipStream_t s);
 
 // Row-only Ember (one fused pass over the rows; the sparse step first
 // validates idx and marks the touched rows).

@@ -32,7 +32,7 @@ EXPORTED = ("ember_workspace_bytes", "ember_init_state", "ember_step_dense",
             "ember_step_sparse_rows", "ember_rowonly_init_state", "ember_rowonly_step_dense",
             "ember_rowonly_step_sparse_rows", "ember_step_sparse_rows_devn",
             "ember_rowonly_step_sparse_rows_devn", "ember_coalesce_workspace_bytes", "ember_coalesce_rows",
-            "ember_get_error", "ember_strerror",
+            "ember_lmhead_step", "ember_get_error", "ember_strerror",
             "ember_profile_enable", "ember_profile_collect")
 
 
@@ -68,6 +68,8 @@ def _load(path: str = _LIB_PATH) -> ctypes.CDLL:
                                                         i64, f32, f32, f32, i32, vp, sz, vp]
     lib.ember_coalesce_workspace_bytes.argtypes = [i64, i64, i64, ctypes.POINTER(sz)]
     lib.ember_coalesce_rows.argtypes = [vp, i64, vp, i32, i64, i64, i64, vp, vp, i32, i64, vp, vp, sz, vp]
+    lib.ember_lmhead_step.argtypes = [vp, i32, i64, vp, i64, vp, i64, i64, vp, i32, i64, vp, vp, i64, i64, i64,
+                                      f32, f32, f32, i32, vp, sz, vp]
     lib.ember_get_error.argtypes = [vp, vp, ctypes.POINTER(i32)]
     lib.ember_strerror.argtypes = [i32]
     lib.ember_strerror.restype = ctypes.c_char_p
@@ -265,6 +267,28 @@ class Coalescer:
         _check(ember_get_error(self.ws), "ember_coalesce_rows (device)")
         n = int(self.n_out.item())
         return self.idx[:n], self.G_rows[:n]
+
+
+def ember_lmhead_step(W: torch.Tensor, dY: torch.Tensor, H: torch.Tensor, G: torch.Tensor,
+                      r: torch.Tensor, c: torch.Tensor, t: int,
+                      lr: float = 1e-3, beta2: float = 0.999, eps: float = 1e-8,
+                      maximize: bool = False, ws: torch.Tensor | None = None) -> None:
+    """LM-head step: G = dY^T H (dY: T x V logits gradient, H: T x D hidden
+    states, both bf16) written to G, and the dense Ember step on W with it."""
+    V, D = W.shape
+    T = dY.shape[0]
+    if dY.dim() != 2 or H.dim() != 2 or dY.shape[1] != V or H.shape[0] != T or H.shape[1] != D:
+        raise ValueError(f"shapes: dY {tuple(dY.shape)}, H {tuple(H.shape)} for W {tuple(W.shape)}")
+    if tuple(G.shape) != (V, D):
+        raise ValueError(f"G must be {V} x {D}")
+    if T and (dY.dtype != torch.bfloat16 or H.dtype != torch.bfloat16):
+        raise TypeError("dY and H must be bfloat16")
+    ldy = _ld(dY) if T else V
+    ldh = _ld(H) if T else D
+    _check(LIB.ember_lmhead_step(_ptr(W), _dtype(W), _ld(W), _ptr(dY), ldy, _ptr(H), ldh, T,
+                                 _ptr(G), _dtype(G), _ld(G), _ptr(r), _ptr(c), V, D, int(t), float(lr),
+                                 float(beta2), float(eps), int(bool(maximize)), _ptr(ws),
+                                 ws.numel() * ws.element_size(), _stream(W)), "ember_lmhead_step")
 
 
 def ember_get_error(ws: torch.Tensor) -> int:

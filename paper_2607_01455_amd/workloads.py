@@ -28,7 +28,7 @@ class Config:
     w_dtype: torch.dtype
     g_dtype: torch.dtype
     steps: int
-    grad: str          # "normal" | "loguniform_rows" | "zipf_rows" | "sparse_zipf"
+    grad: str          # "normal" | "loguniform_rows" | "zipf_rows" | "sparse_zipf" | "logits"
     w_std: float = 0.02
     g_std: float = 1e-3
     batch_tokens: int = 0  # sparse: token ids per step
@@ -44,6 +44,10 @@ CONFIGS = {
     # 128256 x 4096 bf16 input embedding, 8 x 2048 Zipf(1.1) token ids per step
     "embed128k": Config("embed128k", 128256, 4096, torch.bfloat16, torch.bfloat16, 10, "sparse_zipf",
                         batch_tokens=8 * 2048),
+    # 128256 x 4096 bf16 LM head whose gradient is formed from 8 x 2048 tokens:
+    # logits gradient [16384, 128256] and hidden states [16384, 4096], bf16
+    "lmhead128k_wgrad": Config("lmhead128k_wgrad", 128256, 4096, torch.bfloat16, torch.bfloat16, 3, "logits",
+                               batch_tokens=8 * 2048),
     # tied 151936 x 896 fp32 table
     "tied152k": Config("tied152k", 151936, 896, torch.float32, torch.float32, 5, "normal"),
     # 262144 x 8192 bf16 table
@@ -146,6 +150,47 @@ def make_token_batch(cfg: Config, step: int, seed: int = 0, device="cuda", dtype
         r1 = min(cfg.batch_tokens, r0 + 16384)
         U[r0:r1] = (torch.randn(r1 - r0, ld, generator=g, device=device) * cfg.g_std).to(dtype)
     return tok.to(device=device, dtype=torch.int64).contiguous(), U[:, :cfg.D]
+
+
+def make_lmhead_batch(cfg: Config, step: int, seed: int = 0, device="cuda", T: int | None = None,
+                      ldy: int | None = None, ldh: int | None = None):
+    """(dY [T, V], H [T, D]), both bf16, for one step of an LM head whose
+    weight gradient is G = dY^T H (appendix "The LM Head Factorizes Like the
+    Embedding Table").
+
+    H: hidden states N(0, 1) per coordinate (after the final normalisation).
+    Targets y_m: Zipf(1.1) over the V rows.  Logits z_mi = log p_i + N(0, 1),
+    so the softmax background follows the token frequencies, as in the
+    appendix's decomposition of G into a frequency term and a target-count
+    term.  dY = (softmax(z_m) - onehot(y_m)) / T, the gradient of the mean
+    cross-entropy over the T positions.  Optional padded row strides.
+    """
+    T = cfg.batch_tokens if T is None else T
+    V, D = cfg.V, cfg.D
+    ldy = V if ldy is None else ldy
+    ldh = D if ldh is None else ldh
+    gc = _gen("cpu", seed, 3000 + step)
+    p = zipf_probs(V)
+    y = torch.multinomial(p.float(), max(T, 1), replacement=True, generator=gc)[:T].to(device)
+    logp = p.log().float().to(device)
+    g = _gen(device, seed, 3000 + step)
+    H = torch.empty(T, ldh, dtype=torch.bfloat16, device=device)
+    dY = torch.empty(T, ldy, dtype=torch.bfloat16, device=device)
+    for m0 in range(0, T, 1024):
+        m1 = min(T, m0 + 1024)
+        H[m0:m1] = torch.randn(m1 - m0, ldh, generator=g, device=device).to(torch.bfloat16)
+        z = torch.randn(m1 - m0, V, generator=g, device=device) + logp[None, :]
+        q = torch.softmax(z, dim=1)
+        q[torch.arange(m1 - m0, device=device), y[m0:m1]] -= 1.0
+        dY[m0:m1, :V] = (q / T).to(torch.bfloat16)
+        if ldy > V:
+            dY[m0:m1, V:] = torch.randn(m1 - m0, ldy - V, generator=g, device=device).to(torch.bfloat16)
+    return dY[:, :V], H[:, :D]
+
+
+def lmhead_flops(T: int, V: int, D: int) -> int:
+    """Multiply-adds of G = dY^T H, counted as two flops each."""
+    return 2 * T * V * D
 
 
 def coalesce_bytes(P: int, n: int, D: int, u_size: int, g_size: int) -> int:

@@ -62,8 +62,10 @@ def test_workspace_bytes(em):
         # at least: slot table, per-slab row sums, per-block column partials
         assert out.value >= 4 * V + 4 * V * math.ceil(D / 4096) + 4 * D
         sizes[(V, D)] = out.value
-    # fixed-size partial buffers: a few tens of MB at the largest shape
-    assert sizes[(262144, 8192)] < 64 * 2 ** 20
+    # partial buffers: per-block (or per-256-row tile) column sums and per-slab
+    # (or per-256-column tile) row sums, a few tens of MB at the largest shape
+    # (V D / 32 bytes from the tile partials: 1/64 of a bf16 gradient)
+    assert sizes[(262144, 8192)] < 80 * 2 ** 20
 
 
 # Fake, suitably aligned addresses: every call below must fail validation on
@@ -232,6 +234,43 @@ def _devn(em, row_only=False, **kw):
 ])
 def test_device_count_steps_reject_bad_arguments_on_host(em, row_only, kw, status):
     assert _devn(em, row_only=row_only, **kw) == getattr(em, "EMBER_ERR_" + status)
+
+
+DY_, H_ = 7 * A, 8 * A
+
+
+def _lmhead(em, **kw):
+    a = dict(W=W_, wd=1, ldw=64, dY=DY_, ldy=16, H=H_, ldh=64, T=32, G=G_, gd=1, ldg=64, r=R_, c=C_,
+             V=10, D=64, t=1, lr=1e-3, b2=0.999, eps=1e-8, mx=0, ws=WS_, wsb=None)
+    a.update(kw)
+    if a["wsb"] is None:
+        a["wsb"] = _ws_bytes(em, max(a["V"], 1), max(a["D"], 1))
+    return em.LIB.ember_lmhead_step(a["W"], a["wd"], a["ldw"], a["dY"], a["ldy"], a["H"], a["ldh"], a["T"],
+                                    a["G"], a["gd"], a["ldg"], a["r"], a["c"], a["V"], a["D"], a["t"],
+                                    a["lr"], a["b2"], a["eps"], a["mx"], a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(T=-1), "SHAPE"), (dict(T=2 ** 30 + 1), "SHAPE"), (dict(ldy=8), "SHAPE"), (dict(ldh=56), "SHAPE"),
+    (dict(ldy=2 ** 24, V=2 ** 24 - 8), "SHAPE"), (dict(ldh=2 ** 24, D=64), "SHAPE"),
+    (dict(V=0), "SHAPE"), (dict(ldw=32), "SHAPE"),
+    (dict(dY=None), "ARG"), (dict(H=None), "ARG"), (dict(G=None), "ARG"), (dict(W=None), "ARG"),
+    (dict(c=None), "ARG"), (dict(ws=None), "ARG"),
+    (dict(dY=DY_ + 2), "ALIGN"), (dict(H=H_ + 8), "ALIGN"), (dict(ldy=12), "ALIGN"), (dict(G=G_ + 4), "ALIGN"),
+    (dict(ws=WS_ + 64), "ALIGN"),
+    (dict(wd=5), "DTYPE"), (dict(gd=2), "DTYPE"),
+    (dict(wsb=256), "WORKSPACE"),
+    (dict(t=0), "ARG"), (dict(b2=1.5), "ARG"), (dict(lr=float("nan")), "ARG"),
+])
+def test_lmhead_step_rejects_bad_arguments_on_host(em, kw, status):
+    assert _lmhead(em, **kw) == getattr(em, "EMBER_ERR_" + status)
+
+
+def test_lmhead_step_accepts_no_tokens_without_operands(em):
+    # T = 0 lets dY and H be NULL; a bad scalar still fails on the host, so
+    # nothing is launched here
+    assert _lmhead(em, T=0, dY=None, H=None, t=0) == em.EMBER_ERR_ARG
+    assert _lmhead(em, T=0, dY=None, H=None, wsb=0) == em.EMBER_ERR_WORKSPACE
 
 
 def test_init_state_and_get_error_reject_bad_arguments(em):
