@@ -72,8 +72,14 @@ constexpr int kWaves = kBlock / kWave;
 #ifndef EMBER_COAL_RUN_ROWS
 #define EMBER_COAL_RUN_ROWS 32   // gradient coalescing: rows a wavefront sums per batch of loads
 #endif
-#ifndef EMBER_LMHEAD_PAD
-#define EMBER_LMHEAD_PAD 32      // LM-head gradient GEMM: bf16 elements of padding per LDS row
+#ifndef EMBER_LMHEAD_STAGES
+#define EMBER_LMHEAD_STAGES 2    // LM-head gradient GEMM: LDS stages (token steps in flight)
+#endif
+#ifndef EMBER_LMHEAD_SCHED
+#define EMBER_LMHEAD_SCHED 1     // LM-head gradient GEMM: interleave MFMAs with the next operand reads
+#endif
+#ifndef EMBER_LMHEAD_DMA_ASM
+#define EMBER_LMHEAD_DMA_ASM 1   // LM-head gradient GEMM: LDS-direct loads as inline assembly
 #endif
 #ifndef EMBER_LMHEAD_GROUP_M
 #define EMBER_LMHEAD_GROUP_M 4   // LM-head gradient GEMM: row tiles per group of the tile order
@@ -96,7 +102,10 @@ int64_t capped_blocks(int64_t blocks);
 // LM-head gradient GEMM tiles (ember_lmhead.hip): kLmheadTile x kLmheadTile
 // tiles of G, kLmheadK tokens per step.
 constexpr int kLmheadTile = 256;
-constexpr int kLmheadK = 64;
+#ifndef EMBER_LMHEAD_K
+#define EMBER_LMHEAD_K 64        // LM-head gradient GEMM: tokens per step
+#endif
+constexpr int kLmheadK = EMBER_LMHEAD_K;
 
 // Status bits written by the sparse statistics pass.
 constexpr int kFlagRange = 1;

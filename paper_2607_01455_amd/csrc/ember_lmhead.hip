@@ -27,6 +27,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "ember_launch.h"
 
 namespace ember {
@@ -43,15 +45,21 @@ constexpr int kThreads = 256;
 constexpr int kBM = kLmheadTile;        // rows of G per block (vocabulary)
 constexpr int kBN = kLmheadTile;        // columns of G per block (hidden)
 constexpr int kBK = kLmheadK;           // tokens per step
-constexpr int kPad = EMBER_LMHEAD_PAD;  // bf16 elements after each LDS row
-constexpr int kPitch = kBM + kPad;      // LDS row pitch (elements), both operands
-constexpr int kOperandElems = kBK * kPitch;
-constexpr int kLoads = kBK * kBM / 8 / kThreads;  // 16-byte loads per thread per operand
+constexpr int kStages = EMBER_LMHEAD_STAGES;  // LDS stages (steps in flight)
+constexpr int kRowBytes = kBM * 2;              // one token's 256 bf16 of one operand
+constexpr int kOperandBytes = kBK * kRowBytes;  // one operand's slice of a step
+constexpr int kStageBytes = 2 * kOperandBytes;  // dY slice, then H slice
+constexpr int kRowsPerLoad = kWave * 16 / kRowBytes;            // rows one wave-wide load fills (2)
+constexpr int kLoadsPerWave = kBK / kRowsPerLoad / (kThreads / kWave);  // per operand and step
 constexpr int kXcds = 8;
 constexpr int kBufferWord3 = 0x00020000;  // raw 32-bit data format, gfx9 family
 
 static_assert(kBM == kBN, "both operand slices share one LDS layout");
 static_assert(kBM == 256 && kBK % 16 == 0, "wave tiling assumes 256 x 256 tiles");
+static_assert(kStages >= 2 && kLoadsPerWave * kRowsPerLoad * (kThreads / kWave) == kBK, "load split");
+static_assert(kStages * kStageBytes <= 160 * 1024, "LDS of one CU");
+static_assert((kStages - 2) * 2 * kLoadsPerWave < 64, "vmcnt range");
+static_assert(kStages == 2 || kStages == 4 || kStages == 5, "stage rings of 2, 4 or 5");
 
 struct Params {
     const uint16_t* dY;   // [T][ldy] bf16
@@ -109,9 +117,16 @@ __device__ __forceinline__ void tile_of(const Params& a, int64_t l, int& tm, int
 // share a row.  Last, the two waves that share rows (or columns) add their
 // partials in a fixed order through LDS.
 template <typename GT>
-__device__ __forceinline__ void epilogue(const Params& a, int tm, int tn, f32x16 (&acc)[4][4], uint8_t* smem) {
+constexpr int kStripPitch = 128 * (int)sizeof(GT) + 16;    // bytes per strip row (padded)
+template <typename GT>
+constexpr int kStripBytes = 32 * kStripPitch<GT>;           // one wave's strip of 32 rows
+constexpr int kRedBytes = 4 * kLmheadTile * 4;              // rows and columns, two halves each
+
+template <typename GT>
+__device__ __forceinline__ void epilogue(const Params& a, int tm, int tn, f32x16 (&acc)[4][4], uint8_t* strip,
+                                         uint8_t* red) {
     constexpr int kEs = (int)sizeof(GT);
-    constexpr int kStripPitch = 128 * kEs + 16;            // bytes per strip row (padded)
+    constexpr int kStripPitch = ember::kStripPitch<GT>;
     constexpr int kChunksPerRow = 128 * kEs / 16;          // 16-byte chunks per strip row
     constexpr int kLanesPerRow = kChunksPerRow < kWave ? kChunksPerRow : kWave;
     constexpr int kRowsPerPass = kWave / kLanesPerRow;
@@ -122,9 +137,8 @@ __device__ __forceinline__ void epilogue(const Params& a, int tm, int tn, f32x16
     const int64_t m0 = (int64_t)tm * kBM + wm * 128;
     const int64_t n0 = (int64_t)tn * kBN + wn * 128;
     const int half = lane >> 5, col = lane & 31;
-    uint8_t* strip = smem + wave * (32 * kStripPitch);
-    float* rows_lds = reinterpret_cast<float*>(smem + 4 * 32 * kStripPitch);   // [2 column halves][256 rows]
-    float* cols_lds = rows_lds + 2 * kBM;                                        // [2 row halves][256 columns]
+    float* rows_lds = reinterpret_cast<float*>(red);   // [2 column halves][256 rows]
+    float* cols_lds = rows_lds + 2 * kBM;               // [2 row halves][256 columns]
 
     float cs[4];
 #pragma unroll
@@ -211,21 +225,77 @@ __device__ __forceinline__ void epilogue(const Params& a, int tm, int tn, f32x16
     __syncthreads();   // the next tile's first stage overwrites the LDS
 }
 
+// 16 bytes per lane from a buffer into LDS at lds_base + 16 lane (lanes
+// outside the buffer's range write zeros).  Issued as inline assembly so that
+// the compiler does not treat every later LDS read as dependent on it (it
+// would wait for all such loads before any LDS read); completion is awaited
+// explicitly with wait_vmcnt and a barrier before a stage is read.  M0 holds
+// the LDS base (wave-uniform) for the load and is restored afterwards; one
+// wait state separates its write from the load.
+__device__ __forceinline__ void load_to_lds(__amdgpu_buffer_rsrc_t rs, const void* lds_base, int voffset) {
+#if EMBER_LMHEAD_DMA_ASM
+    const uint32_t base = __builtin_amdgcn_readfirstlane(
+        (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)lds_base);
+    uint32_t saved;
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t"
+                 "buffer_load_dwordx4 %2, %3, 0 offen lds\n\ts_mov_b32 m0, %0"
+                 : "=&s"(saved)
+                 : "s"(base), "v"(voffset), "s"(rs)
+                 : "memory");
+#else
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)lds_base, 16, voffset, 0, 0, 0);
+#endif
+}
+
+// Wait until at most N vector-memory loads of this wave are outstanding
+// (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt and lgkmcnt at their
+// "no wait" maxima).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
 template <typename GT>
 __global__ __launch_bounds__(kThreads) void ember_lmhead_grad(Params a) {
-    __shared__ __attribute__((aligned(16))) uint16_t lds[2][2][kOperandElems];   // [stage][operand]
+    // kStages ring of (dY slice, H slice) of kBK tokens each, one LDS array
+    // per stage (so the compiler can tell a stage being loaded from the stage
+    // being read, and does not make the reads wait for the loads).  Each slice
+    // row (one token, 256 columns, 512 bytes) is stored unpadded, its 16-byte
+    // chunks XOR-permuted by the row: chunk c of token row k sits at position
+    // c ^ (4 (k % 4)).  The transpose reads of a quarter-wave then cover all
+    // LDS banks once (no conflicts), and every wave-wide load still fills two
+    // whole rows, as the LDS-direct load requires (lane l -> base + 16 l).
+    __shared__ __attribute__((aligned(1024))) uint8_t lds0[kStageBytes];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds1[kStageBytes];
+#if EMBER_LMHEAD_STAGES > 2
+    __shared__ __attribute__((aligned(1024))) uint8_t lds2[kStageBytes];
+#endif
+#if EMBER_LMHEAD_STAGES > 3
+    __shared__ __attribute__((aligned(1024))) uint8_t lds3[kStageBytes];
+#endif
+#if EMBER_LMHEAD_STAGES > 4
+    __shared__ __attribute__((aligned(1024))) uint8_t lds4[kStageBytes];
+#endif
+    auto stage = [&](auto sc) -> uint8_t* {
+        constexpr int k = decltype(sc)::value;
+        if constexpr (k == 0) return lds0;
+        else if constexpr (k == 1) return lds1;
+#if EMBER_LMHEAD_STAGES > 2
+        else if constexpr (k == 2) return lds2;
+#endif
+#if EMBER_LMHEAD_STAGES > 3
+        else if constexpr (k == 3) return lds3;
+#endif
+#if EMBER_LMHEAD_STAGES > 4
+        else if constexpr (k == 4) return lds4;
+#endif
+        else return nullptr;
+    };
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
     const int wave = tid / kWave;
     const int wm = wave & 1, wn = wave >> 1;
-
-    // copy slice: thread -> rows tid / 32 + 8 q, 16-byte column chunk tid % 32
-    const int ld_row = tid >> 5, ld_chunk = tid & 31;
-    // transpose-read base (elements) of this lane within a stage: token
-    // 8 (lane / 32) + (lane % 16) / 4, column 16 ((lane / 16) % 2) + 4 (lane % 4)
-    const int tr_base = (8 * (lane >> 5) + ((lane & 15) >> 2)) * kPitch + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-    const int a_base = tr_base + wm * 128;
-    const int b_base = tr_base + wn * 128;
 
     // one tile per block (a loop over tiles would keep per-lane epilogue
     // values live across the contraction); blocks of one XCD take consecutive
@@ -233,83 +303,152 @@ __global__ __launch_bounds__(kThreads) void ember_lmhead_grad(Params a) {
     const int64_t l = a.tile0 + (int64_t)(blockIdx.x % kXcds) * a.per_xcd + blockIdx.x / kXcds;
     if (l >= a.tile1) return;
     const int64_t nk = (a.T + kBK - 1) / kBK;
-    {
-        int tm, tn;
-        tile_of(a, l, tm, tn);
-        const int64_t v0 = (int64_t)tm * kBM;
-        const int64_t d0 = (int64_t)tn * kBN;
+    int tm, tn;
+    tile_of(a, l, tm, tn);
+    const int64_t v0 = (int64_t)tm * kBM;
+    const int64_t d0 = (int64_t)tn * kBN;
 
-        u32x4 sa[kLoads], sb[kLoads];
-        auto gload = [&](int64_t kt) {
-            const int64_t k0 = kt * kBK;
-            const uint16_t* pa = a.dY + k0 * a.ldy + v0;
-            const uint16_t* pb = a.H + k0 * a.ldh + d0;
-            const __amdgpu_buffer_rsrc_t ra = rsrc(pa, ((a.T - k0) * a.ldy - v0) * 2);
-            const __amdgpu_buffer_rsrc_t rb = rsrc(pb, ((a.T - k0) * a.ldh - d0) * 2);
+    // loads: wave w fills slice row pairs w, w + 4, ...; lane l writes row
+    // 2 j + l / 32 at chunk position l % 32, i.e. global chunk (l % 32) ^ 4 (row % 4)
+    int off_y[kLoadsPerWave], off_h[kLoadsPerWave];
 #pragma unroll
-            for (int q = 0; q < kLoads; ++q) {
-                const int row = ld_row + 8 * q;
-                sa[q] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                            ra, (int)((row * a.ldy + ld_chunk * 8) * 2), 0, 0));
-                sb[q] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                            rb, (int)((row * a.ldh + ld_chunk * 8) * 2), 0, 0));
-            }
-        };
-        auto lstore = [&](int stage) {
-#pragma unroll
-            for (int q = 0; q < kLoads; ++q) {
-                const int off = (ld_row + 8 * q) * kPitch + ld_chunk * 8;
-                *reinterpret_cast<u32x4*>(&lds[stage][0][off]) = sa[q];
-                *reinterpret_cast<u32x4*>(&lds[stage][1][off]) = sb[q];
-            }
-        };
-
-        f32x16 acc[4][4];
-#pragma unroll
-        for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-            for (int nt = 0; nt < 4; ++nt)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) acc[mt][nt][i] = 0.0f;
-
-        if (nk > 0) {
-            gload(0);
-            lstore(0);
-        }
-        if (nk > 1) gload(1);
-        __syncthreads();
-        for (int64_t kt = 0; kt < nk; ++kt) {
-            const int st = (int)(kt & 1);
-            const uint16_t* As = lds[st][0];
-            const uint16_t* Bs = lds[st][1];
-#pragma unroll
-            for (int kk = 0; kk < kBK / 16; ++kk) {
-                bf16x8 af[4], bfr[4];
-#pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    const int oa = a_base + kk * 16 * kPitch + t * 32;
-                    const int ob = b_base + kk * 16 * kPitch + t * 32;
-                    const i16x4 a_lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(As + oa));
-                    const i16x4 a_hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(As + oa + 4 * kPitch));
-                    const i16x4 b_lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(Bs + ob));
-                    const i16x4 b_hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(Bs + ob + 4 * kPitch));
-                    af[t] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(a_lo, a_hi, 0, 1, 2, 3, 4, 5, 6, 7));
-                    bfr[t] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(b_lo, b_hi, 0, 1, 2, 3, 4, 5, 6, 7));
-                }
-#pragma unroll
-                for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-                    for (int nt = 0; nt < 4; ++nt)
-                        acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mt], bfr[nt], acc[mt][nt], 0, 0, 0);
-            }
-            if (kt + 1 < nk) {
-                lstore(st ^ 1);
-                if (kt + 2 < nk) gload(kt + 2);
-            }
-            __syncthreads();
-        }
-        epilogue<GT>(a, tm, tn, acc, reinterpret_cast<uint8_t*>(&lds[0][0][0]));
+    for (int i = 0; i < kLoadsPerWave; ++i) {
+        const int row = kRowsPerLoad * (wave + 4 * i) + lane / 32;
+        const int chunk = (lane & 31) ^ (4 * (row & 3));
+        off_y[i] = (int)((row * a.ldy + chunk * 8) * 2);
+        off_h[i] = (int)((row * a.ldh + chunk * 8) * 2);
     }
+    auto issue = [&](int64_t kt, uint8_t* st) {
+        // past the last step the resources cover no bytes: the loads write
+        // zeros into a stage that is not read again
+        const bool in = kt < nk;
+        const int64_t k0 = in ? kt * kBK : 0;
+        const __amdgpu_buffer_rsrc_t ra = rsrc(a.dY + k0 * a.ldy + v0, in ? ((a.T - k0) * a.ldy - v0) * 2 : 0);
+        const __amdgpu_buffer_rsrc_t rb = rsrc(a.H + k0 * a.ldh + d0, in ? ((a.T - k0) * a.ldh - d0) * 2 : 0);
+#pragma unroll
+        for (int i = 0; i < kLoadsPerWave; ++i) {
+            uint8_t* dst = st + (wave + 4 * i) * (kRowsPerLoad * kRowBytes);
+            load_to_lds(ra, dst, off_y[i]);
+            load_to_lds(rb, dst + kOperandBytes, off_h[i]);
+        }
+    };
+
+    // transpose reads: lane l reads token row 8 (l / 32) + (l % 16) / 4 (+ 4),
+    // columns 16 ((l / 16) % 2) + 4 (l % 4) + 32 t of its wave's 128; with the
+    // chunk permutation the byte offset of tile t within a row is
+    // 16 (chunk ^ 4 (row % 4)) + 8 (l % 2), and row % 4 = (l % 16) / 4 here
+    const int tr_row = 8 * (lane >> 5) + ((lane & 15) >> 2);
+    int tr_a[4], tr_b[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        const int cpart = t * 4 + 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1);
+        const int pos = cpart ^ (4 * (tr_row & 3));
+        tr_a[t] = tr_row * kRowBytes + (wm * 16 + pos) * 16 + 8 * (lane & 1);
+        tr_b[t] = tr_row * kRowBytes + (wn * 16 + pos) * 16 + 8 * (lane & 1) + kOperandBytes;
+    }
+    auto rd = [&](const uint8_t* p) {
+        return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
+    };
+    auto frags = [&](const uint8_t* st, int kk, bf16x8 (&af)[4], bf16x8 (&bfr)[4]) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const uint8_t* pa = st + tr_a[t] + kk * 16 * kRowBytes;
+            const uint8_t* pb = st + tr_b[t] + kk * 16 * kRowBytes;
+            af[t] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(rd(pa), rd(pa + 4 * kRowBytes),
+                                                                      0, 1, 2, 3, 4, 5, 6, 7));
+            bfr[t] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(rd(pb), rd(pb + 4 * kRowBytes),
+                                                                       0, 1, 2, 3, 4, 5, 6, 7));
+        }
+    };
+
+    f32x16 acc[4][4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) acc[mt][nt][i] = 0.0f;
+
+    // step kt (stage kt % kStages): this wave's loads of step kt are done
+    // once at most the later steps' are outstanding; the barrier makes every
+    // wave's visible and frees the stage of step kt - 1, which then takes the
+    // loads of step kt + kStages - 1
+    auto step = [&](int64_t kt, auto sc) {
+        constexpr int k = decltype(sc)::value;
+        wait_vmcnt<(kStages - 2) * 2 * kLoadsPerWave>();
+        __syncthreads();
+        // the first sub-step's operand reads go out first, the loads of step
+        // kt + kStages - 1 behind them (the loads' inline assembly is a
+        // compiler memory barrier, so this order holds): the read latency
+        // overlaps the load issue, and the loads still have the whole step
+        const uint8_t* st = stage(sc);
+        bf16x8 af[2][4], bfr[2][4];
+        frags(st, 0, af[0], bfr[0]);
+        issue(kt + kStages - 1, stage(std::integral_constant<int, (k + kStages - 1) % kStages>{}));
+        // scheduling fences between sub-steps: the MFMAs of sub-step kk use
+        // operands read in an earlier region, and the reads of sub-step kk + 1
+        // fill their shadow (without the fences the scheduler fetches every
+        // operand just before its MFMA and waits for it)
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int kk = 0; kk < kBK / 16; ++kk) {
+            const int cur = kk & 1;
+            if (kk + 1 < kBK / 16) frags(st, kk + 1, af[cur ^ 1], bfr[cur ^ 1]);
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+                for (int nt = 0; nt < 4; ++nt)
+                    acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][mt], bfr[cur][nt], acc[mt][nt],
+                                                                          0, 0, 0);
+#if EMBER_LMHEAD_SCHED
+            // one MFMA, then one transpose read for the next sub-step
+            if (kk + 1 < kBK / 16) {
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                }
+            }
+#endif
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+    // steps 0 .. kStages - 2 before the loop; step kStages - 1 is issued by step 0
+    issue(0, lds0);
+#if EMBER_LMHEAD_STAGES > 2
+    issue(1, lds1);
+    issue(2, lds2);
+#endif
+#if EMBER_LMHEAD_STAGES > 4
+    issue(3, lds3);
+#endif
+    // whole rounds of kStages steps (one loop exit keeps the accumulators in
+    // place); the up to kStages - 1 steps past the last one multiply the zeros
+    // their loads wrote, which adds exact zeros
+    for (int64_t kt = 0; kt < nk; kt += kStages) {
+        step(kt, std::integral_constant<int, 0>{});
+        step(kt + 1, std::integral_constant<int, 1>{});
+#if EMBER_LMHEAD_STAGES > 2
+        step(kt + 2, std::integral_constant<int, 2>{});
+        step(kt + 3, std::integral_constant<int, 3>{});
+#endif
+#if EMBER_LMHEAD_STAGES > 4
+        step(kt + 4, std::integral_constant<int, 4>{});
+#endif
+    }
+    wait_vmcnt<0>();   // the zero-filling loads past the end, before the LDS is reused
+    // epilogue scratch: the wave strips spread over the stage arrays, the
+    // block's partial sums after the strips in lds1
+    constexpr int kStrip = kStripBytes<GT>;
+    static_assert((kStages > 3 ? 1 : 2) * kStrip + kRedBytes <= kStageBytes, "epilogue scratch fits the stages");
+#if EMBER_LMHEAD_STAGES > 3
+    uint8_t* const strip = wave == 0 ? lds0 : wave == 1 ? lds1 : wave == 2 ? lds2 : lds3;
+    uint8_t* const red = lds1 + kStrip;
+#else
+    uint8_t* const strip = ((wave & 1) ? lds1 : lds0) + (wave >> 1) * kStrip;
+    uint8_t* const red = lds1 + 2 * kStrip;
+#endif
+    epilogue<GT>(a, tm, tn, acc, strip, red);
 }
 
 } // namespace
