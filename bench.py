@@ -30,6 +30,9 @@ V, D = 128256, 4096
 KERNEL_SRC = os.path.join(ROOT, "paper_2607_01455_amd", "csrc", "ember_kernels.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ember_apply_lmhead128k_traffic.txt")
 ROWONLY_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ember_rowonly_lmhead128k_traffic.txt")
+LMHEAD_SRC = os.path.join(ROOT, "paper_2607_01455_amd", "csrc", "ember_lmhead.hip")
+LMHEAD_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ember_lmhead_grad_lmhead128k_wgrad_traffic.txt")
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 
 
 def parse():
@@ -42,17 +45,18 @@ def parse():
     p.add_argument("--no-other-configs", action="store_true")
     p.add_argument("--no-row-only", action="store_true")
     p.add_argument("--no-coalesce", action="store_true")
+    p.add_argument("--no-lmhead-wgrad", action="store_true")
     return p.parse_args()
 
 
-def kernel_source_hash() -> str:
-    with open(KERNEL_SRC, "rb") as f:
+def kernel_source_hash(src=KERNEL_SRC) -> str:
+    with open(src, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def traffic_for_current_kernel(path=TRAFFIC_FILE):
-    """HBM bytes per launch of the dense kernel a committed PMC summary covers,
-    if it was taken on the current kernel source (else None)."""
+def traffic_for_current_kernel(path=TRAFFIC_FILE, src=KERNEL_SRC):
+    """HBM bytes per launch of the kernel a committed PMC summary covers, if
+    it was taken on the current source of that kernel (else None)."""
     rec = {}
     try:
         with open(path) as f:
@@ -62,7 +66,7 @@ def traffic_for_current_kernel(path=TRAFFIC_FILE):
                     rec[k.strip()] = v.strip()
     except OSError:
         return None
-    if rec.get("kernel_source_sha256_16") != kernel_source_hash():
+    if rec.get("kernel_source_sha256_16") != kernel_source_hash(src):
         return None
     try:
         return int(rec["hbm_bytes_per_launch"])
@@ -260,6 +264,71 @@ def coalesce_section(ember, wl, torch, dev, K, Wm):
             "tokens_to_sparse_step_ms": round(e2e_ms, 4)}
 
 
+def lmhead_wgrad_section(ember, wl, torch, dev, K, Wm):
+    """The LM-head step with the statistics fused into the weight-gradient GEMM
+    (ember_lmhead_step): G = dY^T H for 8 x 2048 tokens (logits gradient
+    16384 x 128256 and hidden states 16384 x 4096, bf16) and the Ember step on
+    the 128256 x 4096 bf16 head, against the same work done as a library GEMM
+    (torch.matmul) followed by the two-pass dense step.  The GEMM kernel is
+    timed with HIP events around each launch: MFMA roofline at the bf16 peak."""
+    cfg = wl.CONFIGS["lmhead128k_wgrad"]
+    V_, D_, T = cfg.V, cfg.D, cfg.batch_tokens
+    batches = [wl.make_lmhead_batch(cfg, t + 1, seed=35, device=dev) for t in range(2)]
+    W = wl.make_weights(cfg, seed=35, device=dev)
+    G = torch.empty(V_, D_, dtype=torch.bfloat16, device=dev)
+    tab = ember.EmberTable(V_, D_, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def fused(k):
+        dY, H = batches[k % 2]
+        tab.step_lmhead(W, dY, H, G)
+
+    def unfused(k):
+        dY, H = batches[k % 2]
+        torch.matmul(dY.t(), H, out=G)
+        tab.step(W, G)
+
+    def timed(fn, n):
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for k in range(n):
+            fn(k)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    for k in range(Wm):
+        fused(k)
+        unfused(k)
+    fused_ms = timed(fused, K)
+    unfused_ms = timed(unfused, K)
+    gemm_ms = timed(lambda k: torch.matmul(batches[k % 2][0].t(), batches[k % 2][1], out=G), K)
+    ember.ember_profile_enable(True)
+    timed(fused, K)
+    ember.ember_profile_enable(False)
+    st = ember.ember_profile_collect()
+    n, tot = st["ember_lmhead_grad"]
+    k_ms = tot / n
+    flops = wl.lmhead_flops(T, V_, D_)
+    tflops = flops / (k_ms * 1e-3) / 1e12
+    del batches, W, G, tab
+    torch.cuda.empty_cache()
+    return {"workload": f"lmhead128k_wgrad: G = dY^T H for T={T} tokens, V={V_}, D={D_} bf16, then the "
+                        "Ember step on the bf16 head",
+            "fused_step_ms": round(fused_ms, 4),
+            "library_gemm_plus_two_pass_step_ms": round(unfused_ms, 4),
+            "library_gemm_ms": round(gemm_ms, 4),
+            "speedup_vs_library_path": round(unfused_ms / fused_ms, 4),
+            "kernels_ms_avg": {k: round(v[1] / v[0], 4) for k, v in st.items()},
+            "roofline": {"kernel": "ember_lmhead_grad (GEMM + statistics epilogue)", "bound": "mfma",
+                         "achieved": round(tflops, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                         "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+                         "traffic": traffic_for_current_kernel(LMHEAD_TRAFFIC_FILE, LMHEAD_SRC),
+                         "avg_launch_ms": round(k_ms, 4), "flops_per_launch": flops}}
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -422,6 +491,7 @@ def main():
         "torch_device_copy_GBps": round(copy_gbps, 1),
         "row_only": None,
         "coalesce": None,
+        "lmhead_wgrad": None,
         "other_configs": None,
         "cpu_baseline": None,
     }
@@ -430,9 +500,12 @@ def main():
         out["row_only"] = row_only_section(ember, wl, torch, dev, K, Wm, W_head, W_emb, grads, batches)
     if not args.no_coalesce:
         out["coalesce"] = coalesce_section(ember, wl, torch, dev, K, Wm)
-    if not args.no_other_configs:
+    if not args.no_other_configs or not args.no_lmhead_wgrad:
         del W_head, W_emb, grads, batches
         torch.cuda.empty_cache()
+    if not args.no_lmhead_wgrad:
+        out["lmhead_wgrad"] = lmhead_wgrad_section(ember, wl, torch, dev, K, Wm)
+    if not args.no_other_configs:
         out["other_configs"] = other_configs(ember, wl, torch, dev, K)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.cpu_rows)

@@ -13,16 +13,20 @@
 // as it reduces the statistics pass's partials, so the step's first read of G
 // is gone.
 //
-// Tiling: one block of 4 wavefronts computes a 256 x 256 tile of G (256 rows of
-// the vocabulary, 256 hidden columns); wavefront w owns the 128 x 128 quarter
-// (w % 2, w / 2) as 4 x 4 MFMA 32x32x16 tiles.  The contraction runs over the
-// tokens in steps of 64.  Both operands are stored token-major (the token index
-// is the outer one), so each step's 64 x 256 slices are copied to LDS as they
-// are (16-byte loads and stores) and turned into the MFMA operand layout (8
-// consecutive tokens per lane) by the LDS transpose read ds_read_b64_tr_b16.
-// Two LDS stages: the loads of step k + 2 are in flight while step k is
-// multiplied.  Tiles are numbered so that the blocks one XCD runs at a time
-// share a few row tiles and a window of column tiles (its L2 holds them).
+// Tiling: one block computes a 256 x 256 tile of G (256 rows of the
+// vocabulary, 256 hidden columns) with 8 wavefronts, two per SIMD, so one
+// wave's MFMAs run while the other waits on LDS or a barrier; wave w owns the
+// 64 x 128 part (w % 4, w / 4) as 2 x 4 MFMA 32x32x16 tiles (a 4-wave form
+// with 128 x 128 parts is a compile-time option).  The contraction runs over
+// the tokens in steps of 64.  Both operands are stored token-major, so each
+// step's 64 x 256 slices go from global memory straight into LDS as they are
+// (16-byte buffer loads with an LDS destination) and are turned into the MFMA
+// operand layout (8 consecutive tokens per lane) by the LDS transpose read
+// ds_read_b64_tr_b16.  A ring of LDS stages keeps the loads of the next
+// step(s) in flight while a step is multiplied, and the operand reads of
+// each 16-token sub-step run in the shadow of the previous sub-step's MFMAs.
+// Tiles are numbered so that the blocks one XCD runs at a time share a few
+// row tiles and a window of column tiles (its L2 holds their slices).
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -41,7 +45,10 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
-constexpr int kThreads = 256;
+constexpr int kGemmWaves = EMBER_LMHEAD_WAVES;  // wavefronts per block: 4 or 8
+constexpr int kThreads = kGemmWaves * kWave;
+constexpr int kWavesN = 2;                      // wave grid over the tile: kWavesM x 2
+constexpr int kWavesM = kGemmWaves / kWavesN;
 constexpr int kBM = kLmheadTile;        // rows of G per block (vocabulary)
 constexpr int kBN = kLmheadTile;        // columns of G per block (hidden)
 constexpr int kBK = kLmheadK;           // tokens per step
@@ -50,13 +57,18 @@ constexpr int kRowBytes = kBM * 2;              // one token's 256 bf16 of one o
 constexpr int kOperandBytes = kBK * kRowBytes;  // one operand's slice of a step
 constexpr int kStageBytes = 2 * kOperandBytes;  // dY slice, then H slice
 constexpr int kRowsPerLoad = kWave * 16 / kRowBytes;            // rows one wave-wide load fills (2)
-constexpr int kLoadsPerWave = kBK / kRowsPerLoad / (kThreads / kWave);  // per operand and step
+constexpr int kLoadsPerWave = kBK / kRowsPerLoad / kGemmWaves;  // per operand and step
+constexpr int kWaveRows = kBM / kWavesM;        // rows of one wave's part of the tile (128 or 64)
+constexpr int kWaveCols = kBN / kWavesN;        // its columns (128)
+constexpr int kMT = kWaveRows / 32;             // 32 x 32 MFMA tiles per wave: kMT x kNT
+constexpr int kNT = kWaveCols / 32;
 constexpr int kXcds = 8;
 constexpr int kBufferWord3 = 0x00020000;  // raw 32-bit data format, gfx9 family
 
 static_assert(kBM == kBN, "both operand slices share one LDS layout");
 static_assert(kBM == 256 && kBK % 16 == 0, "wave tiling assumes 256 x 256 tiles");
-static_assert(kStages >= 2 && kLoadsPerWave * kRowsPerLoad * (kThreads / kWave) == kBK, "load split");
+static_assert(kGemmWaves == 4 || kGemmWaves == 8, "4 or 8 wavefronts per block");
+static_assert(kStages >= 2 && kLoadsPerWave * kRowsPerLoad * kGemmWaves == kBK, "load split");
 static_assert(kStages * kStageBytes <= 160 * 1024, "LDS of one CU");
 static_assert((kStages - 2) * 2 * kLoadsPerWave < 64, "vmcnt range");
 static_assert(kStages == 2 || kStages == 4 || kStages == 5, "stage rings of 2, 4 or 5");
@@ -108,121 +120,135 @@ __device__ __forceinline__ void tile_of(const Params& a, int64_t l, int& tm, int
     tn = (int)(q / gm);
 }
 
-// Epilogue of one tile.  Each wavefront takes its 128 x 128 quarter in four
-// strips of 32 rows: the strip's values are rounded to the G dtype (the
-// statistics are taken from the rounded values, as the step would read them)
-// and written to a wave-private LDS strip in the MFMA layout; the column sums
-// are accumulated on the way.  The strip is then read back row by row, stored
-// to G with 16-byte stores, and its row sums are formed by the lanes that
-// share a row.  Last, the two waves that share rows (or columns) add their
+// Epilogue of one tile.  Each wavefront takes its kWaveRows x 128 part in
+// strips of kStripRows rows: the strip's values are rounded to the G dtype
+// (the statistics are taken from the rounded values, as the step would read
+// them) and written to a wave-private LDS strip in the MFMA layout; the column
+// sums are accumulated on the way.  The strip is then read back row by row,
+// stored to G with 16-byte stores, and its row sums are formed by the lanes
+// that share a row.  Last, the waves that share rows (or columns) add their
 // partials in a fixed order through LDS.
+template <typename GT>
+constexpr int kStripRows = (kGemmWaves == 8 && sizeof(GT) == 4) ? 16 : 32;
 template <typename GT>
 constexpr int kStripPitch = 128 * (int)sizeof(GT) + 16;    // bytes per strip row (padded)
 template <typename GT>
-constexpr int kStripBytes = 32 * kStripPitch<GT>;           // one wave's strip of 32 rows
-constexpr int kRedBytes = 4 * kLmheadTile * 4;              // rows and columns, two halves each
+constexpr int kStripBytes = kStripRows<GT> * kStripPitch<GT>;
+constexpr int kRedBytes = (kWavesN + kWavesM) * kLmheadTile * 4;   // row and column partials
 
 template <typename GT>
-__device__ __forceinline__ void epilogue(const Params& a, int tm, int tn, f32x16 (&acc)[4][4], uint8_t* strip,
+__device__ __forceinline__ void epilogue(const Params& a, int tm, int tn, f32x16 (&acc)[kMT][kNT], uint8_t* strip,
                                          uint8_t* red) {
     constexpr int kEs = (int)sizeof(GT);
-    constexpr int kStripPitch = ember::kStripPitch<GT>;
+    constexpr int kRows = kStripRows<GT>;
+    constexpr int kPitch = kStripPitch<GT>;
     constexpr int kChunksPerRow = 128 * kEs / 16;          // 16-byte chunks per strip row
     constexpr int kLanesPerRow = kChunksPerRow < kWave ? kChunksPerRow : kWave;
     constexpr int kRowsPerPass = kWave / kLanesPerRow;
     constexpr int kEpc = 16 / kEs;                          // elements per chunk
+    constexpr int kRegsPerStrip = kRows / 2;                // MFMA registers i of one strip
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
-    const int wm = wave & 1, wn = wave >> 1;
-    const int64_t m0 = (int64_t)tm * kBM + wm * 128;
-    const int64_t n0 = (int64_t)tn * kBN + wn * 128;
+    const int wm = wave % kWavesM, wn = wave / kWavesM;
+    const int64_t m0 = (int64_t)tm * kBM + wm * kWaveRows;
+    const int64_t n0 = (int64_t)tn * kBN + wn * kWaveCols;
     const int half = lane >> 5, col = lane & 31;
-    float* rows_lds = reinterpret_cast<float*>(red);   // [2 column halves][256 rows]
-    float* cols_lds = rows_lds + 2 * kBM;               // [2 row halves][256 columns]
+    float* rows_lds = reinterpret_cast<float*>(red);   // [kWavesN][256 rows]
+    float* cols_lds = rows_lds + kWavesN * kBM;         // [kWavesM][256 columns]
 
-    float cs[4];
+    float cs[kNT];
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) cs[nt] = 0.0f;
+    for (int nt = 0; nt < kNT; ++nt) cs[nt] = 0.0f;
     // read-back mapping: lane -> row pass offset lane / kLanesPerRow, chunk lane % kLanesPerRow
     const int rb_row = lane / kLanesPerRow, rb_chunk = lane % kLanesPerRow;
 
     __syncthreads();   // every wave is done with the operand stages
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
-        const int64_t mstrip = m0 + mt * 32;
+    for (int mt = 0; mt < kMT; ++mt) {
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) {
-            const bool nv = n0 + nt * 32 + col < a.D;
+        for (int sp = 0; sp < 32 / kRows; ++sp) {
+            // rows sp * kRows .. of the 32-row MFMA tile: registers i with
+            // 8 (i / 4) + 4 half + i % 4 in that range, i.e. i in [sp kRows / 2, ...)
+            const int64_t mstrip = m0 + mt * 32 + sp * kRows;
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int r = 8 * (i >> 2) + 4 * half + (i & 3);
-                const bool v = nv && mstrip + r < a.V;
-                float g;
-                uint8_t* e = strip + r * kStripPitch + (nt * 32 + col) * kEs;
-                if constexpr (kEs == 2) {
-                    const uint32_t h = f32_to_bf16_bits(acc[mt][nt][i]);
-                    *reinterpret_cast<uint16_t*>(e) = (uint16_t)h;
-                    g = bf16_bits_to_f32(h);
-                } else {
-                    g = acc[mt][nt][i];
-                    *reinterpret_cast<float*>(e) = g;
-                }
-                cs[nt] += v ? g * g : 0.0f;
-            }
-        }
-        __syncthreads();
-        // read back, store, row sums
+            for (int nt = 0; nt < kNT; ++nt) {
+                const bool nv = n0 + nt * 32 + col < a.D;
 #pragma unroll
-        for (int pass = 0; pass < 32 / kRowsPerPass; ++pass) {
-            const int r = pass * kRowsPerPass + rb_row;
-            const int64_t m = mstrip + r;
-            const int64_t n = n0 + rb_chunk * kEpc;
-            const u32x4 w = *reinterpret_cast<const u32x4*>(strip + r * kStripPitch + rb_chunk * 16);
-            float rsum = 0.0f;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                if constexpr (kEs == 2) {
-                    const float lo = bf16_bits_to_f32(w[q] & 0xFFFFu), hi = bf16_bits_to_f32(w[q] >> 16);
-                    rsum += n + 2 * q < a.D ? lo * lo : 0.0f;
-                    rsum += n + 2 * q + 1 < a.D ? hi * hi : 0.0f;
-                } else {
-                    const float x = __uint_as_float(w[q]);
-                    rsum += n + q < a.D ? x * x : 0.0f;
+                for (int ii = 0; ii < kRegsPerStrip; ++ii) {
+                    const int i = sp * kRegsPerStrip + ii;
+                    const int r = 8 * (i >> 2) + 4 * half + (i & 3) - sp * kRows;
+                    const bool v = nv && mstrip + r < a.V;
+                    float g;
+                    uint8_t* e = strip + r * kPitch + (nt * 32 + col) * kEs;
+                    if constexpr (kEs == 2) {
+                        const uint32_t h = f32_to_bf16_bits(acc[mt][nt][i]);
+                        *reinterpret_cast<uint16_t*>(e) = (uint16_t)h;
+                        g = bf16_bits_to_f32(h);
+                    } else {
+                        g = acc[mt][nt][i];
+                        *reinterpret_cast<float*>(e) = g;
+                    }
+                    cs[nt] += v ? g * g : 0.0f;
                 }
             }
-            if (m < a.V) {
-                char* grow = static_cast<char*>(a.G) + (m * a.ldg + n) * kEs;
-                if (n + kEpc <= a.D) {
-                    *reinterpret_cast<u32x4*>(grow) = w;
-                } else {
-                    for (int e = 0; e < kEpc && n + e < a.D; ++e) {
-                        if constexpr (kEs == 2)
-                            reinterpret_cast<uint16_t*>(grow)[e] = (uint16_t)(w[e >> 1] >> (16 * (e & 1)));
-                        else
-                            reinterpret_cast<uint32_t*>(grow)[e] = w[e];
+            __syncthreads();
+            // read back, store, row sums
+#pragma unroll
+            for (int pass = 0; pass < kRows / kRowsPerPass; ++pass) {
+                const int r = pass * kRowsPerPass + rb_row;
+                const int64_t m = mstrip + r;
+                const int64_t n = n0 + rb_chunk * kEpc;
+                const u32x4 w = *reinterpret_cast<const u32x4*>(strip + r * kPitch + rb_chunk * 16);
+                float rsum = 0.0f;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    if constexpr (kEs == 2) {
+                        const float lo = bf16_bits_to_f32(w[q] & 0xFFFFu), hi = bf16_bits_to_f32(w[q] >> 16);
+                        rsum += n + 2 * q < a.D ? lo * lo : 0.0f;
+                        rsum += n + 2 * q + 1 < a.D ? hi * hi : 0.0f;
+                    } else {
+                        const float x = __uint_as_float(w[q]);
+                        rsum += n + q < a.D ? x * x : 0.0f;
                     }
                 }
-            }
+                if (m < a.V) {
+                    char* grow = static_cast<char*>(a.G) + (m * a.ldg + n) * kEs;
+                    if (n + kEpc <= a.D) {
+                        *reinterpret_cast<u32x4*>(grow) = w;
+                    } else {
+                        for (int e = 0; e < kEpc && n + e < a.D; ++e) {
+                            if constexpr (kEs == 2)
+                                reinterpret_cast<uint16_t*>(grow)[e] = (uint16_t)(w[e >> 1] >> (16 * (e & 1)));
+                            else
+                                reinterpret_cast<uint32_t*>(grow)[e] = w[e];
+                        }
+                    }
+                }
 #pragma unroll
-            for (int x = 1; x < kLanesPerRow; x <<= 1) rsum += __shfl_xor(rsum, x);
-            if (rb_chunk == 0) rows_lds[wn * kBM + wm * 128 + mt * 32 + r] = rsum;
+                for (int x = 1; x < kLanesPerRow; x <<= 1) rsum += __shfl_xor(rsum, x);
+                if (rb_chunk == 0) rows_lds[wn * kBM + wm * kWaveRows + mt * 32 + sp * kRows + r] = rsum;
+            }
+            __syncthreads();   // the strip is rewritten next
         }
-        __syncthreads();   // the strip is rewritten by the next mt
     }
     // columns: rows of the low lane half, then of the high half
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) {
+    for (int nt = 0; nt < kNT; ++nt) {
         const float other = __shfl_xor(cs[nt], 32);
         const float c2 = half == 0 ? cs[nt] + other : other + cs[nt];
-        if (half == 0) cols_lds[wm * kBN + wn * 128 + nt * 32 + col] = c2;
+        if (half == 0) cols_lds[wm * kBN + wn * kWaveCols + nt * 32 + col] = c2;
     }
     __syncthreads();
     const int x = threadIdx.x;
-    const int64_t m = (int64_t)tm * kBM + x;
-    if (m < a.V) a.rowpart[(int64_t)tn * a.V + m] = rows_lds[x] + rows_lds[kBM + x];
-    const int64_t n = (int64_t)tn * kBN + x;
-    if (n < a.D) a.P[(int64_t)tm * a.D + n] = cols_lds[x] + cols_lds[kBN + x];
-    __syncthreads();   // the next tile's first stage overwrites the LDS
+    if (x < kBM) {
+        const int64_t m = (int64_t)tm * kBM + x;
+        if (m < a.V) a.rowpart[(int64_t)tn * a.V + m] = rows_lds[x] + rows_lds[kBM + x];
+        const int64_t n = (int64_t)tn * kBN + x;
+        float c = cols_lds[x];
+#pragma unroll
+        for (int q = 1; q < kWavesM; ++q) c += cols_lds[q * kBN + x];
+        if (n < a.D) a.P[(int64_t)tm * a.D + n] = c;
+    }
 }
 
 // 16 bytes per lane from a buffer into LDS at lds_base + 16 lane (lanes
@@ -295,7 +321,7 @@ __global__ __launch_bounds__(kThreads) void ember_lmhead_grad(Params a) {
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
     const int wave = tid / kWave;
-    const int wm = wave & 1, wn = wave >> 1;
+    const int wm = wave % kWavesM, wn = wave / kWavesM;
 
     // one tile per block (a loop over tiles would keep per-lane epilogue
     // values live across the contraction); blocks of one XCD take consecutive
@@ -308,12 +334,12 @@ __global__ __launch_bounds__(kThreads) void ember_lmhead_grad(Params a) {
     const int64_t v0 = (int64_t)tm * kBM;
     const int64_t d0 = (int64_t)tn * kBN;
 
-    // loads: wave w fills slice row pairs w, w + 4, ...; lane l writes row
+    // loads: wave w fills slice row pairs w, w + kGemmWaves, ...; lane l writes row
     // 2 j + l / 32 at chunk position l % 32, i.e. global chunk (l % 32) ^ 4 (row % 4)
     int off_y[kLoadsPerWave], off_h[kLoadsPerWave];
 #pragma unroll
     for (int i = 0; i < kLoadsPerWave; ++i) {
-        const int row = kRowsPerLoad * (wave + 4 * i) + lane / 32;
+        const int row = kRowsPerLoad * (wave + kGemmWaves * i) + lane / 32;
         const int chunk = (lane & 31) ^ (4 * (row & 3));
         off_y[i] = (int)((row * a.ldy + chunk * 8) * 2);
         off_h[i] = (int)((row * a.ldh + chunk * 8) * 2);
@@ -327,45 +353,52 @@ __global__ __launch_bounds__(kThreads) void ember_lmhead_grad(Params a) {
         const __amdgpu_buffer_rsrc_t rb = rsrc(a.H + k0 * a.ldh + d0, in ? ((a.T - k0) * a.ldh - d0) * 2 : 0);
 #pragma unroll
         for (int i = 0; i < kLoadsPerWave; ++i) {
-            uint8_t* dst = st + (wave + 4 * i) * (kRowsPerLoad * kRowBytes);
+            uint8_t* dst = st + (wave + kGemmWaves * i) * (kRowsPerLoad * kRowBytes);
             load_to_lds(ra, dst, off_y[i]);
             load_to_lds(rb, dst + kOperandBytes, off_h[i]);
         }
     };
 
     // transpose reads: lane l reads token row 8 (l / 32) + (l % 16) / 4 (+ 4),
-    // columns 16 ((l / 16) % 2) + 4 (l % 4) + 32 t of its wave's 128; with the
-    // chunk permutation the byte offset of tile t within a row is
+    // columns 16 ((l / 16) % 2) + 4 (l % 4) + 32 t of its wave's part; with
+    // the chunk permutation the byte offset of tile t within a row is
     // 16 (chunk ^ 4 (row % 4)) + 8 (l % 2), and row % 4 = (l % 16) / 4 here
     const int tr_row = 8 * (lane >> 5) + ((lane & 15) >> 2);
-    int tr_a[4], tr_b[4];
+    const int cpart = 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1);
+    int tr_a[kMT], tr_b[kNT];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-        const int cpart = t * 4 + 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1);
-        const int pos = cpart ^ (4 * (tr_row & 3));
-        tr_a[t] = tr_row * kRowBytes + (wm * 16 + pos) * 16 + 8 * (lane & 1);
-        tr_b[t] = tr_row * kRowBytes + (wn * 16 + pos) * 16 + 8 * (lane & 1) + kOperandBytes;
+    for (int t = 0; t < kMT; ++t) {
+        const int chunk = wm * (kWaveRows / 8) + t * 4 + cpart;
+        tr_a[t] = tr_row * kRowBytes + (chunk ^ (4 * (tr_row & 3))) * 16 + 8 * (lane & 1);
+    }
+#pragma unroll
+    for (int t = 0; t < kNT; ++t) {
+        const int chunk = wn * (kWaveCols / 8) + t * 4 + cpart;
+        tr_b[t] = tr_row * kRowBytes + (chunk ^ (4 * (tr_row & 3))) * 16 + 8 * (lane & 1) + kOperandBytes;
     }
     auto rd = [&](const uint8_t* p) {
         return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
     };
-    auto frags = [&](const uint8_t* st, int kk, bf16x8 (&af)[4], bf16x8 (&bfr)[4]) {
+    auto frags = [&](const uint8_t* st, int kk, bf16x8 (&af)[kMT], bf16x8 (&bfr)[kNT]) {
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
+        for (int t = 0; t < kMT; ++t) {
             const uint8_t* pa = st + tr_a[t] + kk * 16 * kRowBytes;
-            const uint8_t* pb = st + tr_b[t] + kk * 16 * kRowBytes;
             af[t] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(rd(pa), rd(pa + 4 * kRowBytes),
                                                                       0, 1, 2, 3, 4, 5, 6, 7));
+        }
+#pragma unroll
+        for (int t = 0; t < kNT; ++t) {
+            const uint8_t* pb = st + tr_b[t] + kk * 16 * kRowBytes;
             bfr[t] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(rd(pb), rd(pb + 4 * kRowBytes),
                                                                        0, 1, 2, 3, 4, 5, 6, 7));
         }
     };
 
-    f32x16 acc[4][4];
+    f32x16 acc[kMT][kNT];
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
+    for (int mt = 0; mt < kMT; ++mt)
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt)
+        for (int nt = 0; nt < kNT; ++nt)
 #pragma unroll
             for (int i = 0; i < 16; ++i) acc[mt][nt][i] = 0.0f;
 
@@ -382,7 +415,7 @@ __global__ __launch_bounds__(kThreads) void ember_lmhead_grad(Params a) {
         // compiler memory barrier, so this order holds): the read latency
         // overlaps the load issue, and the loads still have the whole step
         const uint8_t* st = stage(sc);
-        bf16x8 af[2][4], bfr[2][4];
+        bf16x8 af[2][kMT], bfr[2][kNT];
         frags(st, 0, af[0], bfr[0]);
         issue(kt + kStages - 1, stage(std::integral_constant<int, (k + kStages - 1) % kStages>{}));
         // scheduling fences between sub-steps: the MFMAs of sub-step kk use
@@ -390,28 +423,38 @@ __global__ __launch_bounds__(kThreads) void ember_lmhead_grad(Params a) {
         // fill their shadow (without the fences the scheduler fetches every
         // operand just before its MFMA and waits for it)
         __builtin_amdgcn_sched_barrier(0);
+#if EMBER_LMHEAD_PRIO
+        __builtin_amdgcn_s_setprio(1);   // MFMA phase: issue ahead of the other wave's copy work
+#endif
 #pragma unroll
         for (int kk = 0; kk < kBK / 16; ++kk) {
             const int cur = kk & 1;
             if (kk + 1 < kBK / 16) frags(st, kk + 1, af[cur ^ 1], bfr[cur ^ 1]);
 #pragma unroll
-            for (int mt = 0; mt < 4; ++mt)
+            for (int mt = 0; mt < kMT; ++mt)
 #pragma unroll
-                for (int nt = 0; nt < 4; ++nt)
+                for (int nt = 0; nt < kNT; ++nt)
                     acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][mt], bfr[cur][nt], acc[mt][nt],
                                                                           0, 0, 0);
 #if EMBER_LMHEAD_SCHED
             // one MFMA, then one transpose read for the next sub-step
             if (kk + 1 < kBK / 16) {
+                constexpr int kM = kMT * kNT, kR = 2 * (kMT + kNT);
+                constexpr int kRpm = (kR + kM - 1) / kM;   // reads after each MFMA
 #pragma unroll
-                for (int i = 0; i < 16; ++i) {
+                for (int i = 0; i < kM; ++i) {
                     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+#pragma unroll
+                    for (int q = 0; q < kRpm; ++q)
+                        if (i * kRpm + q < kR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
                 }
             }
 #endif
             __builtin_amdgcn_sched_barrier(0);
         }
+#if EMBER_LMHEAD_PRIO
+        __builtin_amdgcn_s_setprio(0);
+#endif
     };
     // steps 0 .. kStages - 2 before the loop; step kStages - 1 is issued by step 0
     issue(0, lds0);
@@ -437,17 +480,23 @@ __global__ __launch_bounds__(kThreads) void ember_lmhead_grad(Params a) {
 #endif
     }
     wait_vmcnt<0>();   // the zero-filling loads past the end, before the LDS is reused
-    // epilogue scratch: the wave strips spread over the stage arrays, the
-    // block's partial sums after the strips in lds1
+    // epilogue scratch: wave w's strip in stage array w % kStages (after the
+    // strips of the lower waves there), the block's partial sums after the
+    // strips in lds1
     constexpr int kStrip = kStripBytes<GT>;
-    static_assert((kStages > 3 ? 1 : 2) * kStrip + kRedBytes <= kStageBytes, "epilogue scratch fits the stages");
-#if EMBER_LMHEAD_STAGES > 3
-    uint8_t* const strip = wave == 0 ? lds0 : wave == 1 ? lds1 : wave == 2 ? lds2 : lds3;
-    uint8_t* const red = lds1 + kStrip;
-#else
-    uint8_t* const strip = ((wave & 1) ? lds1 : lds0) + (wave >> 1) * kStrip;
-    uint8_t* const red = lds1 + 2 * kStrip;
+    constexpr int kStripsPerArray = (kGemmWaves + kStages - 1) / kStages;
+    static_assert(kStripsPerArray * kStrip + kRedBytes <= kStageBytes, "epilogue scratch fits the stages");
+    const int sarr = wave % kStages;
+    uint8_t* const sbase = sarr == 0 ? lds0 : sarr == 1 ? lds1
+#if EMBER_LMHEAD_STAGES > 2
+                                   : sarr == 2 ? lds2 : sarr == 3 ? lds3
 #endif
+#if EMBER_LMHEAD_STAGES > 4
+                                   : sarr == 4 ? lds4
+#endif
+                                   : lds0;
+    uint8_t* const strip = sbase + (wave / kStages) * kStrip;
+    uint8_t* const red = lds1 + kStripsPerArray * kStrip;
     epilogue<GT>(a, tm, tn, acc, strip, red);
 }
 

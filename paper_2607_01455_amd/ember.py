@@ -342,6 +342,16 @@ class EmberTable:
                              self.maximize, self.ws)
         self.t += 1
 
+    def step_lmhead(self, W: torch.Tensor, dY: torch.Tensor, H: torch.Tensor, G: torch.Tensor) -> None:
+        """LM-head step from the logits gradient dY [T, V] and hidden states
+        H [T, D] (bf16): G = dY^T H is written to G and the step takes its
+        statistics from the GEMM's epilogue (canonical Ember only)."""
+        if self.row_only:
+            raise ValueError("the fused LM-head step is the canonical (row and column) step")
+        ember_lmhead_step(W, dY, H, G, self.r, self.c, self.t + 1, self.lr, self.beta2, self.eps,
+                          self.maximize, self.ws)
+        self.t += 1
+
     def step_tokens(self, W: torch.Tensor, tok: torch.Tensor, U: torch.Tensor, coalescer: "Coalescer") -> None:
         """Sparse step from token ids and per-position gradient rows: coalescing
         and the step are enqueued back to back with the row count kept in
