@@ -194,3 +194,56 @@ def test_full_lmhead128k_wgrad_step(em):
     del W, G, tab
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(600)
+def test_ragged_shape_with_many_tiles(em):
+    # 79 x 4 tiles of which the last row and column tiles are partial, and a
+    # partial last token step: every element of G is checked
+    run_steps(em, 1000, 20001, 1000, torch.bfloat16, torch.bfloat16, 1, seed=21, ldy_pad=1)
+
+
+def test_captured_step_replays_bitwise(em):
+    """The fused step captured in a HIP graph and replayed on fresh inputs gives
+    the bits of the same step run eagerly on a twin table, replay after replay."""
+    T, V, D = 300, 3000, 512
+    cfg = wl.Config("lmh_graph", V, D, torch.bfloat16, torch.bfloat16, 1, "logits", batch_tokens=T)
+    ldy = (V + 7) // 8 * 8
+
+    def table():
+        return (wl.make_weights(cfg, seed=23, device=DEV), torch.empty(V, D, dtype=torch.bfloat16, device=DEV),
+                em.EmberTable(V, D, device=DEV))
+
+    W, G, tab = table()
+    W2, G2, tab2 = table()
+    dY_s = torch.empty(T, ldy, dtype=torch.bfloat16, device=DEV)[:, :V]
+    H_s = torch.empty(T, D, dtype=torch.bfloat16, device=DEV)
+    t_fixed = 4
+
+    def step(W_, G_, tab_, dY, H):
+        tab_.t = t_fixed - 1
+        tab_.step_lmhead(W_, dY, H, G_)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        dY0, H0 = wl.make_lmhead_batch(cfg, 1, seed=23, device=DEV, ldy=ldy)
+        dY_s.copy_(dY0)
+        H_s.copy_(H0)
+        step(W, G, tab, dY_s, H_s)
+        step(W2, G2, tab2, dY0, H0)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step(W, G, tab, dY_s, H_s)
+    for rep in range(2, 5):
+        dY, H = wl.make_lmhead_batch(cfg, rep, seed=23, device=DEV, ldy=ldy)
+        dY_s.copy_(dY)
+        H_s.copy_(H)
+        graph.replay()
+        step(W2, G2, tab2, dY, H)
+        torch.cuda.synchronize()
+        assert torch.equal(G.view(torch.int16), G2.view(torch.int16))
+        assert torch.equal(W.view(torch.int16), W2.view(torch.int16))
+        assert torch.equal(tab.r, tab2.r) and torch.equal(tab.c, tab2.c)
