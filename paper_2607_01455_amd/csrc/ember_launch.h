@@ -84,9 +84,6 @@ constexpr int kWaves = kBlock / kWave;
 #ifndef EMBER_LMHEAD_WAVES
 #define EMBER_LMHEAD_WAVES 8     // LM-head gradient GEMM: wavefronts per 256 x 256 tile (4 or 8)
 #endif
-#ifndef EMBER_LMHEAD_PRIO
-#define EMBER_LMHEAD_PRIO 0      // LM-head gradient GEMM: raise the wave priority over MFMA phases
-#endif
 #ifndef EMBER_LMHEAD_GROUP_M
 #define EMBER_LMHEAD_GROUP_M 2   // LM-head gradient GEMM: row tiles per group of the tile order
 #endif

@@ -423,9 +423,6 @@ __global__ __launch_bounds__(kThreads) void ember_lmhead_grad(Params a) {
         // fill their shadow (without the fences the scheduler fetches every
         // operand just before its MFMA and waits for it)
         __builtin_amdgcn_sched_barrier(0);
-#if EMBER_LMHEAD_PRIO
-        __builtin_amdgcn_s_setprio(1);   // MFMA phase: issue ahead of the other wave's copy work
-#endif
 #pragma unroll
         for (int kk = 0; kk < kBK / 16; ++kk) {
             const int cur = kk & 1;
@@ -452,9 +449,6 @@ __global__ __launch_bounds__(kThreads) void ember_lmhead_grad(Params a) {
 #endif
             __builtin_amdgcn_sched_barrier(0);
         }
-#if EMBER_LMHEAD_PRIO
-        __builtin_amdgcn_s_setprio(0);
-#endif
     };
     // steps 0 .. kStages - 2 before the loop; step kStages - 1 is issued by step 0
     issue(0, lds0);

@@ -66,7 +66,8 @@ def check_grad(G_bits: np.ndarray, dY64: np.ndarray, H64: np.ndarray, what: str)
     return float(np.mean(g == e32))
 
 
-def run_steps(em, T, V, D, g_dtype, w_dtype, steps, seed, ldy_pad=0, ldh_pad=0, nan_pad=False):
+def run_steps(em, T, V, D, g_dtype, w_dtype, steps, seed, ldy_pad=0, ldh_pad=0, nan_pad=False,
+              lr=LR, maximize=False):
     cfg = wl.Config("lmh", V, D, w_dtype, g_dtype, steps, "logits", batch_tokens=T)
     print(f"lmhead step T={T} V={V} D={D} G={g_dtype} W={w_dtype} pads=({ldy_pad},{ldh_pad}) nan={nan_pad}",
           flush=True)
@@ -87,12 +88,12 @@ def run_steps(em, T, V, D, g_dtype, w_dtype, steps, seed, ldy_pad=0, ldh_pad=0, 
             full_h[:, D:] = float("nan")
         W_prev = host_bits(W)
         tab.t = t - 1
-        em.ember_lmhead_step(W, dY, H, G, tab.r, tab.c, t, LR, B2, EPS, False, tab.ws)
+        em.ember_lmhead_step(W, dY, H, G, tab.r, tab.c, t, lr, B2, EPS, maximize, tab.ws)
         torch.cuda.synchronize()
         G_h = host_bits(G)
         frac = check_grad(G_h, as_f64(host_bits(dY)), as_f64(host_bits(H)), f"G step {t}")
         W_ref = W_prev.copy()
-        assert oracle.step(W_ref, G_h, r_o, c_o, t) == 0
+        assert oracle.step(W_ref, G_h, r_o, c_o, t, lr=lr, maximize=maximize) == 0
         check_state(tab.r, r_o, f"r step {t}")
         check_state(tab.c, c_o, f"c step {t}")
         check_w(host_bits(W), W_ref, W_prev, f"W step {t}")
@@ -247,3 +248,12 @@ def test_captured_step_replays_bitwise(em):
         assert torch.equal(G.view(torch.int16), G2.view(torch.int16))
         assert torch.equal(W.view(torch.int16), W2.view(torch.int16))
         assert torch.equal(tab.r, tab2.r) and torch.equal(tab.c, tab2.c)
+
+
+def test_ascent_and_zero_learning_rate(em):
+    # maximize: the paper's literal ascent; lr = 0: the state advances and W
+    # keeps every bit (the apply pass is skipped)
+    run_steps(em, 120, 700, 300, torch.bfloat16, torch.float32, 2, seed=25, maximize=True)
+    W, _, _ = run_steps(em, 120, 700, 300, torch.bfloat16, torch.bfloat16, 2, seed=26, lr=0.0)
+    cfg = wl.Config("lmh", 700, 300, torch.bfloat16, torch.bfloat16, 1, "logits", batch_tokens=120)
+    assert torch.equal(W.view(torch.int16), wl.make_weights(cfg, seed=26, device=DEV).view(torch.int16))
