@@ -40,7 +40,6 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
-typedef short i16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
@@ -285,8 +284,9 @@ __device__ __forceinline__ void wait_vmcnt() {
 template <typename GT>
 __global__ __launch_bounds__(kThreads) void ember_lmhead_grad(Params a) {
     // kStages ring of (dY slice, H slice) of kBK tokens each, one LDS array
-    // per stage (so the compiler can tell a stage being loaded from the stage
-    // being read, and does not make the reads wait for the loads).  Each slice
+    // per stage, addressed statically (the step loop is unrolled by the ring
+    // size; with the compiler's load builtin this also lets it tell the stage
+    // being loaded from the stage being read).  Each slice
     // row (one token, 256 columns, 512 bytes) is stored unpadded, its 16-byte
     // chunks XOR-permuted by the row: chunk c of token row k sits at position
     // c ^ (4 (k % 4)).  The transpose reads of a quarter-wave then cover all
@@ -434,7 +434,8 @@ __global__ __launch_bounds__(kThreads) void ember_lmhead_grad(Params a) {
                     acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][mt], bfr[cur][nt], acc[mt][nt],
                                                                           0, 0, 0);
 #if EMBER_LMHEAD_SCHED
-            // one MFMA, then one transpose read for the next sub-step
+            // each MFMA followed by its share of the next sub-step's transpose
+            // reads (one with 4 wavefronts, two with 8)
             if (kk + 1 < kBK / 16) {
                 constexpr int kM = kMT * kNT, kR = 2 * (kMT + kNT);
                 constexpr int kRpm = (kR + kM - 1) / kM;   // reads after each MFMA
