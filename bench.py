@@ -74,6 +74,11 @@ def traffic_for_current_kernel(path=TRAFFIC_FILE, src=KERNEL_SRC):
         return None
 
 
+def traffic_rate(traffic, ms):
+    """HBM GB/s from the PMC bytes per launch and the launch's average duration."""
+    return None if traffic is None or not ms else round(traffic / (ms * 1e-3) / 1e9, 1)
+
+
 def cpu_baseline(rows: int, steps: int = 3):
     """The oracle on the first `rows` rows of the LM-head table (dense, bf16)."""
     import numpy as np
@@ -204,6 +209,8 @@ def row_only_section(ember, wl, torch, dev, K, Wm, W_head, W_emb, grads, batches
                      "achieved": round(fused_gbps, 1), "peak": PEAK_GBPS, "unit": "GB/s",
                      "frac": round(fused_gbps / PEAK_GBPS, 4),
                      "traffic": traffic_for_current_kernel(ROWONLY_TRAFFIC_FILE),
+                     "traffic_GBps": traffic_rate(traffic_for_current_kernel(ROWONLY_TRAFFIC_FILE),
+                                                  fused_avg_ms),
                      "avg_launch_ms": round(fused_avg_ms, 5),
                      "algorithmic_bytes_per_launch": dense_bytes},
     }
@@ -326,6 +333,8 @@ def lmhead_wgrad_section(ember, wl, torch, dev, K, Wm):
                          "achieved": round(tflops, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                          "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
                          "traffic": traffic_for_current_kernel(LMHEAD_TRAFFIC_FILE, LMHEAD_SRC),
+                         "traffic_GBps": traffic_rate(
+                             traffic_for_current_kernel(LMHEAD_TRAFFIC_FILE, LMHEAD_SRC), k_ms),
                          "avg_launch_ms": round(k_ms, 4), "flops_per_launch": flops}}
 
 
@@ -485,6 +494,7 @@ def main():
             "unit": "GB/s",
             "frac": round(apply_gbps / PEAK_GBPS, 4),
             "traffic": traffic_for_current_kernel(),
+            "traffic_GBps": traffic_rate(traffic_for_current_kernel(), apply_avg_ms),
             "avg_launch_ms": round(apply_avg_ms, 5),
             "algorithmic_bytes_per_launch": apply_bytes,
         },
