@@ -40,25 +40,29 @@ def build(verbose: bool = False, extra_flags=(), out: str = LIB) -> str:
     (e.g. -DEMBER_APPLY_ROWS=8 to try another tuning constant)."""
     objs = []
     tag = str(abs(hash((tuple(extra_flags), out))))
-    for src in SOURCES:
-        obj = os.path.join(CSRC, f"{src}.{tag}.o")
-        lang = ["-x", "hip"] if src.endswith(".hip") else []
-        cmd = [HIPCC, f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
-               "-ffp-contract=fast", "-Wall", "-Wno-unused-function",
-               "-I", INCLUDE, "-I", CSRC, *DEVICE_FLAGS, *extra_flags, *lang, "-c",
-               os.path.join(CSRC, src), "-o", obj]
+    try:
+        for src in SOURCES:
+            obj = os.path.join(CSRC, f"{src}.{tag}.o")
+            objs.append(obj)
+            lang = ["-x", "hip"] if src.endswith(".hip") else []
+            cmd = [HIPCC, f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
+                   "-ffp-contract=fast", "-Wall", "-Wno-unused-function",
+                   "-I", INCLUDE, "-I", CSRC, *DEVICE_FLAGS, *extra_flags, *lang, "-c",
+                   os.path.join(CSRC, src), "-o", obj]
+            if verbose:
+                print(" ".join(cmd), flush=True)
+            _run(cmd, verbose)
+        tmp = out + ".tmp"
+        cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
         if verbose:
             print(" ".join(cmd), flush=True)
         _run(cmd, verbose)
-        objs.append(obj)
-    tmp = out + ".tmp"
-    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    _run(cmd, verbose)
-    os.replace(tmp, out)
-    for obj in objs:
-        os.remove(obj)
+        os.replace(tmp, out)
+    finally:
+        # objects are intermediate: none is left behind, also when a step fails
+        for obj in objs:
+            if os.path.exists(obj):
+                os.remove(obj)
     return out
 
 
