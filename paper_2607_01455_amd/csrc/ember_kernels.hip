@@ -527,12 +527,14 @@ __global__ __launch_bounds__(kBlock) void ember_stats(StatsParams a) {
 constexpr int kFinThreads = 1024;                  // 16 waves
 constexpr int kFinWaves = kFinThreads / kWave;
 constexpr int kFinRowsPerBlock = kFinThreads * kVRowsPerThread;
+constexpr int kFinGroups = kFinThreads / kFinCols;  // row groups of a column block
+static_assert(kFinCols == 16 || kFinCols == 32 || kFinCols == 64, "a column block's columns lie in one wave");
 
 struct FinParams {
     const float* P;        // [nb][D] per-block column sums of g^2
     int nb;
     int64_t D;
-    int ncolblocks;        // ceil(D / 64)
+    int ncolblocks;        // ceil(D / kFinCols)
     const float* rowpart;  // [nslab][rows]
     int nslab;
     int64_t rows;
@@ -558,21 +560,33 @@ struct FinParams {
 // sums in a fixed order, and the step scale sqrt(1 / (bias s)) / alpha_s.  The
 // preconditioner's root sqrt(rhat_i chat_j / s) / alpha_s is applied as
 // [sqrt(r_i / bias) * scale] * sqrt(c_j): a row factor times the column factor
-// the column blocks stored, which needs no pass over the columns here.
-__device__ void step_scale(const FinParams& a, int nrsum) {
+// the column blocks stored, which needs no pass over the columns here.  Every
+// thread of the block takes part: thread t adds entries t, t + 1024, ... in
+// float64, then the waves' sums are added in wave order.
+__device__ void step_scale(const FinParams& a, int nrsum, double (*lds2)[kFinWaves]) {
     const int lane = threadIdx.x & (kWave - 1);
-    if (threadIdx.x < kWave) {
-        double sr = 0.0, sc = 0.0;
-        for (int k = lane; k < nrsum; k += kWave) sr += (double)ld_agent(a.rsum + k);
-        for (int k = lane; k < a.ncolblocks; k += kWave) sc += (double)ld_agent(a.csum + k);
-        sr = wave_sum(sr);
-        sc = wave_sum(sc);
-        if (lane == 0) {
-            const double mean_rhat = sr / (double)a.V * a.inv_bias;
-            const double mean_chat = sc / (double)a.D * a.inv_bias;
-            const double s = sqrt(mean_rhat * mean_chat);
-            *a.scale = s > 0.0 ? (float)(sqrt(a.inv_bias / s) * a.inv_alpha) : 0.0f;
+    const int wave = threadIdx.x / kWave;
+    double sr = 0.0, sc = 0.0;
+    for (int k = threadIdx.x; k < nrsum; k += kFinThreads) sr += (double)ld_agent(a.rsum + k);
+    for (int k = threadIdx.x; k < a.ncolblocks; k += kFinThreads) sc += (double)ld_agent(a.csum + k);
+    sr = wave_sum(sr);
+    sc = wave_sum(sc);
+    if (lane == 0) {
+        lds2[0][wave] = sr;
+        lds2[1][wave] = sc;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        sr = 0.0;
+        sc = 0.0;
+        for (int w = 0; w < kFinWaves; ++w) {
+            sr += lds2[0][w];
+            sc += lds2[1][w];
         }
+        const double mean_rhat = sr / (double)a.V * a.inv_bias;
+        const double mean_chat = sc / (double)a.D * a.inv_bias;
+        const double s = sqrt(mean_rhat * mean_chat);
+        *a.scale = s > 0.0 ? (float)(sqrt(a.inv_bias / s) * a.inv_alpha) : 0.0f;
     }
 }
 
@@ -590,12 +604,13 @@ __device__ __forceinline__ float block_sum_1024(float v, float* lds16) {
 }
 
 template <bool kSparse>
-__device__ __forceinline__ void finalize_body(const FinParams& a, int err, float (*part)[kWave], float* lds16);
+__device__ __forceinline__ void finalize_body(const FinParams& a, int err, float (*part)[kFinCols], float* lds16);
 
 template <bool kSparse>
 __global__ __launch_bounds__(kFinThreads) void ember_finalize(FinParams a) {
-    __shared__ float part[kFinWaves][kWave];
+    __shared__ float part[kFinGroups][kFinCols];
     __shared__ float lds16[kFinWaves];
+    __shared__ double lds2[2][kFinWaves];
     __shared__ int last;
     const int err = kSparse ? *a.flag : 0;
     if (blockIdx.x == 0 && threadIdx.x == 0) *a.status = err;
@@ -605,36 +620,39 @@ __global__ __launch_bounds__(kFinThreads) void ember_finalize(FinParams a) {
     // sums (written with agent-scope stores).
     if (!block_ticket(a.ticket, (int)gridDim.x, &last)) return;
     const int nrsum = (int)((a.V + kFinRowsPerBlock - 1) / kFinRowsPerBlock);
-    if (!err) step_scale(a, nrsum);
+    if (!err) step_scale(a, nrsum, lds2);
     if (threadIdx.x == 0) *a.ticket = 0;
 }
 
 template <bool kSparse>
-__device__ __forceinline__ void finalize_body(const FinParams& a, int err, float (*part)[kWave], float* lds16) {
+__device__ __forceinline__ void finalize_body(const FinParams& a, int err, float (*part)[kFinCols], float* lds16) {
     const int lane = threadIdx.x & (kWave - 1);
-    const int wave = threadIdx.x / kWave;
     if ((int)blockIdx.x < a.ncolblocks) {
-        // 64 columns: wave w sums partial rows w, w + 16, ... in ascending order,
-        // then the 16 wave sums are added in wave order.
-        const int64_t j = (int64_t)blockIdx.x * kWave + lane;
+        // kFinCols columns: thread (g, x) sums partial rows g, g + kFinGroups, ...
+        // of column x in ascending order, then the first kFinCols threads add
+        // the kFinGroups group sums in group order.
+        const int x = threadIdx.x % kFinCols;
+        const int g = threadIdx.x / kFinCols;
+        const int64_t j = (int64_t)blockIdx.x * kFinCols + x;
         const bool jv = j < a.D;
         float s = 0.0f;
         if (jv) {
 #pragma unroll 8
-            for (int b = wave; b < a.nb; b += kFinWaves) s += a.P[(int64_t)b * a.D + j];
+            for (int b = g; b < a.nb; b += kFinGroups) s += a.P[(int64_t)b * a.D + j];
         }
-        part[wave][lane] = s;
+        part[g][x] = s;
         __syncthreads();
-        float cn = 0.0f;
-        if (wave == 0) {
-            float colsum = 0.0f;
-#pragma unroll
-            for (int w = 0; w < kFinWaves; ++w) colsum += part[w][lane];
-            if (jv && !err) {
-                const float mean = (float)((double)colsum / (double)a.V);
-                cn = fmaf(a.beta2, a.c[j], a.one_minus_beta2 * mean);
-                st_agent(a.c + j, cn);
-                a.qa[j] = sqrtf(cn);
+        if (threadIdx.x < kWave) {
+            float cn = 0.0f;
+            if (lane < kFinCols) {
+                float colsum = 0.0f;
+                for (int w = 0; w < kFinGroups; ++w) colsum += part[w][lane];
+                if (jv && !err) {
+                    const float mean = (float)((double)colsum / (double)a.V);
+                    cn = fmaf(a.beta2, a.c[j], a.one_minus_beta2 * mean);
+                    st_agent(a.c + j, cn);
+                    a.qa[j] = sqrtf(cn);
+                }
             }
             cn = wave_sum(cn);
             if (lane == 0) st_agent(a.csum + blockIdx.x, cn);
@@ -1321,7 +1339,7 @@ WsLayout ws_layout(int64_t V, int64_t D) {
     L.rsum = off;
     off = align256(off + (size_t)((V + kFinRowsPerBlock - 1) / kFinRowsPerBlock) * 4);
     L.csum = off;
-    off = align256(off + (size_t)((D + kWave - 1) / kWave) * 4);
+    off = align256(off + (size_t)((D + kFinCols - 1) / kFinCols) * 4);
     L.p = off;
     off = align256(off + (size_t)nb * (size_t)D * 4);
     L.total = off;
@@ -1377,7 +1395,7 @@ hipError_t launch_finalize(const StepArgs& a, hipStream_t s) {
     p.P = reinterpret_cast<const float*>(a.ws + L.p);
     p.nb = a.fin_nb > 0 ? a.fin_nb : row_blocks(a.rows, a.sparse);
     p.D = a.D;
-    p.ncolblocks = (int)((a.D + kWave - 1) / kWave);
+    p.ncolblocks = (int)((a.D + kFinCols - 1) / kFinCols);
     p.rowpart = reinterpret_cast<const float*>(a.ws + L.rowpart);
     p.nslab = a.fin_nslab > 0 ? a.fin_nslab : col_plan(a.D, a.g_dtype).nslab;
     p.rows = a.rows;

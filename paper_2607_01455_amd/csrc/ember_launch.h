@@ -66,6 +66,12 @@ constexpr int kWaves = kBlock / kWave;
 #ifndef EMBER_ROWONLY_NT
 #define EMBER_ROWONLY_NT 1       // row-only kernel: non-temporal G/W loads and W stores
 #endif
+#ifndef EMBER_FIN_ROWS
+#define EMBER_FIN_ROWS 1         // finalize: rows of r per thread
+#endif
+#ifndef EMBER_FIN_COLS
+#define EMBER_FIN_COLS 64        // finalize: columns per column block (16, 32 or 64)
+#endif
 #ifndef EMBER_COAL_ITEMS
 #define EMBER_COAL_ITEMS 4       // gradient coalescing: keys per thread per sort tile
 #endif
@@ -97,7 +103,8 @@ constexpr int kApplyRows = EMBER_APPLY_ROWS;
 constexpr int kApplyBatches = EMBER_APPLY_BATCHES;
 constexpr int kMaxBlocks = EMBER_MAX_BLOCKS;
 constexpr int kRowsPerBlockMin = 8; // fewer rows than this per block: fewer blocks
-constexpr int kVRowsPerThread = 4;  // rows per thread in the r pass
+constexpr int kVRowsPerThread = EMBER_FIN_ROWS;  // rows per thread in the r pass of finalize
+constexpr int kFinCols = EMBER_FIN_COLS;         // columns per column block of finalize
 constexpr int kDecayRows = 1024;    // rows per decay block of the row-only sparse step
 constexpr int64_t kMaxGridBlocks = (int64_t)1 << 20;  // launched blocks per kernel at most
 int64_t capped_blocks(int64_t blocks);
@@ -161,7 +168,7 @@ struct WsLayout {
     size_t qa;      // float[D rounded up to 8]: column factors sqrt(c_j)
     size_t rowpart; // float[max(nslab, NT)][V]: per-slab (or per-column-tile) row sums of g^2
     size_t rsum;    // float[ceil(V / 4096)]: per-block sums of the new r
-    size_t csum;    // float[ceil(D / 64)]: per-block sums of the new c
+    size_t csum;    // float[ceil(D / kFinCols)]: per-block sums of the new c
     size_t p;       // float[max(row_blocks(V), MT)][D]: per-block (or per-row-tile) column sums of g^2
     size_t total;
 };
