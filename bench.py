@@ -8,10 +8,16 @@ scales), the input embedding a sparse-row step (8 x 2048 Zipf(1.1) token ids
 per step, ~4650 distinct rows).  All inputs are synthetic, made before the
 timed region and resident in HBM.
 
+By default both tables take their step in one ember_step_multi call (three
+launches shared by the two tables; the same bits as one call per table);
+--schedule sequential times one call per table instead, and the line reports
+both schedules.
+
 Prints one JSON line: whole-step throughput in algorithmic GB/s (the bytes
 the method must move, see paper_2607_01455_amd.workloads.algorithmic_bytes),
-ms per step, per-part times, the roofline of the dominant kernel (the dense
-apply pass, timed with HIP events around each launch), torch's device copy
+ms per step, per-part times, the roofline of the dominant kernel (the apply
+pass of the timed schedule, timed with HIP events around each launch; the
+single-table dense apply pass is reported beside it), torch's device copy
 for reference, the other table shapes, and the CPU oracle timed on a sample.
 """
 import argparse
@@ -29,6 +35,7 @@ PEAK_GBPS = 8000.0
 V, D = 128256, 4096
 KERNEL_SRC = os.path.join(ROOT, "paper_2607_01455_amd", "csrc", "ember_kernels.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ember_apply_lmhead128k_traffic.txt")
+MULTI_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ember_apply_multi_lmhead128k_embed128k_traffic.txt")
 ROWONLY_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ember_rowonly_lmhead128k_traffic.txt")
 LMHEAD_SRC = os.path.join(ROOT, "paper_2607_01455_amd", "csrc", "ember_lmhead.hip")
 LMHEAD_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ember_lmhead_grad_lmhead128k_wgrad_traffic.txt")
@@ -46,6 +53,9 @@ def parse():
     p.add_argument("--no-row-only", action="store_true")
     p.add_argument("--no-coalesce", action="store_true")
     p.add_argument("--no-lmhead-wgrad", action="store_true")
+    p.add_argument("--schedule", choices=("multi", "sequential"), default="multi",
+                   help="multi: both tables in one ember_step_multi call (three launches); "
+                        "sequential: ember_step_dense, then ember_step_sparse_rows")
     return p.parse_args()
 
 
@@ -367,13 +377,20 @@ def main():
     emb = ember.EmberTable(V, D, device=dev)
     torch.cuda.synchronize()
 
-    def step(k):
+    def step_sequential(k):
         head.step(W_head, grads[k % n_grads])
         idx, Gr = batches[k]
         emb.step_sparse_rows(W_emb, Gr, idx)
 
-    for k in range(Wm):
-        step(k)
+    def step_multi(k):
+        idx, Gr = batches[k]
+        ember.step_tables([(head, W_head, grads[k % n_grads]), (emb, W_emb, Gr, idx)])
+
+    schedules = {"multi": step_multi, "sequential": step_sequential}
+    step = schedules[args.schedule]
+    for fn in schedules.values():
+        for k in range(Wm):
+            fn(k)
     torch.cuda.synchronize()
     if ember.ember_get_error(emb.ws) != ember.EMBER_OK:
         raise RuntimeError("sparse step reported an index error")
@@ -381,15 +398,21 @@ def main():
     stream = torch.cuda.current_stream()
 
     # --- timed region A: K whole steps, nothing else on the stream -----------
-    torch.cuda.synchronize()
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    t_start.record(stream)
-    for k in range(K):
-        step(Wm + k)
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    ms_step = t_start.elapsed_time(t_end) / K
+    def whole_steps(fn):
+        torch.cuda.synchronize()
+        t_start = torch.cuda.Event(enable_timing=True)
+        t_end = torch.cuda.Event(enable_timing=True)
+        t_start.record(stream)
+        for k in range(K):
+            fn(Wm + k)
+        t_end.record(stream)
+        torch.cuda.synchronize()
+        return t_start.elapsed_time(t_end) / K
+
+    ms_step = whole_steps(step)
+    # the other schedule on the same inputs, for comparison (not the value)
+    other = "sequential" if args.schedule == "multi" else "multi"
+    schedule_ms = {args.schedule: round(ms_step, 4), other: round(whole_steps(schedules[other]), 4)}
 
     # --- timed region A1: the same steps with a marker between the two tables
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
@@ -429,12 +452,45 @@ def main():
 
     dstats, dense_ms_events = kernel_region(lambda k: head.step(W_head, grads[(Wm + K + k) % n_grads]))
     sstats, sparse_ms_events = kernel_region(lambda k: emb.step_sparse_rows(W_emb, batches[Wm + k][1], batches[Wm + k][0]))
+    mstats, multi_ms_events = kernel_region(lambda k: step_multi(Wm + k))
     if ember.ember_get_error(emb.ws) != ember.EMBER_OK:
         raise RuntimeError("sparse step reported an index error")
     apply_launches, apply_ms = dstats["ember_apply"]
     apply_avg_ms = apply_ms / apply_launches
+    # apply pass: G read, W read and written, r and the column factors read
     apply_bytes = V * D * (2 + 2 * 2) + 4 * (V + D)
     apply_gbps = apply_bytes / (apply_avg_ms * 1e-3) / 1e9
+    # the multi-table apply launch: the dense pass above plus the sparse rows
+    # (G rows, W rows read and written, their r entries and int64 ids, column factors)
+    sparse_apply_bytes = sum(n * D * (2 + 2 * 2) + 12 * n + 4 * D for n in n_rows) / K
+    mapply_launches, mapply_ms = mstats["ember_apply_multi"]
+    mapply_avg_ms = mapply_ms / mapply_launches
+    mapply_bytes = apply_bytes + sparse_apply_bytes
+    mapply_gbps = mapply_bytes / (mapply_avg_ms * 1e-3) / 1e9
+    dense_roofline = {
+        "kernel": "ember_apply (dense LM-head step)",
+        "bound": "hbm",
+        "achieved": round(apply_gbps, 1),
+        "peak": PEAK_GBPS,
+        "unit": "GB/s",
+        "frac": round(apply_gbps / PEAK_GBPS, 4),
+        "traffic": traffic_for_current_kernel(),
+        "traffic_GBps": traffic_rate(traffic_for_current_kernel(), apply_avg_ms),
+        "avg_launch_ms": round(apply_avg_ms, 5),
+        "algorithmic_bytes_per_launch": apply_bytes,
+    }
+    multi_roofline = {
+        "kernel": "ember_apply_multi (LM head dense + embedding sparse rows, one launch)",
+        "bound": "hbm",
+        "achieved": round(mapply_gbps, 1),
+        "peak": PEAK_GBPS,
+        "unit": "GB/s",
+        "frac": round(mapply_gbps / PEAK_GBPS, 4),
+        "traffic": traffic_for_current_kernel(MULTI_TRAFFIC_FILE),
+        "traffic_GBps": traffic_rate(traffic_for_current_kernel(MULTI_TRAFFIC_FILE), mapply_avg_ms),
+        "avg_launch_ms": round(mapply_avg_ms, 5),
+        "algorithmic_bytes_per_launch": int(mapply_bytes),
+    }
 
     # --- plain device copy over a W-sized buffer: practical ceiling ----------
     src = torch.empty(V * D, dtype=torch.bfloat16, device=dev).fill_(1.0)
@@ -471,8 +527,11 @@ def main():
             "V": V, "D": D, "storage": "bf16 W and G, fp32 r and c",
             "sparse_rows_per_step": round(sum(n_rows) / K, 1),
             "algorithmic_bytes_per_step": int(step_bytes),
-            "schedule": "dense step then sparse step, one stream",
+            "schedule": ("both tables in one ember_step_multi call: statistics, finalize and apply "
+                         "launches shared by the two tables, one stream" if args.schedule == "multi"
+                         else "dense step then sparse step, one stream"),
         },
+        "schedules_ms_per_step": schedule_ms,
         "pct_of_peak": round(100.0 * value / PEAK_GBPS, 2),
         "parts": {
             "dense_lmhead": {"ms": round(dense_ms, 4), "bytes": dense_bytes,
@@ -484,20 +543,12 @@ def main():
         "kernels_ms_avg": {
             "dense": {k: round(v[1] / v[0], 5) for k, v in dstats.items()},
             "sparse": {k: round(v[1] / v[0], 5) for k, v in sstats.items()},
+            "multi": {k: round(v[1] / v[0], 5) for k, v in mstats.items()},
         },
-        "ms_with_kernel_events": {"dense": round(dense_ms_events, 4), "sparse": round(sparse_ms_events, 4)},
-        "roofline": {
-            "kernel": "ember_apply (dense LM-head step)",
-            "bound": "hbm",
-            "achieved": round(apply_gbps, 1),
-            "peak": PEAK_GBPS,
-            "unit": "GB/s",
-            "frac": round(apply_gbps / PEAK_GBPS, 4),
-            "traffic": traffic_for_current_kernel(),
-            "traffic_GBps": traffic_rate(traffic_for_current_kernel(), apply_avg_ms),
-            "avg_launch_ms": round(apply_avg_ms, 5),
-            "algorithmic_bytes_per_launch": apply_bytes,
-        },
+        "ms_with_kernel_events": {"dense": round(dense_ms_events, 4), "sparse": round(sparse_ms_events, 4),
+                                  "multi": round(multi_ms_events, 4)},
+        "roofline": multi_roofline if args.schedule == "multi" else dense_roofline,
+        "roofline_dense_apply": dense_roofline,
         "torch_device_copy_GBps": round(copy_gbps, 1),
         "row_only": None,
         "coalesce": None,

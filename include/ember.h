@@ -159,6 +159,64 @@ int ember_step_sparse_rows_devn(void* W, int w_dtype, int64_t ldw,
                                 void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * Several canonical Ember steps in one call: the tables of a model (for
+ * example the LM head, dense, and the input embedding, sparse rows) each take
+ * the step Algorithm 1 defines for them, exactly as the single-table entry
+ * points above would, but the library enqueues three launches in all (one
+ * statistics pass, one finalize pass, one apply pass over every table)
+ * instead of three per table, so the tables share the chip and a small table
+ * costs its bytes instead of its launch latency.  Each table's results are
+ * the same bits as its own ember_step_dense or ember_step_sparse_rows call.
+ *
+ * One ember_table_step per table:
+ *   W, w_dtype, ldw, G, g_dtype, ldg, r, c, V, D, t, lr, beta2, eps,
+ *   maximize, ws, ws_bytes   as for ember_step_dense;
+ *   sparse = 0               dense step: G is V x D; idx, n_idx, n_idx_dev unused;
+ *   sparse = 1               sparse-row step: G holds n_idx compact rows of the
+ *                            rows idx lists, as for ember_step_sparse_rows;
+ *                            with n_idx_dev non-NULL the row count is read from
+ *                            that device int64 when the step runs and n_idx is
+ *                            its maximum, as for ember_step_sparse_rows_devn.
+ * Tables may differ in every field (shape, dtypes, scalars, t).  Tables with
+ * the same dtypes and the same columns-per-lane plan share launches; others
+ * add launches of their own.
+ *
+ * Errors: each table is checked as its own call would be, and additionally
+ * the tables' workspaces, state vectors and weight matrices must not overlap
+ * one another (EMBER_ERR_ARG); 1 <= n_tables <= EMBER_MAX_TABLES
+ * (EMBER_ERR_ARG).  A failed check enqueues nothing for any table.  Index
+ * errors of a sparse table leave that table untouched (the others step
+ * normally) and are reported by ember_get_error on its workspace.
+ */
+#define EMBER_MAX_TABLES 8
+
+typedef struct {
+    void* W;
+    int w_dtype;
+    int64_t ldw;
+    const void* G;
+    int g_dtype;
+    int64_t ldg;
+    int sparse;
+    const int64_t* idx;
+    int64_t n_idx;
+    const int64_t* n_idx_dev;
+    float* r;
+    float* c;
+    int64_t V;
+    int64_t D;
+    int64_t t;
+    float lr;
+    float beta2;
+    float eps;
+    int maximize;
+    void* ws;
+    size_t ws_bytes;
+} ember_table_step;
+
+int ember_step_multi(const ember_table_step* tables, int n_tables, hipStream_t stream);
+
+/*
  * Row-only Ember (Section 2.1, the variant the paper analyses most, listed in
  * its ablation table with V floats of state): only the row statistic r is
  * kept, and each row's gradient is divided by the square root of its own

@@ -156,6 +156,68 @@ int check_rowonly_state(const float* r, const void* ws, size_t ws_bytes, int64_t
     return EMBER_OK;
 }
 
+// Byte range [lo, hi) of device memory an argument covers.
+struct Span {
+    uintptr_t lo, hi;
+};
+bool overlap(Span a, Span b) { return a.lo < b.hi && b.lo < a.hi; }
+Span span_of(const void* p, size_t bytes) {
+    const uintptr_t lo = reinterpret_cast<uintptr_t>(p);
+    return Span{lo, lo + bytes};
+}
+
+// Checks one table of ember_step_multi as its own call would check it.
+int check_table(const ember_table_step& x) {
+    int st = check_shape(x.V, x.D);
+    if (st != EMBER_OK) return st;
+    if (x.sparse != 0 && x.sparse != 1) return EMBER_ERR_ARG;
+    if (!x.sparse) {
+        st = check_matrix(x.W, x.w_dtype, x.ldw, x.D, false);
+        if (st == EMBER_OK) st = check_matrix(x.G, x.g_dtype, x.ldg, x.D, false);
+    } else if (x.n_idx_dev != nullptr) {
+        st = check_devn(x.W, x.w_dtype, x.ldw, x.G, x.g_dtype, x.ldg, x.idx, x.n_idx_dev, x.n_idx, x.V, x.D);
+    } else {
+        if (x.n_idx < 0 || x.n_idx > x.V) st = EMBER_ERR_SHAPE;
+        if (st == EMBER_OK) st = check_matrix(x.W, x.w_dtype, x.ldw, x.D, false);
+        if (st == EMBER_OK) st = check_matrix(x.G, x.g_dtype, x.ldg, x.D, x.n_idx == 0);
+        if (st == EMBER_OK && x.n_idx > 0 && x.idx == nullptr) st = EMBER_ERR_ARG;
+        if (st == EMBER_OK && x.idx != nullptr && !aligned(x.idx, 8)) st = EMBER_ERR_ALIGN;
+    }
+    if (st == EMBER_OK) st = check_state(x.r, x.c, x.ws, x.ws_bytes, x.V, x.D);
+    if (st == EMBER_OK) st = check_scalars(x.t, x.lr, x.beta2, x.eps);
+    return st;
+}
+
+// The memory one table writes: workspace, r, c and W.
+void table_spans(const ember_table_step& x, Span out[4]) {
+    out[0] = span_of(x.ws, ember::ws_layout(x.V, x.D).total);
+    out[1] = span_of(x.r, (size_t)x.V * 4);
+    out[2] = span_of(x.c, (size_t)x.D * 4);
+    const size_t es = dtype_size(x.w_dtype);
+    out[3] = span_of(x.W, ((size_t)(x.V - 1) * (size_t)x.ldw + (size_t)x.D) * es);
+}
+
+// Launches of one phase: tables in `order`, grouped by kernel key in order of
+// first appearance, one launcher call per group.
+template <typename Key, typename Launch>
+hipError_t run_phase(const std::vector<const StepArgs*>& order, Key key, Launch launch, hipStream_t s) {
+    std::vector<int> keys;
+    for (const StepArgs* a : order) {
+        const int k = key(*a);
+        bool seen = false;
+        for (int q : keys) seen = seen || q == k;
+        if (!seen) keys.push_back(k);
+    }
+    for (int k : keys) {
+        std::vector<const StepArgs*> group;
+        for (const StepArgs* a : order)
+            if (key(*a) == k) group.push_back(a);
+        const hipError_t e = launch(group.data(), (int)group.size(), s);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
 } // namespace
 
 extern "C" {
@@ -286,6 +348,79 @@ int ember_step_sparse_rows(void* W, int w_dtype, int64_t ldw, const void* G_rows
     a.D = D;
     a.ws = static_cast<char*>(ws);
     return run_step(a, lr, beta2, eps, t, maximize, stream);
+}
+
+int ember_step_multi(const ember_table_step* tables, int n_tables, hipStream_t stream) {
+    if (tables == nullptr || n_tables < 1 || n_tables > EMBER_MAX_TABLES) return EMBER_ERR_ARG;
+    for (int i = 0; i < n_tables; ++i) {
+        const int st = check_table(tables[i]);
+        if (st != EMBER_OK) return st;
+    }
+    for (int i = 0; i < n_tables; ++i) {
+        Span si[4];
+        table_spans(tables[i], si);
+        for (int j = i + 1; j < n_tables; ++j) {
+            Span sj[4];
+            table_spans(tables[j], sj);
+            for (int x = 0; x < 4; ++x)
+                for (int y = 0; y < 4; ++y)
+                    if (overlap(si[x], sj[y])) return EMBER_ERR_ARG;
+        }
+    }
+    std::vector<StepArgs> args((size_t)n_tables);
+    for (int i = 0; i < n_tables; ++i) {
+        const ember_table_step& x = tables[i];
+        StepArgs& a = args[(size_t)i];
+        a = StepArgs{};
+        a.sparse = x.sparse != 0;
+        a.W = x.W;
+        a.w_dtype = x.w_dtype;
+        a.ldw = x.ldw;
+        a.G = x.G;
+        a.g_dtype = x.g_dtype;
+        a.ldg = x.ldg;
+        a.idx = a.sparse ? x.idx : nullptr;
+        a.n_dev = a.sparse ? x.n_idx_dev : nullptr;
+        a.rows = a.sparse ? x.n_idx : x.V;
+        a.r = x.r;
+        a.c = x.c;
+        a.V = x.V;
+        a.D = x.D;
+        a.ws = static_cast<char*>(x.ws);
+        set_scalars(a, x.lr, x.beta2, x.eps, x.t, x.maximize);
+    }
+    // Block order inside a launch: the statistics pass runs the sparse tables
+    // first, so that the dense tables' last rows, which the apply pass (rows
+    // high to low) reads first, are the ones left in the last-level cache; the
+    // apply pass runs the dense tables first.  A dense table with lr = 0 keeps
+    // every weight and has no apply blocks (a sparse one still clears its
+    // index-error flag there).
+    bool any_dense = false;
+    for (const StepArgs& a : args) any_dense = any_dense || !a.sparse;
+    for (StepArgs& a : args) a.stats_stream = EMBER_MULTI_SPARSE_STREAM && a.sparse && any_dense;
+    std::vector<const StepArgs*> sparse_first, dense_first;
+    for (const StepArgs& a : args)
+        if (a.sparse != (bool)EMBER_MULTI_DENSE_STATS_FIRST) sparse_first.push_back(&a);
+    for (const StepArgs& a : args)
+        if (a.sparse == (bool)EMBER_MULTI_DENSE_STATS_FIRST) sparse_first.push_back(&a);
+    for (const StepArgs& a : args)
+        if (EMBER_MULTI_SPARSE_APPLY_FIRST && a.sparse) dense_first.push_back(&a);
+    for (const StepArgs& a : args)
+        if (!a.sparse && a.inv_alpha != 0.0) dense_first.push_back(&a);
+    for (const StepArgs& a : args)
+        if (!EMBER_MULTI_SPARSE_APPLY_FIRST && a.sparse) dense_first.push_back(&a);
+    hipError_t e = timed("ember_stats_multi", stream, [&] {
+        return run_phase(sparse_first, ember::stats_key, ember::launch_stats_multi, stream);
+    });
+    if (e == hipSuccess)
+        e = timed("ember_finalize_multi", stream, [&] {
+            return run_phase(sparse_first, [](const StepArgs&) { return 0; }, ember::launch_finalize_multi, stream);
+        });
+    if (e == hipSuccess && !dense_first.empty())
+        e = timed("ember_apply_multi", stream, [&] {
+            return run_phase(dense_first, ember::apply_key, ember::launch_apply_multi, stream);
+        });
+    return e == hipSuccess ? EMBER_OK : EMBER_ERR_HIP;
 }
 
 int ember_rowonly_init_state(float* r, int64_t V, int64_t D, void* ws, size_t ws_bytes, hipStream_t stream) {

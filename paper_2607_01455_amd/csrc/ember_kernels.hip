@@ -393,16 +393,25 @@ __device__ __forceinline__ RowSet stats_rows(int64_t rows, int nb, int b) {
 // the row count.
 constexpr int64_t kWideRowsPerWave = 1024;
 
-template <typename GT, int M, int R, bool kSparse, bool kWide>
-__global__ __launch_bounds__(kBlock) void ember_stats(StatsParams a) {
+// More than kWideRowsPerWave rows per wavefront: the kWide instance.
+static bool stats_wide(const StatsParams& p) {
+    return (p.rows + (int64_t)p.nb * kWaves - 1) / ((int64_t)p.nb * kWaves) > kWideRowsPerWave;
+}
+
+// Block `blk` of the statistics pass of one table; `lds` is the block's
+// [kWaves][kWave * EPC] staging area for the column-sum combine.
+template <typename GT, int M, int R, bool kSparseArg, bool kWide, bool kRuntime = false>
+__device__ __forceinline__ void stats_block(const StatsParams& a, unsigned blk, float (*lds)[kWave * 16 / sizeof(GT)],
+                                           bool sparse_rt = false) {
+    const bool kSparse = kRuntime ? sparse_rt : kSparseArg;
     constexpr int EPC = 16 / (int)sizeof(GT);
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
-    const int slab = (int)(blockIdx.x % (unsigned)a.nslab);
-    const int b = (int)(blockIdx.x / (unsigned)a.nslab);
+    const int slab = (int)(blk % (unsigned)a.nslab);
+    const int b = (int)(blk / (unsigned)a.nslab);
     bool bad_count = false;
     const int64_t nrows = kSparse ? active_rows(a.n_dev, a.rows, bad_count) : a.rows;
-    if (kSparse && bad_count && blockIdx.x == 0 && threadIdx.x == 0) atomicOr(a.flag, kFlagCount);
+    if (kSparse && bad_count && blk == 0 && threadIdx.x == 0) atomicOr(a.flag, kFlagCount);
     const RowSet rset = stats_rows(nrows, a.nb, b);
     const int cbeg = slab * a.slab_chunks;
     const int cend = min(cbeg + a.slab_chunks, a.total_chunks);
@@ -503,7 +512,6 @@ __global__ __launch_bounds__(kBlock) void ember_stats(StatsParams a) {
     }
 
     // Combine the 4 waves' column sums in a fixed order, one chunk column at a time.
-    __shared__ float lds[kWaves][kWave * EPC];
     float* P = a.P + (int64_t)b * a.D;
 #pragma unroll
     for (int m = 0; m < M; ++m) {
@@ -518,6 +526,43 @@ __global__ __launch_bounds__(kBlock) void ember_stats(StatsParams a) {
         }
         __syncthreads();
     }
+}
+
+template <typename GT, int M, int R, bool kSparse, bool kWide>
+__global__ __launch_bounds__(kBlock) void ember_stats(StatsParams a) {
+    __shared__ float lds[kWaves][kWave * 16 / sizeof(GT)];
+    stats_block<GT, M, R, kSparse, kWide>(a, blockIdx.x, lds);
+}
+
+// Several tables in one launch: table k owns blocks [first[k], first[k+1]).
+// Each table's blocks do exactly what its own launch would, so the results
+// are the same bits; one launch lets the tables share the chip instead of
+// each paying its own ramp and tail.
+template <typename P>
+struct MultiParams {
+    int ntab;
+    unsigned first[kMaxTables + 1];
+    int sparse[kMaxTables];
+    P p[kMaxTables];
+};
+
+__device__ __forceinline__ int multi_table(const unsigned* first, int ntab) {
+    int k = 0;
+#pragma unroll
+    for (int j = 1; j < kMaxTables; ++j) k += (j < ntab && blockIdx.x >= first[j]) ? 1 : 0;
+    return k;
+}
+
+// At least the occupancy of the single-table kernel (three waves per SIMD for
+// two chunks per lane).  The table's parameters are copied out of the
+// argument array first (uniform values, loaded once).
+template <typename GT, int M, int R, bool kWide>
+__global__ __launch_bounds__(kBlock, (M == 2 && !kWide) ? 3 : 1) void ember_stats_multi(MultiParams<StatsParams> g) {
+    __shared__ float lds[kWaves][kWave * 16 / sizeof(GT)];
+    const int k = multi_table(g.first, g.ntab);
+    const unsigned blk = blockIdx.x - g.first[k];
+    const StatsParams p = g.p[k];
+    stats_block<GT, M, R, false, kWide, true>(p, blk, lds, g.sparse[k] != 0);
 }
 
 // ---------------------------------------------------------------------------
@@ -604,36 +649,58 @@ __device__ __forceinline__ float block_sum_1024(float v, float* lds16) {
 }
 
 template <bool kSparse>
-__device__ __forceinline__ void finalize_body(const FinParams& a, int err, float (*part)[kFinCols], float* lds16);
+__device__ __forceinline__ void finalize_body(const FinParams& a, int blk, int err, float (*part)[kFinCols],
+                                              float* lds16);
 
+// Shared memory of a finalize block.
+struct FinLds {
+    float part[kFinGroups][kFinCols];
+    float lds16[kFinWaves];
+    double lds2[2][kFinWaves];
+    int last;
+};
+
+// Block `blk` of the `nblocks` finalize blocks of one table.
 template <bool kSparse>
-__global__ __launch_bounds__(kFinThreads) void ember_finalize(FinParams a) {
-    __shared__ float part[kFinGroups][kFinCols];
-    __shared__ float lds16[kFinWaves];
-    __shared__ double lds2[2][kFinWaves];
-    __shared__ int last;
+__device__ __forceinline__ void finalize_block(const FinParams& a, int blk, int nblocks, FinLds& sh) {
     const int err = kSparse ? *a.flag : 0;
-    if (blockIdx.x == 0 && threadIdx.x == 0) *a.status = err;
-    finalize_body<kSparse>(a, err, part, lds16);
+    if (blk == 0 && threadIdx.x == 0) *a.status = err;
+    finalize_body<kSparse>(a, blk, err, sh.part, sh.lds16);
 
     // The block that finishes last derives the step scale from the per-block
     // sums (written with agent-scope stores).
-    if (!block_ticket(a.ticket, (int)gridDim.x, &last)) return;
+    if (!block_ticket(a.ticket, nblocks, &sh.last)) return;
     const int nrsum = (int)((a.V + kFinRowsPerBlock - 1) / kFinRowsPerBlock);
-    if (!err) step_scale(a, nrsum, lds2);
+    if (!err) step_scale(a, nrsum, sh.lds2);
     if (threadIdx.x == 0) *a.ticket = 0;
 }
 
 template <bool kSparse>
-__device__ __forceinline__ void finalize_body(const FinParams& a, int err, float (*part)[kFinCols], float* lds16) {
+__global__ __launch_bounds__(kFinThreads) void ember_finalize(FinParams a) {
+    __shared__ FinLds sh;
+    finalize_block<kSparse>(a, (int)blockIdx.x, (int)gridDim.x, sh);
+}
+
+__global__ __launch_bounds__(kFinThreads) void ember_finalize_multi(MultiParams<FinParams> g) {
+    __shared__ FinLds sh;
+    const int k = multi_table(g.first, g.ntab);
+    const int blk = (int)(blockIdx.x - g.first[k]);
+    const int nblocks = (int)(g.first[k + 1] - g.first[k]);
+    if (g.sparse[k]) finalize_block<true>(g.p[k], blk, nblocks, sh);
+    else finalize_block<false>(g.p[k], blk, nblocks, sh);
+}
+
+template <bool kSparse>
+__device__ __forceinline__ void finalize_body(const FinParams& a, int blk, int err, float (*part)[kFinCols],
+                                              float* lds16) {
     const int lane = threadIdx.x & (kWave - 1);
-    if ((int)blockIdx.x < a.ncolblocks) {
+    if (blk < a.ncolblocks) {
         // kFinCols columns: thread (g, x) sums partial rows g, g + kFinGroups, ...
         // of column x in ascending order, then the first kFinCols threads add
         // the kFinGroups group sums in group order.
         const int x = threadIdx.x % kFinCols;
         const int g = threadIdx.x / kFinCols;
-        const int64_t j = (int64_t)blockIdx.x * kFinCols + x;
+        const int64_t j = (int64_t)blk * kFinCols + x;
         const bool jv = j < a.D;
         float s = 0.0f;
         if (jv) {
@@ -655,12 +722,12 @@ __device__ __forceinline__ void finalize_body(const FinParams& a, int err, float
                 }
             }
             cn = wave_sum(cn);
-            if (lane == 0) st_agent(a.csum + blockIdx.x, cn);
+            if (lane == 0) st_agent(a.csum + blk, cn);
         }
         return;
     }
 
-    const int vb = blockIdx.x - a.ncolblocks;
+    const int vb = blk - a.ncolblocks;
     const double invD = 1.0 / (double)a.D;
     float psum = 0.0f;
 #pragma unroll
@@ -719,13 +786,15 @@ struct ApplyParams {
     int* flag;            // sparse only: cleared for the next step
 };
 
-template <typename GT, typename WT, int M, int R, bool kSparse>
-__global__ __launch_bounds__(kBlock) void ember_apply(ApplyParams a) {
+// Block `blk` of the `nblk` apply blocks of one table.
+template <typename GT, typename WT, int M, int R, bool kSparseArg, bool kRuntime = false>
+__device__ __forceinline__ void apply_block(const ApplyParams& a, unsigned blk, unsigned nblk, bool sparse_rt = false) {
+    const bool kSparse = kRuntime ? sparse_rt : kSparseArg;
     constexpr int EPC = 16 / (int)sizeof(GT);
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     if (kSparse) {
-        if (blockIdx.x == 0 && threadIdx.x == 0) *a.flag = 0;
+        if (blk == 0 && threadIdx.x == 0) *a.flag = 0;
         if (*a.status != 0) return;
     }
     if (a.inv_alpha == 0.0) return;   // lr == 0: every weight keeps its bits
@@ -735,7 +804,7 @@ __global__ __launch_bounds__(kBlock) void ember_apply(ApplyParams a) {
     // (row block, slab) pairs, slab-fastest; the grid is capped, so a block may
     // take several pairs
     const int64_t nvb = (int64_t)a.nb * a.nslab;
-    for (int64_t vb = blockIdx.x; vb < nvb; vb += gridDim.x) {
+    for (int64_t vb = blk; vb < nvb; vb += nblk) {
         const int slab = (int)(vb % a.nslab);
         // Row blocks in reverse order: the rows the statistics pass read last are
         // the likeliest still to sit in the last-level cache.
@@ -802,6 +871,20 @@ __global__ __launch_bounds__(kBlock) void ember_apply(ApplyParams a) {
             }
         }
     }
+}
+
+template <typename GT, typename WT, int M, int R, bool kSparse>
+__global__ __launch_bounds__(kBlock) void ember_apply(ApplyParams a) {
+    apply_block<GT, WT, M, R, kSparse>(a, blockIdx.x, gridDim.x);
+}
+
+template <typename GT, typename WT, int M, int R>
+__global__ __launch_bounds__(kBlock) void ember_apply_multi(MultiParams<ApplyParams> g) {
+    const int k = multi_table(g.first, g.ntab);
+    const unsigned blk = blockIdx.x - g.first[k];
+    const unsigned nblk = g.first[k + 1] - g.first[k];
+    const ApplyParams p = g.p[k];
+    apply_block<GT, WT, M, R, false, true>(p, blk, nblk, g.sparse[k] != 0);
 }
 
 // ---------------------------------------------------------------------------
@@ -1221,7 +1304,7 @@ __global__ __launch_bounds__(kBlock) void ember_zero(uint32_t* p, int64_t words)
 
 template <typename GT, bool kSparse>
 hipError_t stats_dispatch(const StatsParams& p, int m, dim3 grid, hipStream_t s) {
-    const bool wide = (p.rows + (int64_t)p.nb * kWaves - 1) / ((int64_t)p.nb * kWaves) > kWideRowsPerWave;
+    const bool wide = stats_wide(p);
     if (m == 1 && !wide) ember_stats<GT, 1, kStatsRows, kSparse, false><<<grid, kBlock, 0, s>>>(p);
     else if (m == 2 && !wide) ember_stats<GT, 2, kStatsRows, kSparse, false><<<grid, kBlock, 0, s>>>(p);
     else if (m == 1) ember_stats<GT, 1, kStatsRows, kSparse, true><<<grid, kBlock, 0, s>>>(p);
@@ -1355,7 +1438,7 @@ hipError_t launch_zero(void* p, size_t bytes, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_stats(const StepArgs& a, hipStream_t s) {
+static StatsParams stats_params(const StepArgs& a) {
     const WsLayout L = ws_layout(a.V, a.D);
     const ColPlan cp = col_plan(a.D, a.g_dtype);
     StatsParams p;
@@ -1371,7 +1454,7 @@ hipError_t launch_stats(const StepArgs& a, hipStream_t s) {
         const double row_bytes = (double)a.D * (a.g_dtype == 0 ? 4 : 2);
         const int64_t keep = (int64_t)((double)EMBER_STATS_KEEP_MB * 1048576.0 / row_bytes);
         p.cached_from = EMBER_STATS_NT == 0 ? 0
-                      : EMBER_STATS_NT == 1 ? a.rows
+                      : (EMBER_STATS_NT == 1 || a.stats_stream) ? a.rows
                       : (keep >= a.rows ? 0 : a.rows - keep);
     }
     p.rowpart = reinterpret_cast<float*>(a.ws + L.rowpart);
@@ -1381,6 +1464,12 @@ hipError_t launch_stats(const StepArgs& a, hipStream_t s) {
     p.V = a.V;
     p.slot = reinterpret_cast<int*>(a.ws + L.slot);
     p.flag = reinterpret_cast<int*>(a.ws + L.flag);
+    return p;
+}
+
+hipError_t launch_stats(const StepArgs& a, hipStream_t s) {
+    const StatsParams p = stats_params(a);
+    const ColPlan cp = col_plan(a.D, a.g_dtype);
     // at most 384 row blocks x D / 512 slabs: far below the 2^32-thread limit
     const dim3 grid((unsigned)((int64_t)p.nb * cp.nslab));
     const bool sparse = a.sparse;
@@ -1389,7 +1478,7 @@ hipError_t launch_stats(const StepArgs& a, hipStream_t s) {
     return sparse ? stats_dispatch<uint16_t, true>(p, cp.m, grid, s) : stats_dispatch<uint16_t, false>(p, cp.m, grid, s);
 }
 
-hipError_t launch_finalize(const StepArgs& a, hipStream_t s) {
+static FinParams finalize_params(const StepArgs& a) {
     const WsLayout L = ws_layout(a.V, a.D);
     FinParams p;
     p.P = reinterpret_cast<const float*>(a.ws + L.p);
@@ -1415,8 +1504,16 @@ hipError_t launch_finalize(const StepArgs& a, hipStream_t s) {
     p.scale = reinterpret_cast<float*>(a.ws + L.scale);
     p.inv_bias = a.inv_bias;
     p.inv_alpha = a.inv_alpha;
-    const int nvb = (int)((a.V + kFinRowsPerBlock - 1) / kFinRowsPerBlock);
-    const dim3 grid((unsigned)(p.ncolblocks + nvb));
+    return p;
+}
+
+static int64_t finalize_blocks(const StepArgs& a) {
+    return (a.D + kFinCols - 1) / kFinCols + (a.V + kFinRowsPerBlock - 1) / kFinRowsPerBlock;
+}
+
+hipError_t launch_finalize(const StepArgs& a, hipStream_t s) {
+    const FinParams p = finalize_params(a);
+    const dim3 grid((unsigned)finalize_blocks(a));
     if (a.sparse)
         ember_finalize<true><<<grid, kFinThreads, 0, s>>>(p);
     else
@@ -1424,7 +1521,7 @@ hipError_t launch_finalize(const StepArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_apply(const StepArgs& a, hipStream_t s) {
+static ApplyParams apply_params(const StepArgs& a) {
     const WsLayout L = ws_layout(a.V, a.D);
     const ColPlan cp = col_plan(a.D, a.g_dtype);
     ApplyParams p;
@@ -1448,6 +1545,12 @@ hipError_t launch_apply(const StepArgs& a, hipStream_t s) {
     p.eps_over_alpha = a.eps_over_alpha;
     p.status = reinterpret_cast<const int*>(a.ws + L.status);
     p.flag = reinterpret_cast<int*>(a.ws + L.flag);
+    return p;
+}
+
+hipError_t launch_apply(const StepArgs& a, hipStream_t s) {
+    const ApplyParams p = apply_params(a);
+    const ColPlan cp = col_plan(a.D, a.g_dtype);
     const dim3 grid((unsigned)capped_blocks((int64_t)p.nb * cp.nslab));
     const bool sparse = a.sparse;
     if (a.g_dtype == 0)
@@ -1510,6 +1613,115 @@ hipError_t launch_rowonly(const StepArgs& a, hipStream_t s) {
     if (a.sparse)
         return rowonly_dispatch_t<true>(p, a.g_dtype, a.w_dtype, cp.m, spw, resident, grid, waves * kWave, s);
     return rowonly_dispatch_t<false>(p, a.g_dtype, a.w_dtype, cp.m, spw, resident, grid, waves * kWave, s);
+}
+
+// ---------------------------------------------------------------------------
+// several tables per launch
+// ---------------------------------------------------------------------------
+
+// Threads of one multi-table launch at most (the dispatch packet counts work
+// items in 32 bits); the tables past it go to the next launch.
+constexpr int64_t kMultiMaxThreads = (int64_t)1 << 31;
+
+namespace {
+
+template <typename GT>
+hipError_t stats_multi_dispatch(const MultiParams<StatsParams>& g, int m, bool wide, dim3 grid, hipStream_t s) {
+    if (m == 1 && !wide) ember_stats_multi<GT, 1, kStatsRows, false><<<grid, kBlock, 0, s>>>(g);
+    else if (m == 2 && !wide) ember_stats_multi<GT, 2, kStatsRows, false><<<grid, kBlock, 0, s>>>(g);
+    else if (m == 1) ember_stats_multi<GT, 1, kStatsRows, true><<<grid, kBlock, 0, s>>>(g);
+    else if (m == 2) ember_stats_multi<GT, 2, kStatsRows, true><<<grid, kBlock, 0, s>>>(g);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+template <typename GT, typename WT>
+hipError_t apply_multi_dispatch(const MultiParams<ApplyParams>& g, int m, dim3 grid, hipStream_t s) {
+    if (m == 1) ember_apply_multi<GT, WT, 1, kApplyRows><<<grid, kBlock, 0, s>>>(g);
+    else if (m == 2) ember_apply_multi<GT, WT, 2, kApplyRows><<<grid, kBlock, 0, s>>>(g);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+// Packs tables t[0..n) in order into as few launches as the table and thread
+// limits allow; build(a) gives a table's parameters, blocks(a) its block count.
+template <typename P, typename Build, typename Blocks, typename Launch>
+hipError_t launch_groups(const StepArgs* const* t, int n, int threads, Build build, Blocks blocks, Launch launch) {
+    int k = 0;
+    while (k < n) {
+        MultiParams<P> g{};
+        int64_t total = 0;
+        while (k < n && g.ntab < kMaxTables) {
+            const int64_t nb = blocks(*t[k]);
+            if (g.ntab > 0 && (total + nb) * threads > kMultiMaxThreads) break;
+            g.first[g.ntab] = (unsigned)total;
+            g.sparse[g.ntab] = t[k]->sparse ? 1 : 0;
+            g.p[g.ntab] = build(*t[k]);
+            total += nb;
+            ++g.ntab;
+            ++k;
+        }
+        for (int j = g.ntab; j <= kMaxTables; ++j) g.first[j] = (unsigned)total;
+        const hipError_t e = launch(g, dim3((unsigned)total));
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+} // namespace
+
+int stats_key(const StepArgs& a) {
+    return a.g_dtype * 4 + (col_plan(a.D, a.g_dtype).m - 1) * 2 + (stats_wide(stats_params(a)) ? 1 : 0);
+}
+
+int apply_key(const StepArgs& a) {
+    return a.g_dtype * 4 + a.w_dtype * 2 + (col_plan(a.D, a.g_dtype).m - 1);
+}
+
+hipError_t launch_stats_multi(const StepArgs* const* t, int n, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    const StepArgs& a0 = *t[0];
+    const int m = col_plan(a0.D, a0.g_dtype).m;
+    const bool wide = stats_wide(stats_params(a0));
+    return launch_groups<StatsParams>(
+        t, n, kBlock, stats_params,
+        [](const StepArgs& a) {
+            const StatsParams p = stats_params(a);
+            return (int64_t)p.nb * p.nslab;
+        },
+        [&](const MultiParams<StatsParams>& g, dim3 grid) {
+            return a0.g_dtype == 0 ? stats_multi_dispatch<float>(g, m, wide, grid, s)
+                                   : stats_multi_dispatch<uint16_t>(g, m, wide, grid, s);
+        });
+}
+
+hipError_t launch_finalize_multi(const StepArgs* const* t, int n, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    return launch_groups<FinParams>(
+        t, n, kFinThreads, finalize_params, finalize_blocks,
+        [&](const MultiParams<FinParams>& g, dim3 grid) {
+            ember_finalize_multi<<<grid, kFinThreads, 0, s>>>(g);
+            return hipGetLastError();
+        });
+}
+
+hipError_t launch_apply_multi(const StepArgs* const* t, int n, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    const StepArgs& a0 = *t[0];
+    const int m = col_plan(a0.D, a0.g_dtype).m;
+    return launch_groups<ApplyParams>(
+        t, n, kBlock, apply_params,
+        [](const StepArgs& a) {
+            const ApplyParams p = apply_params(a);
+            return capped_blocks((int64_t)p.nb * p.nslab);
+        },
+        [&](const MultiParams<ApplyParams>& g, dim3 grid) {
+            if (a0.g_dtype == 0)
+                return a0.w_dtype == 0 ? apply_multi_dispatch<float, float>(g, m, grid, s)
+                                       : apply_multi_dispatch<float, uint16_t>(g, m, grid, s);
+            return a0.w_dtype == 0 ? apply_multi_dispatch<uint16_t, float>(g, m, grid, s)
+                                   : apply_multi_dispatch<uint16_t, uint16_t>(g, m, grid, s);
+        });
 }
 
 } // namespace ember

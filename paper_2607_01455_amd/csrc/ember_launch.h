@@ -7,6 +7,8 @@
 
 #include <hip/hip_runtime_api.h>
 
+#include "ember.h"
+
 namespace ember {
 
 constexpr int kWave = 64;           // CDNA wavefront width
@@ -92,6 +94,16 @@ constexpr int kWaves = kBlock / kWave;
 #endif
 #ifndef EMBER_LMHEAD_GROUP_M
 #define EMBER_LMHEAD_GROUP_M 2   // LM-head gradient GEMM: row tiles per group of the tile order
+#endif
+#ifndef EMBER_MULTI_DENSE_STATS_FIRST
+#define EMBER_MULTI_DENSE_STATS_FIRST 1  // multi-table statistics launch: dense tables' blocks first
+#endif
+#ifndef EMBER_MULTI_SPARSE_APPLY_FIRST
+#define EMBER_MULTI_SPARSE_APPLY_FIRST 0 // multi-table apply launch: sparse tables' blocks first
+#endif
+#ifndef EMBER_MULTI_SPARSE_STREAM
+#define EMBER_MULTI_SPARSE_STREAM 0      // multi-table launch with a dense table: sparse tables'
+                                         // statistics loads non-temporal
 #endif
 #ifndef EMBER_MAX_BLOCKS
 #define EMBER_MAX_BLOCKS 384        // row blocks of the statistics pass
@@ -195,6 +207,9 @@ struct StepArgs {
     double inv_alpha;   // 1 / (+lr or -lr); 0 when lr == 0 (no apply launch)
     float eps_over_alpha;
     char* ws;
+    bool stats_stream;  // statistics pass: load every gradient row non-temporally (a
+                        // small table sharing a launch with a dense one keeps out of
+                        // the last-level cache the dense table's rows are left in)
     int fin_nb;         // finalize: partial rows of P and row slabs of rowpart, when
     int fin_nslab;      // they come from the LM-head gradient GEMM (0: the statistics pass's)
 };
@@ -204,6 +219,16 @@ hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
 hipError_t launch_stats(const StepArgs& a, hipStream_t s);
 hipError_t launch_finalize(const StepArgs& a, hipStream_t s);
 hipError_t launch_apply(const StepArgs& a, hipStream_t s);
+
+// Several tables per launch (ember_step_multi).  Tables whose keys are equal
+// use the same kernel instance and may share a launch; each launcher takes
+// tables of one key, in the order their blocks are to be numbered.
+constexpr int kMaxTables = EMBER_MAX_TABLES;
+int stats_key(const StepArgs& a);
+int apply_key(const StepArgs& a);
+hipError_t launch_stats_multi(const StepArgs* const* t, int n, hipStream_t s);
+hipError_t launch_finalize_multi(const StepArgs* const* t, int n, hipStream_t s);
+hipError_t launch_apply_multi(const StepArgs* const* t, int n, hipStream_t s);
 
 // LM-head weight gradient G = dY^T H with the statistics partials in the
 // epilogue (ember_lmhead.hip): rowpart[NT][V] and P[MT][D] in the workspace.

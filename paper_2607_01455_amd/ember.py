@@ -32,7 +32,7 @@ EXPORTED = ("ember_workspace_bytes", "ember_init_state", "ember_step_dense",
             "ember_step_sparse_rows", "ember_rowonly_init_state", "ember_rowonly_step_dense",
             "ember_rowonly_step_sparse_rows", "ember_step_sparse_rows_devn",
             "ember_rowonly_step_sparse_rows_devn", "ember_coalesce_workspace_bytes", "ember_coalesce_rows",
-            "ember_lmhead_step", "ember_get_error", "ember_strerror",
+            "ember_lmhead_step", "ember_step_multi", "ember_get_error", "ember_strerror",
             "ember_profile_enable", "ember_profile_collect")
 
 
@@ -40,6 +40,20 @@ class EmberError(RuntimeError):
     def __init__(self, status: int, where: str):
         super().__init__(f"{where}: {ember_strerror(status)} (status {status})")
         self.status = status
+
+
+EMBER_MAX_TABLES = 8
+
+
+class TableStep(ctypes.Structure):
+    """One table of ember_step_multi (the C struct ember_table_step)."""
+    _fields_ = [("W", ctypes.c_void_p), ("w_dtype", ctypes.c_int), ("ldw", ctypes.c_int64),
+                ("G", ctypes.c_void_p), ("g_dtype", ctypes.c_int), ("ldg", ctypes.c_int64),
+                ("sparse", ctypes.c_int), ("idx", ctypes.c_void_p), ("n_idx", ctypes.c_int64),
+                ("n_idx_dev", ctypes.c_void_p), ("r", ctypes.c_void_p), ("c", ctypes.c_void_p),
+                ("V", ctypes.c_int64), ("D", ctypes.c_int64), ("t", ctypes.c_int64),
+                ("lr", ctypes.c_float), ("beta2", ctypes.c_float), ("eps", ctypes.c_float),
+                ("maximize", ctypes.c_int), ("ws", ctypes.c_void_p), ("ws_bytes", ctypes.c_size_t)]
 
 
 class _KernelStat(ctypes.Structure):
@@ -70,6 +84,7 @@ def _load(path: str = _LIB_PATH) -> ctypes.CDLL:
     lib.ember_coalesce_rows.argtypes = [vp, i64, vp, i32, i64, i64, i64, vp, vp, i32, i64, vp, vp, sz, vp]
     lib.ember_lmhead_step.argtypes = [vp, i32, i64, vp, i64, vp, i64, i64, vp, i32, i64, vp, vp, i64, i64, i64,
                                       f32, f32, f32, i32, vp, sz, vp]
+    lib.ember_step_multi.argtypes = [ctypes.POINTER(TableStep), i32, vp]
     lib.ember_get_error.argtypes = [vp, vp, ctypes.POINTER(i32)]
     lib.ember_strerror.argtypes = [i32]
     lib.ember_strerror.restype = ctypes.c_char_p
@@ -289,6 +304,50 @@ def ember_lmhead_step(W: torch.Tensor, dY: torch.Tensor, H: torch.Tensor, G: tor
                                  _ptr(G), _dtype(G), _ld(G), _ptr(r), _ptr(c), V, D, int(t), float(lr),
                                  float(beta2), float(eps), int(bool(maximize)), _ptr(ws),
                                  ws.numel() * ws.element_size(), _stream(W)), "ember_lmhead_step")
+
+
+def table_step(W: torch.Tensor, G: torch.Tensor | None, r: torch.Tensor, c: torch.Tensor, t: int,
+               ws: torch.Tensor, idx: torch.Tensor | None = None, n_idx_dev: torch.Tensor | None = None,
+               lr: float = 1e-3, beta2: float = 0.999, eps: float = 1e-8,
+               maximize: bool = False) -> TableStep:
+    """One entry of ember_step_multi: a dense step when idx is None, else a
+    sparse-row step on the rows idx lists (with n_idx_dev: the row count in
+    device memory, idx.numel() its maximum).  The tensors must stay alive until
+    the step has run."""
+    V, D = W.shape
+    sparse = idx is not None
+    if sparse and idx.dtype != torch.int64:
+        raise TypeError("idx must be int64")
+    n = idx.numel() if sparse else 0
+    ldg = _ld(G) if G is not None and G.numel() else D
+    return TableStep(_ptr(W), _dtype(W), _ld(W), _ptr(G), _dtype(G) if G is not None else _dtype(W), ldg,
+                     int(sparse), _ptr(idx) if sparse else None, n, _ptr(n_idx_dev), _ptr(r), _ptr(c),
+                     V, D, int(t), float(lr), float(beta2), float(eps), int(bool(maximize)), _ptr(ws),
+                     ws.numel() * ws.element_size())
+
+
+def ember_step_multi(steps, stream_of: torch.Tensor) -> None:
+    """Enqueue the steps of several tables (TableStep entries) on the current
+    stream of stream_of's device: three launches in all."""
+    arr = (TableStep * len(steps))(*steps)
+    _check(LIB.ember_step_multi(arr, len(steps), _stream(stream_of)), "ember_step_multi")
+
+
+def step_tables(items) -> None:
+    """Canonical Ember steps of several tables in one call.  items: tuples
+    (EmberTable, W, G) for a dense step or (EmberTable, W, G_rows, idx) for a
+    sparse-row step; every table advances t by one."""
+    steps = []
+    for it in items:
+        tab, W, G = it[0], it[1], it[2]
+        idx = it[3] if len(it) > 3 else None
+        if tab.row_only:
+            raise ValueError("ember_step_multi takes canonical (row and column) tables")
+        steps.append(table_step(W, G, tab.r, tab.c, tab.t + 1, tab.ws, idx=idx, lr=tab.lr, beta2=tab.beta2,
+                                eps=tab.eps, maximize=tab.maximize))
+    ember_step_multi(steps, items[0][1])
+    for it in items:
+        it[0].t += 1
 
 
 def ember_get_error(ws: torch.Tensor) -> int:

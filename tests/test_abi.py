@@ -302,3 +302,52 @@ def test_binding_marshals_dtypes_and_strides(em):
     assert em._ld(torch.zeros(1, 4096, dtype=torch.bfloat16)) == 4096
     with pytest.raises(TypeError):
         em._ld(torch.zeros(5, 8).t())
+
+
+# ---------------------------------------------------------------------------
+# ember_step_multi: host checks (fake addresses again: every call must fail)
+# ---------------------------------------------------------------------------
+
+def _table(em, base=0, **kw):
+    """A TableStep of a 10 x 64 bf16 table whose buffers start at base + the
+    fake addresses above (base = k * 16 A keeps tables apart)."""
+    a = dict(W=W_ + base, w_dtype=1, ldw=64, G=G_ + base, g_dtype=1, ldg=64, sparse=0, idx=None, n_idx=0,
+             n_idx_dev=None, r=R_ + base, c=C_ + base, V=10, D=64, t=1, lr=1e-3, beta2=0.999, eps=1e-8,
+             maximize=0, ws=WS_ + base, ws_bytes=None)
+    a.update(kw)
+    if a["ws_bytes"] is None:
+        a["ws_bytes"] = _ws_bytes(em, max(a["V"], 1), max(a["D"], 1))
+    return em.TableStep(**a)
+
+
+def _multi(em, tables, n=None):
+    arr = (em.TableStep * max(len(tables), 1))(*tables)
+    return em.LIB.ember_step_multi(arr, len(tables) if n is None else n, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(V=0), "SHAPE"), (dict(ldw=32), "SHAPE"), (dict(W=None), "ARG"), (dict(G=G_ + 16 * A + 2), "ALIGN"),
+    (dict(w_dtype=5), "DTYPE"), (dict(ws_bytes=64), "WORKSPACE"), (dict(t=0), "ARG"), (dict(beta2=1.0), "ARG"),
+    (dict(sparse=2), "ARG"),
+    (dict(sparse=1, idx=IDX_ + 16 * A, n_idx=11), "SHAPE"), (dict(sparse=1, idx=None, n_idx=3), "ARG"),
+    (dict(sparse=1, idx=IDX_ + 16 * A + 4, n_idx=3), "ALIGN"),
+    (dict(sparse=1, idx=IDX_ + 16 * A, n_idx=3, n_idx_dev=IDX_ + 16 * A + 4), "ALIGN"),
+    (dict(sparse=1, idx=IDX_ + 16 * A, n_idx=-1, n_idx_dev=IDX_ + 17 * A), "SHAPE"),
+])
+def test_multi_step_checks_every_table(em, kw, status):
+    # the first table is valid; the second fails its own call's check
+    good = _table(em)
+    assert _multi(em, [good, _table(em, base=16 * A, **kw)]) == getattr(em, "EMBER_ERR_" + status)
+
+
+def test_multi_step_rejects_table_counts_and_overlaps(em):
+    good = _table(em)
+    assert _multi(em, [good], n=0) == em.EMBER_ERR_ARG
+    assert _multi(em, [good] * 9) == em.EMBER_ERR_ARG
+    assert em.LIB.ember_step_multi(None, 1, None) == em.EMBER_ERR_ARG
+    # two tables sharing a workspace, an r/c vector or a weight matrix
+    assert _multi(em, [good, _table(em, base=16 * A, ws=WS_)]) == em.EMBER_ERR_ARG
+    assert _multi(em, [good, _table(em, base=16 * A, r=C_)]) == em.EMBER_ERR_ARG
+    assert _multi(em, [good, _table(em, base=16 * A, W=W_ + 128)]) == em.EMBER_ERR_ARG
+    assert _multi(em, [good, _table(em, base=16 * A, c=WS_ + 256)]) == em.EMBER_ERR_ARG
+    assert _multi(em, [good, good]) == em.EMBER_ERR_ARG
