@@ -45,8 +45,8 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=10)
-    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-rows", type=int, default=65536, help="rows of the oracle's sample")
     p.add_argument("--no-other-configs", action="store_true")
@@ -388,7 +388,9 @@ def main():
 
     schedules = {"multi": step_multi, "sequential": step_sequential}
     step = schedules[args.schedule]
-    for fn in schedules.values():
+    other = "sequential" if args.schedule == "multi" else "multi"
+    # warm-up: the other schedule, then the timed one right before its region
+    for fn in (schedules[other], step):
         for k in range(Wm):
             fn(k)
     torch.cuda.synchronize()
@@ -411,7 +413,6 @@ def main():
 
     ms_step = whole_steps(step)
     # the other schedule on the same inputs, for comparison (not the value)
-    other = "sequential" if args.schedule == "multi" else "multi"
     schedule_ms = {args.schedule: round(ms_step, 4), other: round(whole_steps(schedules[other]), 4)}
 
     # --- timed region A1: the same steps with a marker between the two tables
