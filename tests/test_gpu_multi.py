@@ -212,3 +212,69 @@ def test_full_size_lmhead_and_embedding_tables(em):
     specs = [Spec("lmhead128k", 128256, 4096, torch.bfloat16),
              Spec("embed128k", 128256, 4096, torch.bfloat16, sparse=True, batch_tokens=8 * 2048)]
     _run_against_single_calls(em, specs, steps=2)
+
+
+def test_captured_multi_step_replays_bitwise(em):
+    """One HIP graph holding token -> coalesce and a multi-table call (dense
+    LM head + device-count sparse embedding), replayed on fresh inputs; each
+    replay must give the bits of single-table steps run eagerly on twins."""
+    Vh, Dh, P = 8192, 512, 2048
+    head_cfg = wl.Config("g_head", Vh, Dh, torch.bfloat16, torch.bfloat16, 1, "zipf_rows")
+    emb_cfg = wl.Config("g_emb", Vh, Dh, torch.bfloat16, torch.bfloat16, 1, "sparse_zipf", batch_tokens=P)
+    print("graph capture of ember_step_multi", flush=True)
+
+    def tables():
+        return (wl.make_weights(head_cfg, seed=53, device=DEV), wl.make_weights(emb_cfg, seed=54, device=DEV),
+                em.EmberTable(Vh, Dh, device=DEV), em.EmberTable(Vh, Dh, device=DEV),
+                em.Coalescer(P, Vh, Dh, device=DEV))
+
+    Wh, We, th, te, co = tables()
+    Wh2, We2, th2, te2, co2 = tables()
+    G_static = torch.empty(Vh, Dh, dtype=torch.bfloat16, device=DEV)
+    tok_static = torch.empty(P, dtype=torch.int64, device=DEV)
+    U_static = torch.empty(P, Dh, dtype=torch.bfloat16, device=DEV)
+    t_fixed = 4   # the step counter is a launch argument: a captured step keeps its t
+
+    def multi(G, tok, U):
+        co.enqueue(tok, U)
+        em.ember_step_multi([em.table_step(Wh, G, th.r, th.c, t_fixed, th.ws),
+                             em.table_step(We, co.G_rows, te.r, te.c, t_fixed, te.ws, idx=co.idx,
+                                           n_idx_dev=co.n_out)], G)
+
+    def eager(G, tok, U):
+        th2.t = te2.t = t_fixed - 1
+        th2.step(Wh2, G)
+        te2.step_tokens(We2, tok, U, co2)
+
+    def check():
+        assert em.ember_get_error(te.ws) == em.EMBER_OK and em.ember_get_error(co.ws) == em.EMBER_OK
+        for a, b in ((Wh, Wh2), (th.r, th2.r), (th.c, th2.c), (We, We2), (te.r, te2.r), (te.c, te2.c)):
+            assert _bits_equal(a, b)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        G0 = wl.make_dense_grad(head_cfg, 1, seed=55, device=DEV)
+        tok0, U0 = wl.make_token_batch(emb_cfg, 1, seed=55, device=DEV)
+        G_static.copy_(G0)
+        tok_static.copy_(tok0)
+        U_static.copy_(U0)
+        multi(G_static, tok_static, U_static)
+        eager(G0, tok0, U0)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    check()
+
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        multi(G_static, tok_static, U_static)
+    for rep in range(2, 5):
+        G = wl.make_dense_grad(head_cfg, rep, seed=55, device=DEV)
+        tok, U = wl.make_token_batch(emb_cfg, rep, seed=55, device=DEV)
+        G_static.copy_(G)
+        tok_static.copy_(tok)
+        U_static.copy_(U)
+        graph.replay()
+        eager(G, tok, U)
+        torch.cuda.synchronize()
+        check()
