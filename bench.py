@@ -506,7 +506,20 @@ def main():
     c1.record(stream)
     torch.cuda.synchronize()
     copy_gbps = 2 * src.numel() * 2 / (c0.elapsed_time(c1) / 10 * 1e-3) / 1e9
-    del src, dst
+    # the library's streaming probe over the same bytes: practical ceilings of a
+    # pure read, a copy and two reads + one write (the apply pass's pattern)
+    src2 = torch.empty_like(src).fill_(2.0)
+    ceilings = {}
+    for mode, name, ops in ((0, "read", 1), (1, "copy", 2), (2, "two_reads_one_write", 3)):
+        for _ in range(2):
+            ember.ember_stream_probe(mode, dst, src, src2)
+        c0.record(stream)
+        for _ in range(10):
+            ember.ember_stream_probe(mode, dst, src, src2)
+        c1.record(stream)
+        torch.cuda.synchronize()
+        ceilings[name] = round(ops * src.numel() * 2 / (c0.elapsed_time(c1) / 10 * 1e-3) / 1e9, 1)
+    del src, src2, dst
 
     out = {
         "metric": METRIC,
@@ -551,6 +564,7 @@ def main():
         "roofline": multi_roofline if args.schedule == "multi" else dense_roofline,
         "roofline_dense_apply": dense_roofline,
         "torch_device_copy_GBps": round(copy_gbps, 1),
+        "stream_ceilings_GBps": ceilings,
         "row_only": None,
         "coalesce": None,
         "lmhead_wgrad": None,

@@ -365,6 +365,21 @@ typedef struct {
 } ember_kernel_stat;
 
 int ember_profile_enable(int enable);
+
+/*
+ * Streaming probe (diagnostics): the practical HBM ceilings the passes above
+ * are measured against.  Enqueues one grid-stride kernel with 16-byte
+ * non-temporal accesses over `bytes` bytes of each operand:
+ *   mode 0: reads a (dst receives at most 4 bytes, in practice none);
+ *   mode 1: dst <- a (copy);
+ *   mode 2: dst <- a + b in 32-bit integer lanes (two reads, one write: the
+ *           apply pass's access pattern).
+ * dst, a (and b for mode 2) are device pointers, 16-byte aligned, each
+ * covering `bytes`, which must be a multiple of 16; dst must not overlap a
+ * or b.  Returns EMBER_ERR_ARG (mode or null pointer), EMBER_ERR_SHAPE,
+ * EMBER_ERR_ALIGN, EMBER_ERR_HIP or EMBER_OK.
+ */
+int ember_stream_probe(int mode, void* dst, const void* a, const void* b, size_t bytes, hipStream_t stream);
 int ember_profile_collect(ember_kernel_stat* out, int max_entries, int* n_entries);
 
 #ifdef __cplusplus

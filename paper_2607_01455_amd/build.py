@@ -14,7 +14,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libember.so")
-SOURCES = ["ember_kernels.hip", "ember_coalesce.hip", "ember_lmhead.hip", "ember_api.cpp"]
+SOURCES = ["ember_kernels.hip", "ember_coalesce.hip", "ember_lmhead.hip", "ember_probe.hip", "ember_api.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

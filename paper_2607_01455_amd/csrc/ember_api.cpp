@@ -618,6 +618,16 @@ const char* ember_strerror(int status) {
     }
 }
 
+int ember_stream_probe(int mode, void* dst, const void* a, const void* b, size_t bytes, hipStream_t stream) {
+    if (mode < 0 || mode > 2 || dst == nullptr || a == nullptr || (mode == 2 && b == nullptr))
+        return EMBER_ERR_ARG;
+    if (bytes % 16 != 0) return EMBER_ERR_SHAPE;
+    if (!aligned(dst, 16) || !aligned(a, 16) || (b != nullptr && !aligned(b, 16))) return EMBER_ERR_ALIGN;
+    const hipError_t e = timed("ember_stream_probe", stream,
+                               [&] { return ember::launch_stream_probe(mode, dst, a, b, bytes, stream); });
+    return e == hipSuccess ? EMBER_OK : EMBER_ERR_HIP;
+}
+
 int ember_profile_enable(int enable) {
     std::lock_guard<std::mutex> lock(g_prof_mu);
     g_prof_on = enable != 0;

@@ -220,6 +220,9 @@ hipError_t launch_stats(const StepArgs& a, hipStream_t s);
 hipError_t launch_finalize(const StepArgs& a, hipStream_t s);
 hipError_t launch_apply(const StepArgs& a, hipStream_t s);
 
+// Streaming probe (ember_probe.hip): mode 0 read, 1 copy, 2 dst = a + b.
+hipError_t launch_stream_probe(int mode, void* dst, const void* a, const void* b, size_t bytes, hipStream_t s);
+
 // Several tables per launch (ember_step_multi).  Tables whose keys are equal
 // use the same kernel instance and may share a launch; each launcher takes
 // tables of one key, in the order their blocks are to be numbered.

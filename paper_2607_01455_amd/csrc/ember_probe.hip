@@ -1,0 +1,87 @@
+// Streaming probe kernels: the practical HBM ceilings that the Ember passes
+// are measured against (a diagnostic beside the method, not part of it).
+//
+// mode 0 reads a; mode 1 copies a to dst; mode 2 writes dst = a + b (32-bit
+// integer lanes): two reads and one write, the access pattern of the apply
+// pass.  16-byte non-temporal accesses, eight in flight per thread and operand,
+// over contiguous 32 KiB tiles.
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "ember_launch.h"
+
+namespace ember {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kProbeUnroll = 8;                                  // 16-byte accesses per thread per tile
+constexpr int64_t kProbeTile = (int64_t)kBlock * kProbeUnroll;   // 16-byte chunks per tile (32 KiB)
+constexpr int64_t kProbeMaxBlocks = 8192;
+// mode 0 stores its xor of the data only if it equals this value, so the loads
+// stay live; dst then receives at most 4 bytes
+constexpr uint32_t kProbeMagic = 0x9E3779B9u;
+
+// Block b streams tiles b, b + gridDim, ...; within a tile, access u of all
+// threads covers 4 KiB contiguously.
+template <int kMode>
+__global__ __launch_bounds__(kBlock) void ember_stream_probe_kernel(u32x4* __restrict__ dst, const u32x4* __restrict__ a,
+                                                                    const u32x4* __restrict__ b, int64_t n) {
+    uint32_t acc = 0;
+    const int64_t full = n / kProbeTile;
+    for (int64_t t = blockIdx.x; t < full; t += gridDim.x) {
+        const int64_t base = t * kProbeTile + threadIdx.x;
+        u32x4 x[kProbeUnroll], y[kProbeUnroll];
+#pragma unroll
+        for (int u = 0; u < kProbeUnroll; ++u) x[u] = __builtin_nontemporal_load(a + base + u * kBlock);
+        if constexpr (kMode == 2) {
+#pragma unroll
+            for (int u = 0; u < kProbeUnroll; ++u) y[u] = __builtin_nontemporal_load(b + base + u * kBlock);
+        }
+#pragma unroll
+        for (int u = 0; u < kProbeUnroll; ++u) {
+            if constexpr (kMode == 0) {
+                acc ^= x[u].x ^ x[u].y ^ x[u].z ^ x[u].w;
+            } else {
+                u32x4 v = x[u];
+                if constexpr (kMode == 2) v += y[u];
+                __builtin_nontemporal_store(v, dst + base + u * kBlock);
+            }
+        }
+    }
+    // the last partial tile, one chunk per thread at a time
+    for (int64_t i = full * kProbeTile + (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * kBlock) {
+        u32x4 v = __builtin_nontemporal_load(a + i);
+        if constexpr (kMode == 0) {
+            acc ^= v.x ^ v.y ^ v.z ^ v.w;
+        } else {
+            if constexpr (kMode == 2) v += __builtin_nontemporal_load(b + i);
+            __builtin_nontemporal_store(v, dst + i);
+        }
+    }
+    if constexpr (kMode == 0) {
+        if (acc == kProbeMagic) reinterpret_cast<uint32_t*>(dst)[0] = acc;
+    }
+}
+
+} // namespace
+
+hipError_t launch_stream_probe(int mode, void* dst, const void* a, const void* b, size_t bytes, hipStream_t s) {
+    const int64_t n = (int64_t)(bytes / 16);
+    if (n == 0) return hipSuccess;
+    int64_t blocks = (n + kProbeTile - 1) / kProbeTile;
+    if (blocks > kProbeMaxBlocks) blocks = kProbeMaxBlocks;
+    const dim3 grid((unsigned)blocks);
+    u32x4* d = static_cast<u32x4*>(dst);
+    const u32x4* x = static_cast<const u32x4*>(a);
+    const u32x4* y = static_cast<const u32x4*>(b);
+    if (mode == 0) ember_stream_probe_kernel<0><<<grid, kBlock, 0, s>>>(d, x, y, n);
+    else if (mode == 1) ember_stream_probe_kernel<1><<<grid, kBlock, 0, s>>>(d, x, y, n);
+    else if (mode == 2) ember_stream_probe_kernel<2><<<grid, kBlock, 0, s>>>(d, x, y, n);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+} // namespace ember

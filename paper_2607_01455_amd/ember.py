@@ -33,7 +33,7 @@ EXPORTED = ("ember_workspace_bytes", "ember_init_state", "ember_step_dense",
             "ember_rowonly_step_sparse_rows", "ember_step_sparse_rows_devn",
             "ember_rowonly_step_sparse_rows_devn", "ember_coalesce_workspace_bytes", "ember_coalesce_rows",
             "ember_lmhead_step", "ember_step_multi", "ember_get_error", "ember_strerror",
-            "ember_profile_enable", "ember_profile_collect")
+            "ember_profile_enable", "ember_profile_collect", "ember_stream_probe")
 
 
 class EmberError(RuntimeError):
@@ -90,6 +90,7 @@ def _load(path: str = _LIB_PATH) -> ctypes.CDLL:
     lib.ember_strerror.restype = ctypes.c_char_p
     lib.ember_profile_enable.argtypes = [i32]
     lib.ember_profile_collect.argtypes = [ctypes.POINTER(_KernelStat), i32, ctypes.POINTER(i32)]
+    lib.ember_stream_probe.argtypes = [i32, vp, vp, vp, sz, vp]
     for name in EXPORTED:
         if name != "ember_strerror":
             getattr(lib, name).restype = i32
@@ -367,6 +368,14 @@ def ember_profile_collect() -> dict:
     n = ctypes.c_int(0)
     _check(LIB.ember_profile_collect(buf, 16, ctypes.byref(n)), "ember_profile_collect")
     return {buf[k].name.decode(): (buf[k].launches, buf[k].total_ms) for k in range(n.value)}
+
+
+def ember_stream_probe(mode: int, dst: torch.Tensor, a: torch.Tensor, b: torch.Tensor | None = None) -> None:
+    """Streaming probe over a's bytes: 0 read a, 1 copy a to dst, 2 dst = a + b
+    (32-bit integer lanes)."""
+    nbytes = a.numel() * a.element_size()
+    _check(LIB.ember_stream_probe(int(mode), _ptr(dst), _ptr(a), _ptr(b), nbytes, _stream(a)),
+           "ember_stream_probe")
 
 
 class EmberTable:

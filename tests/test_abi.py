@@ -351,3 +351,15 @@ def test_multi_step_rejects_table_counts_and_overlaps(em):
     assert _multi(em, [good, _table(em, base=16 * A, W=W_ + 128)]) == em.EMBER_ERR_ARG
     assert _multi(em, [good, _table(em, base=16 * A, c=WS_ + 256)]) == em.EMBER_ERR_ARG
     assert _multi(em, [good, good]) == em.EMBER_ERR_ARG
+
+
+def test_stream_probe_rejects_bad_arguments_on_host(em):
+    P = em.LIB.ember_stream_probe
+    assert P(3, W_, G_, None, 64, None) == em.EMBER_ERR_ARG
+    assert P(-1, W_, G_, None, 64, None) == em.EMBER_ERR_ARG
+    assert P(1, None, G_, None, 64, None) == em.EMBER_ERR_ARG
+    assert P(1, W_, None, None, 64, None) == em.EMBER_ERR_ARG
+    assert P(2, W_, G_, None, 64, None) == em.EMBER_ERR_ARG
+    assert P(1, W_, G_, None, 40, None) == em.EMBER_ERR_SHAPE
+    assert P(1, W_ + 8, G_, None, 64, None) == em.EMBER_ERR_ALIGN
+    assert P(2, W_, G_, R_ + 4, 64, None) == em.EMBER_ERR_ALIGN
