@@ -1404,7 +1404,10 @@ WsLayout ws_layout(int64_t V, int64_t D) {
     WsLayout L;
     // the LM-head gradient GEMM writes its partials into the same regions
     const LmheadPlan lp = lmhead_plan(V, D);
-    const int nb = row_blocks(V) > lp.MT ? row_blocks(V) : lp.MT;
+    // the narrower plan (bf16: half the slabs of fp32) allows the most row blocks
+    int nb = row_blocks(V, col_plan(D, 1).nslab);
+    if (row_blocks(V, col_plan(D, 0).nslab) > nb) nb = row_blocks(V, col_plan(D, 0).nslab);
+    if (lp.MT > nb) nb = lp.MT;
     const int nslab = nslab_for(D) > lp.NT ? nslab_for(D) : lp.NT;
     size_t off = 0;
     L.flag = off;
@@ -1449,7 +1452,7 @@ static StatsParams stats_params(const StepArgs& a) {
     p.total_chunks = cp.total_chunks;
     p.slab_chunks = cp.slab_chunks;
     p.nslab = cp.nslab;
-    p.nb = a.fin_nb > 0 ? a.fin_nb : row_blocks(a.rows, a.sparse);
+    p.nb = a.fin_nb > 0 ? a.fin_nb : row_blocks(a.rows, col_plan(a.D, a.g_dtype).nslab, a.sparse);
     {
         const double row_bytes = (double)a.D * (a.g_dtype == 0 ? 4 : 2);
         const int64_t keep = (int64_t)((double)EMBER_STATS_KEEP_MB * 1048576.0 / row_bytes);
@@ -1482,7 +1485,7 @@ static FinParams finalize_params(const StepArgs& a) {
     const WsLayout L = ws_layout(a.V, a.D);
     FinParams p;
     p.P = reinterpret_cast<const float*>(a.ws + L.p);
-    p.nb = a.fin_nb > 0 ? a.fin_nb : row_blocks(a.rows, a.sparse);
+    p.nb = a.fin_nb > 0 ? a.fin_nb : row_blocks(a.rows, col_plan(a.D, a.g_dtype).nslab, a.sparse);
     p.D = a.D;
     p.ncolblocks = (int)((a.D + kFinCols - 1) / kFinCols);
     p.rowpart = reinterpret_cast<const float*>(a.ws + L.rowpart);
