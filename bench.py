@@ -149,29 +149,38 @@ def other_configs(ember, wl, torch, dev, K):
 
 def row_only_section(ember, wl, torch, dev, K, Wm, W_head, W_emb, grads, batches):
     """The same two-table workload with row-only Ember (Section 2.1; state V,
-    one fused pass per table): whole-step time, per-table medians and kernel
-    averages, in row-only algorithmic bytes."""
+    one fused pass per table): whole-step time (both tables in one multi-table
+    call, and one call per table), per-table medians and kernel averages, in
+    row-only algorithmic bytes."""
     stream = torch.cuda.current_stream()
     head = ember.EmberTable(V, D, device=dev, row_only=True)
     emb = ember.EmberTable(V, D, device=dev, row_only=True)
     n_grads = len(grads)
 
-    def step(k):
+    def step_sequential(k):
         head.step(W_head, grads[k % n_grads])
         idx, Gr = batches[k]
         emb.step_sparse_rows(W_emb, Gr, idx)
 
-    for k in range(Wm):
-        step(k)
-    torch.cuda.synchronize()
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for k in range(K):
-        step(Wm + k)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    ms_step = e0.elapsed_time(e1) / K
+    def step_multi(k):
+        idx, Gr = batches[k]
+        ember.step_tables([(head, W_head, grads[k % n_grads]), (emb, W_emb, Gr, idx)])
+
+    def whole_steps(fn):
+        for k in range(Wm):
+            fn(k)
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for k in range(K):
+            fn(Wm + k)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / K
+
+    seq_ms = whole_steps(step_sequential)
+    ms_step = whole_steps(step_multi)
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
     for k in range(K):
         ev[k][0].record(stream)
@@ -206,6 +215,7 @@ def row_only_section(ember, wl, torch, dev, K, Wm, W_head, W_emb, grads, batches
         "ms_per_step": round(ms_step, 4),
         "GBps": round(gbps, 1),
         "pct_of_peak": round(100.0 * gbps / PEAK_GBPS, 2),
+        "schedules_ms_per_step": {"multi": round(ms_step, 4), "sequential": round(seq_ms, 4)},
         "algorithmic_bytes_per_step": int(dense_bytes + sparse_bytes),
         "dense_lmhead": {"ms": round(dense_ms, 4), "bytes": dense_bytes,
                          "GBps": round(dense_bytes / (dense_ms * 1e-3) / 1e9, 1),

@@ -177,6 +177,11 @@ int ember_step_sparse_rows_devn(void* W, int w_dtype, int64_t ldw,
  *                            with n_idx_dev non-NULL the row count is read from
  *                            that device int64 when the step runs and n_idx is
  *                            its maximum, as for ember_step_sparse_rows_devn.
+ *   row_only = 1             the row-only step of that table (state r only; c
+ *                            may be NULL), as ember_rowonly_step_dense /
+ *                            ember_rowonly_step_sparse_rows(_devn) would take
+ *                            it: the sparse row-only tables' id checks share one
+ *                            launch and the row-only passes one more.
  * Tables may differ in every field (shape, dtypes, scalars, t).  Tables with
  * the same dtypes and the same columns-per-lane plan share launches; others
  * add launches of their own.
@@ -198,6 +203,7 @@ typedef struct {
     int g_dtype;
     int64_t ldg;
     int sparse;
+    int row_only;
     const int64_t* idx;
     int64_t n_idx;
     const int64_t* n_idx_dev;

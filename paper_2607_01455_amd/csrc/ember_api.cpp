@@ -183,7 +183,10 @@ int check_table(const ember_table_step& x) {
         if (st == EMBER_OK && x.n_idx > 0 && x.idx == nullptr) st = EMBER_ERR_ARG;
         if (st == EMBER_OK && x.idx != nullptr && !aligned(x.idx, 8)) st = EMBER_ERR_ALIGN;
     }
-    if (st == EMBER_OK) st = check_state(x.r, x.c, x.ws, x.ws_bytes, x.V, x.D);
+    if (st == EMBER_OK && x.row_only != 0 && x.row_only != 1) st = EMBER_ERR_ARG;
+    if (st == EMBER_OK)
+        st = x.row_only ? check_rowonly_state(x.r, x.ws, x.ws_bytes, x.V, x.D)
+                        : check_state(x.r, x.c, x.ws, x.ws_bytes, x.V, x.D);
     if (st == EMBER_OK) st = check_scalars(x.t, x.lr, x.beta2, x.eps);
     return st;
 }
@@ -192,7 +195,7 @@ int check_table(const ember_table_step& x) {
 void table_spans(const ember_table_step& x, Span out[4]) {
     out[0] = span_of(x.ws, ember::ws_layout(x.V, x.D).total);
     out[1] = span_of(x.r, (size_t)x.V * 4);
-    out[2] = span_of(x.c, (size_t)x.D * 4);
+    out[2] = x.row_only ? span_of(nullptr, 0) : span_of(x.c, (size_t)x.D * 4);
     const size_t es = dtype_size(x.w_dtype);
     out[3] = span_of(x.W, ((size_t)(x.V - 1) * (size_t)x.ldw + (size_t)x.D) * es);
 }
@@ -383,12 +386,14 @@ int ember_step_multi(const ember_table_step* tables, int n_tables, hipStream_t s
         a.n_dev = a.sparse ? x.n_idx_dev : nullptr;
         a.rows = a.sparse ? x.n_idx : x.V;
         a.r = x.r;
-        a.c = x.c;
+        a.c = x.row_only ? nullptr : x.c;
         a.V = x.V;
         a.D = x.D;
         a.ws = static_cast<char*>(x.ws);
         set_scalars(a, x.lr, x.beta2, x.eps, x.t, x.maximize);
     }
+    std::vector<bool> row_only((size_t)n_tables);
+    for (int i = 0; i < n_tables; ++i) row_only[(size_t)i] = tables[i].row_only != 0;
     // Block order inside a launch: the statistics pass runs the sparse tables
     // first, so that the dense tables' last rows, which the apply pass (rows
     // high to low) reads first, are the ones left in the last-level cache; the
@@ -396,29 +401,49 @@ int ember_step_multi(const ember_table_step* tables, int n_tables, hipStream_t s
     // every weight and has no apply blocks (a sparse one still clears its
     // index-error flag there).
     bool any_dense = false;
-    for (const StepArgs& a : args) any_dense = any_dense || !a.sparse;
-    for (StepArgs& a : args) a.stats_stream = EMBER_MULTI_SPARSE_STREAM && a.sparse && any_dense;
-    std::vector<const StepArgs*> sparse_first, dense_first;
-    for (const StepArgs& a : args)
-        if (a.sparse != (bool)EMBER_MULTI_DENSE_STATS_FIRST) sparse_first.push_back(&a);
-    for (const StepArgs& a : args)
-        if (a.sparse == (bool)EMBER_MULTI_DENSE_STATS_FIRST) sparse_first.push_back(&a);
-    for (const StepArgs& a : args)
-        if (EMBER_MULTI_SPARSE_APPLY_FIRST && a.sparse) dense_first.push_back(&a);
-    for (const StepArgs& a : args)
-        if (!a.sparse && a.inv_alpha != 0.0) dense_first.push_back(&a);
-    for (const StepArgs& a : args)
-        if (!EMBER_MULTI_SPARSE_APPLY_FIRST && a.sparse) dense_first.push_back(&a);
-    hipError_t e = timed("ember_stats_multi", stream, [&] {
-        return run_phase(sparse_first, ember::stats_key, ember::launch_stats_multi, stream);
-    });
-    if (e == hipSuccess)
+    for (size_t i = 0; i < args.size(); ++i) any_dense = any_dense || (!row_only[i] && !args[i].sparse);
+    for (size_t i = 0; i < args.size(); ++i)
+        args[i].stats_stream = EMBER_MULTI_SPARSE_STREAM && !row_only[i] && args[i].sparse && any_dense;
+    // canonical tables: statistics, finalize and apply launches; row-only
+    // tables: the sparse ones' id checks, then one fused pass
+    std::vector<const StepArgs*> sparse_first, dense_first, ro_sparse, ro_all;
+    for (size_t i = 0; i < args.size(); ++i)
+        if (!row_only[i] && args[i].sparse != (bool)EMBER_MULTI_DENSE_STATS_FIRST) sparse_first.push_back(&args[i]);
+    for (size_t i = 0; i < args.size(); ++i)
+        if (!row_only[i] && args[i].sparse == (bool)EMBER_MULTI_DENSE_STATS_FIRST) sparse_first.push_back(&args[i]);
+    for (size_t i = 0; i < args.size(); ++i)
+        if (!row_only[i] && EMBER_MULTI_SPARSE_APPLY_FIRST && args[i].sparse) dense_first.push_back(&args[i]);
+    for (size_t i = 0; i < args.size(); ++i)
+        if (!row_only[i] && !args[i].sparse && args[i].inv_alpha != 0.0) dense_first.push_back(&args[i]);
+    for (size_t i = 0; i < args.size(); ++i)
+        if (!row_only[i] && !EMBER_MULTI_SPARSE_APPLY_FIRST && args[i].sparse) dense_first.push_back(&args[i]);
+    for (size_t i = 0; i < args.size(); ++i) {
+        if (!row_only[i]) continue;
+        // a sparse table with no rows and a host count has no ids to check
+        if (args[i].sparse && (args[i].rows > 0 || args[i].n_dev != nullptr)) ro_sparse.push_back(&args[i]);
+        ro_all.push_back(&args[i]);
+    }
+    hipError_t e = hipSuccess;
+    if (!ro_sparse.empty())
+        e = timed("ember_rowonly_validate_multi", stream, [&] {
+            return run_phase(ro_sparse, [](const StepArgs&) { return 0; }, ember::launch_rowonly_validate_multi,
+                             stream);
+        });
+    if (e == hipSuccess && !sparse_first.empty())
+        e = timed("ember_stats_multi", stream, [&] {
+            return run_phase(sparse_first, ember::stats_key, ember::launch_stats_multi, stream);
+        });
+    if (e == hipSuccess && !sparse_first.empty())
         e = timed("ember_finalize_multi", stream, [&] {
             return run_phase(sparse_first, [](const StepArgs&) { return 0; }, ember::launch_finalize_multi, stream);
         });
     if (e == hipSuccess && !dense_first.empty())
         e = timed("ember_apply_multi", stream, [&] {
             return run_phase(dense_first, ember::apply_key, ember::launch_apply_multi, stream);
+        });
+    if (e == hipSuccess && !ro_all.empty())
+        e = timed("ember_rowonly_multi", stream, [&] {
+            return run_phase(ro_all, ember::rowonly_key, ember::launch_rowonly_multi, stream);
         });
     return e == hipSuccess ? EMBER_OK : EMBER_ERR_HIP;
 }

@@ -1107,8 +1107,9 @@ __device__ __forceinline__ void rowonly_rows(const RowOnlyParams& a, int64_t nro
 // the row sum is a butterfly over the wave, and no barrier is needed.  Each
 // wave takes kRowOnlyWaveRows adjacent rows at a time; the waves of a block
 // interleave over the block's rows.
-template <typename GT, typename WT, int C, bool kSparse, bool kExact>
-__device__ __forceinline__ void rowonly_wave_rows(const RowOnlyParams& a, int64_t nrows, int64_t vb) {
+template <typename GT, typename WT, int C, bool kSparse, bool kExact, bool kRuntime = false>
+__device__ __forceinline__ void rowonly_wave_rows(const RowOnlyParams& a, int64_t nrows, int64_t vb,
+                                                  bool sparse_rt = false) {
     constexpr int EPC = 16 / (int)sizeof(GT);
     constexpr int R = kRowOnlyWaveRows;
     constexpr int kWBytes = EPC * (int)sizeof(WT);   // bytes of W per chunk
@@ -1136,7 +1137,7 @@ __device__ __forceinline__ void rowonly_wave_rows(const RowOnlyParams& a, int64_
         for (int j = 0; j < R; ++j) {
             rv[j] = k0 + j < r1;
             const int64_t row = rv[j] ? k0 + j : r0;
-            wrow[j] = kSparse ? a.idx[row] : row;
+            wrow[j] = (kRuntime ? sparse_rt : kSparse) ? a.idx[row] : row;
             gr[j] = G + row * a.ldg;
             wr[j] = W + wrow[j] * a.ldw;
             rold[j] = a.r[wrow[j]];
@@ -1218,8 +1219,8 @@ __device__ __forceinline__ void rowonly_decay(const RowOnlyParams& a, int err, i
 
 // Every block of the sparse step has read the error bits before it counts
 // itself; the last one clears them for the next step.
-__device__ __forceinline__ void rowonly_clear_flag(const RowOnlyParams& a, int* last) {
-    if (block_ticket(a.ticket, (int)gridDim.x, last) && threadIdx.x == 0) {
+__device__ __forceinline__ void rowonly_clear_flag(const RowOnlyParams& a, int nblocks, int* last) {
+    if (block_ticket(a.ticket, nblocks, last) && threadIdx.x == 0) {
         *a.flag = 0;
         *a.ticket = 0;
     }
@@ -1228,24 +1229,42 @@ __device__ __forceinline__ void rowonly_clear_flag(const RowOnlyParams& a, int* 
 // Dense: blocks [0, nb) over the V rows.  Sparse: the same over the n gradient
 // rows (mapped through idx), then the decay blocks.  kExact: D is a multiple
 // of the chunk width, so no chunk is partial.
-template <typename GT, typename WT, int C, bool kSparse, bool kExact>
-__global__ __launch_bounds__(kBlock) void ember_rowonly_wave(RowOnlyParams a) {
-    __shared__ int last;
+// Block `blk` of the `nblk` blocks of one table (kRuntime: dense or sparse is
+// the uniform flag sparse_rt, one body for both kinds in a multi-table launch).
+template <typename GT, typename WT, int C, bool kSparseArg, bool kExact, bool kRuntime = false>
+__device__ __forceinline__ void rowonly_wave_block(const RowOnlyParams& a, unsigned blk, unsigned nblk, int* last,
+                                                   bool sparse_rt = false) {
+    const bool kSparse = kRuntime ? sparse_rt : kSparseArg;
     if (!kSparse) {
-        if (blockIdx.x == 0 && threadIdx.x == 0) *a.status = 0;
-        for (int64_t vb = blockIdx.x; vb < a.nb; vb += gridDim.x)
-            rowonly_wave_rows<GT, WT, C, false, kExact>(a, a.rows, vb);
+        if (blk == 0 && threadIdx.x == 0) *a.status = 0;
+        for (int64_t vb = blk; vb < a.nb; vb += nblk)
+            rowonly_wave_rows<GT, WT, C, false, kExact, kRuntime>(a, a.rows, vb, false);
         return;
     }
     const int err = *a.flag;
-    if (blockIdx.x == 0 && threadIdx.x == 0) *a.status = err;
+    if (blk == 0 && threadIdx.x == 0) *a.status = err;
     bool bad_count = false;
     const int64_t nrows = active_rows(a.n_dev, a.rows, bad_count);
-    for (int64_t vb = blockIdx.x; vb < a.nvb; vb += gridDim.x) {
+    for (int64_t vb = blk; vb < a.nvb; vb += nblk) {
         if (vb >= a.nb) rowonly_decay(a, err, vb - a.nb);
-        else if (!err) rowonly_wave_rows<GT, WT, C, true, kExact>(a, nrows, vb);
+        else if (!err) rowonly_wave_rows<GT, WT, C, true, kExact, kRuntime>(a, nrows, vb, true);
     }
-    rowonly_clear_flag(a, &last);
+    rowonly_clear_flag(a, (int)nblk, last);
+}
+
+template <typename GT, typename WT, int C, bool kSparse, bool kExact>
+__global__ __launch_bounds__(kBlock) void ember_rowonly_wave(RowOnlyParams a) {
+    __shared__ int last;
+    rowonly_wave_block<GT, WT, C, kSparse, kExact>(a, blockIdx.x, gridDim.x, &last);
+}
+
+template <typename GT, typename WT, int C, bool kExact>
+__global__ __launch_bounds__(kBlock) void ember_rowonly_wave_multi(MultiParams<RowOnlyParams> g) {
+    __shared__ int last;
+    const int k = multi_table(g.first, g.ntab);
+    const RowOnlyParams p = g.p[k];
+    rowonly_wave_block<GT, WT, C, false, kExact, true>(p, blockIdx.x - g.first[k], g.first[k + 1] - g.first[k], &last,
+                                                       g.sparse[k] != 0);
 }
 
 // Longer rows: a block of waves per row (see rowonly_rows).
@@ -1268,25 +1287,48 @@ __global__ __launch_bounds__(kRowOnlyMaxWaves * kWave) void ember_rowonly(RowOnl
         if (vb >= a.nb) rowonly_decay(a, err, vb - a.nb);
         else if (!err) rowonly_rows<GT, WT, M, S, true, kResident>(a, nrows, vb, part, rn_lds);
     }
-    rowonly_clear_flag(a, &last);
+    rowonly_clear_flag(a, (int)gridDim.x, &last);
 }
 
 // Sparse row-only step, first launch: validates idx and marks the touched rows
 // (slot = 1 + position in idx).  Error bits are ORed into the flag, which the
 // fused launch reads and clears.
-__global__ __launch_bounds__(kBlock) void ember_rowonly_validate(const int64_t* idx, int64_t n_max,
-                                                                const int64_t* n_dev, int64_t V, int* slot,
-                                                                int* flag) {
+struct ValidateParams {
+    const int64_t* idx;
+    int64_t n_max;
+    const int64_t* n_dev;
+    int64_t V;
+    int* slot;
+    int* flag;
+};
+
+// Block `blk` of the row-only sparse step's id validation of one table.
+__device__ __forceinline__ void rowonly_validate_block(const ValidateParams& a, unsigned blk) {
+    const int64_t* idx = a.idx;
+    const int64_t V = a.V;
+    int* slot = a.slot;
+    int* flag = a.flag;
     bool bad_count = false;
-    const int64_t n = active_rows(n_dev, n_max, bad_count);
-    if (bad_count && blockIdx.x == 0 && threadIdx.x == 0) atomicOr(flag, kFlagCount);
-    const int64_t k = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    const int64_t n = active_rows(a.n_dev, a.n_max, bad_count);
+    if (bad_count && blk == 0 && threadIdx.x == 0) atomicOr(flag, kFlagCount);
+    const int64_t k = (int64_t)blk * kBlock + threadIdx.x;
     if (k >= n) return;
     const int64_t i = idx[k];
     int bits = 0;
     if (i < 0 || i >= V) bits = kFlagRange;
     else if (atomicCAS(&slot[i], 0, (int)(k + 1)) != 0) bits = kFlagDuplicate;
     if (bits) atomicOr(flag, bits);
+}
+
+__global__ __launch_bounds__(kBlock) void ember_rowonly_validate(const int64_t* idx, int64_t n_max,
+                                                                const int64_t* n_dev, int64_t V, int* slot,
+                                                                int* flag) {
+    rowonly_validate_block(ValidateParams{idx, n_max, n_dev, V, slot, flag}, blockIdx.x);
+}
+
+__global__ __launch_bounds__(kBlock) void ember_rowonly_validate_multi(MultiParams<ValidateParams> g) {
+    const int k = multi_table(g.first, g.ntab);
+    rowonly_validate_block(g.p[k], blockIdx.x - g.first[k]);
 }
 
 // ---------------------------------------------------------------------------
@@ -1572,13 +1614,9 @@ hipError_t launch_rowonly_validate(const StepArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_rowonly(const StepArgs& a, hipStream_t s) {
+static RowOnlyParams rowonly_params(const StepArgs& a) {
     const WsLayout L = ws_layout(a.V, a.D);
     const ColPlan cp = col_plan(a.D, a.g_dtype);
-    const bool resident = cp.nslab <= 2 * kRowOnlyMaxWaves;
-    const int spw = cp.nslab <= kRowOnlyMaxWaves ? 1 : 2;
-    const int waves = resident ? (cp.nslab + spw - 1) / spw : kRowOnlyMaxWaves;
-    if ((spw == 2 || !resident) && cp.m != 2) return hipErrorInvalidValue;
     RowOnlyParams p;
     p.W = a.W;
     p.ldw = a.ldw;
@@ -1605,14 +1643,31 @@ hipError_t launch_rowonly(const StepArgs& a, hipStream_t s) {
     p.status = reinterpret_cast<int*>(a.ws + L.status);
     const int64_t ndecay = a.sparse ? (a.V + kDecayRows - 1) / kDecayRows : 0;
     p.nvb = p.nb + ndecay;
+    return p;
+}
+
+// Chunks per lane of the one-wave-per-row kernel, or 0 for rows too long for it.
+static int rowonly_wave_chunks(const StepArgs& a) {
+    const ColPlan cp = col_plan(a.D, a.g_dtype);
+    if (cp.total_chunks > kRowOnlyWaveChunks) return 0;
+    int c = 1;
+    while (c * kWave < cp.total_chunks) c *= 2;
+    return c;
+}
+
+hipError_t launch_rowonly(const StepArgs& a, hipStream_t s) {
+    const ColPlan cp = col_plan(a.D, a.g_dtype);
+    const bool resident = cp.nslab <= 2 * kRowOnlyMaxWaves;
+    const int spw = cp.nslab <= kRowOnlyMaxWaves ? 1 : 2;
+    const int waves = resident ? (cp.nslab + spw - 1) / spw : kRowOnlyMaxWaves;
+    if ((spw == 2 || !resident) && cp.m != 2) return hipErrorInvalidValue;
+    const RowOnlyParams p = rowonly_params(a);
     if (p.nvb == 0) return hipSuccess;
     const dim3 grid((unsigned)capped_blocks(p.nvb));
-    if (cp.total_chunks <= kRowOnlyWaveChunks) {
-        int c = 1;
-        while (c * kWave < cp.total_chunks) c *= 2;
+    const int c = rowonly_wave_chunks(a);
+    if (c > 0)
         return a.sparse ? rowonly_wave_dispatch_t<true>(p, a.g_dtype, a.w_dtype, c, grid, s)
                         : rowonly_wave_dispatch_t<false>(p, a.g_dtype, a.w_dtype, c, grid, s);
-    }
     if (a.sparse)
         return rowonly_dispatch_t<true>(p, a.g_dtype, a.w_dtype, cp.m, spw, resident, grid, waves * kWave, s);
     return rowonly_dispatch_t<false>(p, a.g_dtype, a.w_dtype, cp.m, spw, resident, grid, waves * kWave, s);
@@ -1724,6 +1779,81 @@ hipError_t launch_apply_multi(const StepArgs* const* t, int n, hipStream_t s) {
                                        : apply_multi_dispatch<float, uint16_t>(g, m, grid, s);
             return a0.w_dtype == 0 ? apply_multi_dispatch<uint16_t, float>(g, m, grid, s)
                                    : apply_multi_dispatch<uint16_t, uint16_t>(g, m, grid, s);
+        });
+}
+
+
+// Row-only tables of ember_step_multi.
+
+namespace {
+
+template <typename GT, typename WT, bool kExact>
+hipError_t rowonly_wave_multi_c(const MultiParams<RowOnlyParams>& g, int c, dim3 grid, hipStream_t s) {
+    switch (c) {
+    case 1: ember_rowonly_wave_multi<GT, WT, 1, kExact><<<grid, kBlock, 0, s>>>(g); break;
+    case 2: ember_rowonly_wave_multi<GT, WT, 2, kExact><<<grid, kBlock, 0, s>>>(g); break;
+    case 4: ember_rowonly_wave_multi<GT, WT, 4, kExact><<<grid, kBlock, 0, s>>>(g); break;
+    case 8: ember_rowonly_wave_multi<GT, WT, 8, kExact><<<grid, kBlock, 0, s>>>(g); break;
+    case 16: ember_rowonly_wave_multi<GT, WT, 16, kExact><<<grid, kBlock, 0, s>>>(g); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+template <typename GT, typename WT>
+hipError_t rowonly_wave_multi_x(const MultiParams<RowOnlyParams>& g, int c, bool exact, dim3 grid, hipStream_t s) {
+    return exact ? rowonly_wave_multi_c<GT, WT, true>(g, c, grid, s) : rowonly_wave_multi_c<GT, WT, false>(g, c, grid, s);
+}
+
+bool rowonly_exact(const StepArgs& a) { return a.D % col_plan(a.D, a.g_dtype).epc == 0; }
+
+} // namespace
+
+int rowonly_key(const StepArgs& a) {
+    const int c = rowonly_wave_chunks(a);
+    if (c == 0) return -1;   // rows too long for the one-wave kernel: a launch of its own
+    int lc = 0;
+    while ((1 << lc) < c) ++lc;
+    return ((a.g_dtype * 2 + a.w_dtype) * 8 + lc) * 2 + (rowonly_exact(a) ? 1 : 0);
+}
+
+hipError_t launch_rowonly_multi(const StepArgs* const* t, int n, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    const StepArgs& a0 = *t[0];
+    const int c = rowonly_wave_chunks(a0);
+    if (c == 0) {
+        for (int k = 0; k < n; ++k) {
+            const hipError_t e = launch_rowonly(*t[k], s);
+            if (e != hipSuccess) return e;
+        }
+        return hipSuccess;
+    }
+    const bool exact = rowonly_exact(a0);
+    return launch_groups<RowOnlyParams>(
+        t, n, kBlock, rowonly_params,
+        [](const StepArgs& a) { return capped_blocks(rowonly_params(a).nvb); },
+        [&](const MultiParams<RowOnlyParams>& g, dim3 grid) {
+            if (a0.g_dtype == 0)
+                return a0.w_dtype == 0 ? rowonly_wave_multi_x<float, float>(g, c, exact, grid, s)
+                                       : rowonly_wave_multi_x<float, uint16_t>(g, c, exact, grid, s);
+            return a0.w_dtype == 0 ? rowonly_wave_multi_x<uint16_t, float>(g, c, exact, grid, s)
+                                   : rowonly_wave_multi_x<uint16_t, uint16_t>(g, c, exact, grid, s);
+        });
+}
+
+hipError_t launch_rowonly_validate_multi(const StepArgs* const* t, int n, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    return launch_groups<ValidateParams>(
+        t, n, kBlock,
+        [](const StepArgs& a) {
+            const WsLayout L = ws_layout(a.V, a.D);
+            return ValidateParams{a.idx, a.rows, a.n_dev, a.V, reinterpret_cast<int*>(a.ws + L.slot),
+                                  reinterpret_cast<int*>(a.ws + L.flag)};
+        },
+        [](const StepArgs& a) { return (int64_t)(a.rows > 0 ? (a.rows + kBlock - 1) / kBlock : 1); },
+        [&](const MultiParams<ValidateParams>& g, dim3 grid) {
+            ember_rowonly_validate_multi<<<grid, kBlock, 0, s>>>(g);
+            return hipGetLastError();
         });
 }
 

@@ -241,6 +241,12 @@ int apply_key(const StepArgs& a);
 hipError_t launch_stats_multi(const StepArgs* const* t, int n, hipStream_t s);
 hipError_t launch_finalize_multi(const StepArgs* const* t, int n, hipStream_t s);
 hipError_t launch_apply_multi(const StepArgs* const* t, int n, hipStream_t s);
+// Row-only tables: id validation of the sparse ones (one launch), then the
+// fused pass; rowonly_key is -1 for tables whose rows are too long for the
+// one-wave kernel (each of those gets a launch of its own).
+int rowonly_key(const StepArgs& a);
+hipError_t launch_rowonly_validate_multi(const StepArgs* const* t, int n, hipStream_t s);
+hipError_t launch_rowonly_multi(const StepArgs* const* t, int n, hipStream_t s);
 
 // LM-head weight gradient G = dY^T H with the statistics partials in the
 // epilogue (ember_lmhead.hip): rowpart[NT][V] and P[MT][D] in the workspace.

@@ -49,7 +49,8 @@ class TableStep(ctypes.Structure):
     """One table of ember_step_multi (the C struct ember_table_step)."""
     _fields_ = [("W", ctypes.c_void_p), ("w_dtype", ctypes.c_int), ("ldw", ctypes.c_int64),
                 ("G", ctypes.c_void_p), ("g_dtype", ctypes.c_int), ("ldg", ctypes.c_int64),
-                ("sparse", ctypes.c_int), ("idx", ctypes.c_void_p), ("n_idx", ctypes.c_int64),
+                ("sparse", ctypes.c_int), ("row_only", ctypes.c_int), ("idx", ctypes.c_void_p),
+                ("n_idx", ctypes.c_int64),
                 ("n_idx_dev", ctypes.c_void_p), ("r", ctypes.c_void_p), ("c", ctypes.c_void_p),
                 ("V", ctypes.c_int64), ("D", ctypes.c_int64), ("t", ctypes.c_int64),
                 ("lr", ctypes.c_float), ("beta2", ctypes.c_float), ("eps", ctypes.c_float),
@@ -307,14 +308,14 @@ def ember_lmhead_step(W: torch.Tensor, dY: torch.Tensor, H: torch.Tensor, G: tor
                                  ws.numel() * ws.element_size(), _stream(W)), "ember_lmhead_step")
 
 
-def table_step(W: torch.Tensor, G: torch.Tensor | None, r: torch.Tensor, c: torch.Tensor, t: int,
+def table_step(W: torch.Tensor, G: torch.Tensor | None, r: torch.Tensor, c: torch.Tensor | None, t: int,
                ws: torch.Tensor, idx: torch.Tensor | None = None, n_idx_dev: torch.Tensor | None = None,
                lr: float = 1e-3, beta2: float = 0.999, eps: float = 1e-8,
-               maximize: bool = False) -> TableStep:
+               maximize: bool = False, row_only: bool = False) -> TableStep:
     """One entry of ember_step_multi: a dense step when idx is None, else a
     sparse-row step on the rows idx lists (with n_idx_dev: the row count in
-    device memory, idx.numel() its maximum).  The tensors must stay alive until
-    the step has run."""
+    device memory, idx.numel() its maximum); row_only: the row-only step (c
+    unused).  The tensors must stay alive until the step has run."""
     V, D = W.shape
     sparse = idx is not None
     if sparse and idx.dtype != torch.int64:
@@ -322,7 +323,8 @@ def table_step(W: torch.Tensor, G: torch.Tensor | None, r: torch.Tensor, c: torc
     n = idx.numel() if sparse else 0
     ldg = _ld(G) if G is not None and G.numel() else D
     return TableStep(_ptr(W), _dtype(W), _ld(W), _ptr(G), _dtype(G) if G is not None else _dtype(W), ldg,
-                     int(sparse), _ptr(idx) if sparse else None, n, _ptr(n_idx_dev), _ptr(r), _ptr(c),
+                     int(sparse), int(bool(row_only)), _ptr(idx) if sparse else None, n, _ptr(n_idx_dev),
+                     _ptr(r), _ptr(c),
                      V, D, int(t), float(lr), float(beta2), float(eps), int(bool(maximize)), _ptr(ws),
                      ws.numel() * ws.element_size())
 
@@ -335,17 +337,16 @@ def ember_step_multi(steps, stream_of: torch.Tensor) -> None:
 
 
 def step_tables(items) -> None:
-    """Canonical Ember steps of several tables in one call.  items: tuples
-    (EmberTable, W, G) for a dense step or (EmberTable, W, G_rows, idx) for a
-    sparse-row step; every table advances t by one."""
+    """Ember steps of several tables in one call.  items: tuples (EmberTable,
+    W, G) for a dense step or (EmberTable, W, G_rows, idx) for a sparse-row
+    step; each table takes its canonical or row-only step; every table
+    advances t by one."""
     steps = []
     for it in items:
         tab, W, G = it[0], it[1], it[2]
         idx = it[3] if len(it) > 3 else None
-        if tab.row_only:
-            raise ValueError("ember_step_multi takes canonical (row and column) tables")
         steps.append(table_step(W, G, tab.r, tab.c, tab.t + 1, tab.ws, idx=idx, lr=tab.lr, beta2=tab.beta2,
-                                eps=tab.eps, maximize=tab.maximize))
+                                eps=tab.eps, maximize=tab.maximize, row_only=tab.row_only))
     ember_step_multi(steps, items[0][1])
     for it in items:
         it[0].t += 1

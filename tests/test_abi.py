@@ -333,6 +333,8 @@ def _multi(em, tables, n=None):
     (dict(sparse=1, idx=IDX_ + 16 * A + 4, n_idx=3), "ALIGN"),
     (dict(sparse=1, idx=IDX_ + 16 * A, n_idx=3, n_idx_dev=IDX_ + 16 * A + 4), "ALIGN"),
     (dict(sparse=1, idx=IDX_ + 16 * A, n_idx=-1, n_idx_dev=IDX_ + 17 * A), "SHAPE"),
+    (dict(row_only=2), "ARG"), (dict(row_only=1, r=None), "ARG"), (dict(row_only=1, ws_bytes=64), "WORKSPACE"),
+    (dict(row_only=1, sparse=1, idx=None, n_idx=3), "ARG"),
 ])
 def test_multi_step_checks_every_table(em, kw, status):
     # the first table is valid; the second fails its own call's check

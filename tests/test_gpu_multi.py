@@ -35,10 +35,10 @@ class Spec:
     """One table of a test: shape, dtypes, step kind and scalars."""
 
     def __init__(self, name, V, D, dtype, sparse=False, batch_tokens=0, lr=LR, beta2=B2, eps=EPS,
-                 maximize=False, empty=False):
+                 maximize=False, empty=False, row_only=False):
         grad = "sparse_zipf" if sparse else "zipf_rows"
         self.cfg = wl.Config(name, V, D, dtype, dtype, 3, grad, batch_tokens=batch_tokens)
-        self.sparse, self.empty = sparse, empty
+        self.sparse, self.empty, self.row_only = sparse, empty, row_only
         self.lr, self.beta2, self.eps, self.maximize = lr, beta2, eps, maximize
 
 
@@ -48,7 +48,7 @@ def _tables(em, spec, seed):
     out = []
     for _ in range(2):
         tab = em.EmberTable(spec.cfg.V, spec.cfg.D, device=DEV, lr=spec.lr, beta2=spec.beta2, eps=spec.eps,
-                            maximize=spec.maximize)
+                            maximize=spec.maximize, row_only=spec.row_only)
         out.append((tab, wl.make_weights(spec.cfg, seed=seed, device=DEV)))
     return out
 
@@ -89,7 +89,8 @@ def _run_against_single_calls(em, specs, steps, seed=0):
             what = f"{s.cfg.name} step {t}"
             assert _bits_equal(multi[1], single[1]), f"{what}: W differs from the single-table step"
             assert _bits_equal(multi[0].r, single[0].r), f"{what}: r differs"
-            assert _bits_equal(multi[0].c, single[0].c), f"{what}: c differs"
+            if not s.row_only:
+                assert _bits_equal(multi[0].c, single[0].c), f"{what}: c differs"
     return pairs
 
 
@@ -105,6 +106,29 @@ def test_mixed_tables_match_single_table_steps_bitwise(em):
         Spec("sparse_f32", 2000, 96, torch.float32, sparse=True, batch_tokens=512, eps=1e-6),
     ]
     _run_against_single_calls(em, specs, steps=3)
+
+
+def test_row_only_tables_match_single_table_steps_bitwise(em):
+    # row-only tables (Section 2.1) beside canonical ones: dense and sparse, bf16
+    # and fp32, shuffled ids, an empty sparse table, rows long enough for the
+    # block-per-row kernel (D = 16384 bf16: 2048 chunks)
+    specs = [
+        Spec("ro_dense_bf16", 3000, 1000, torch.bfloat16, row_only=True),
+        Spec("ro_sparse_bf16", 5000, 4096, torch.bfloat16, sparse=True, batch_tokens=2048, row_only=True),
+        Spec("canon_dense_bf16", 2000, 512, torch.bfloat16),
+        Spec("ro_sparse_f32_empty", 300, 64, torch.float32, sparse=True, empty=True, row_only=True),
+        Spec("ro_dense_f32", 700, 260, torch.float32, beta2=0.99, maximize=True, row_only=True),
+        Spec("ro_long_rows", 300, 16384, torch.bfloat16, sparse=True, batch_tokens=200, row_only=True),
+        Spec("canon_sparse_bf16", 4000, 1024, torch.bfloat16, sparse=True, batch_tokens=900),
+    ]
+    _run_against_single_calls(em, specs, steps=3, seed=7)
+
+
+def test_full_size_row_only_tables(em):
+    """The benchmarked pair as row-only tables, bitwise against single calls."""
+    specs = [Spec("ro_lmhead128k", 128256, 4096, torch.bfloat16, row_only=True),
+             Spec("ro_embed128k", 128256, 4096, torch.bfloat16, sparse=True, batch_tokens=8 * 2048, row_only=True)]
+    _run_against_single_calls(em, specs, steps=2, seed=9)
 
 
 def test_eight_tables_in_one_call(em):
