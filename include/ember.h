@@ -159,14 +159,16 @@ int ember_step_sparse_rows_devn(void* W, int w_dtype, int64_t ldw,
                                 void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
- * Several canonical Ember steps in one call: the tables of a model (for
- * example the LM head, dense, and the input embedding, sparse rows) each take
- * the step Algorithm 1 defines for them, exactly as the single-table entry
- * points above would, but the library enqueues three launches in all (one
- * statistics pass, one finalize pass, one apply pass over every table)
- * instead of three per table, so the tables share the chip and a small table
- * costs its bytes instead of its launch latency.  Each table's results are
- * the same bits as its own ember_step_dense or ember_step_sparse_rows call.
+ * Several Ember steps in one call: the tables of a model (for example the
+ * LM head, dense, and the input embedding, sparse rows) each take the step
+ * Algorithm 1 defines for them (or the row-only step of Section 2.1), exactly
+ * as the single-table entry points would, but the library enqueues three
+ * launches in all for the canonical tables (one statistics pass, one finalize
+ * pass, one apply pass over every table) instead of three per table, so the
+ * tables share the chip and a small table costs its bytes instead of its
+ * launch latency.  Each table's results are the same bits as its own
+ * single-table call (ember_step_dense, ember_step_sparse_rows(_devn), or the
+ * row-only entry points declared below).
  *
  * One ember_table_step per table:
  *   W, w_dtype, ldw, G, g_dtype, ldg, r, c, V, D, t, lr, beta2, eps,
