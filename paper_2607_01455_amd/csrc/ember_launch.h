@@ -34,7 +34,7 @@ constexpr int kWaves = kBlock / kWave;
                                     // EMBER_STATS_KEEP_MB of rows (reused by apply)
 #endif
 #ifndef EMBER_STATS_KEEP_MB
-#define EMBER_STATS_KEEP_MB 192
+#define EMBER_STATS_KEEP_MB 224
 #endif
 #ifndef EMBER_APPLY_NT
 #define EMBER_APPLY_NT 1            // non-temporal gradient loads and weight stores in apply
