@@ -365,3 +365,25 @@ def test_stream_probe_rejects_bad_arguments_on_host(em):
     assert P(1, W_, G_, None, 40, None) == em.EMBER_ERR_SHAPE
     assert P(1, W_ + 8, G_, None, 64, None) == em.EMBER_ERR_ALIGN
     assert P(2, W_, G_, R_ + 4, 64, None) == em.EMBER_ERR_ALIGN
+
+
+def test_table_step_struct_matches_the_header(em):
+    """The binding's TableStep has the fields of ember_table_step, in order and
+    with C types of the same size (a mismatch would hand the library wrong
+    pointers)."""
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    body = re.search(r"typedef struct \{(.*?)\}\s*ember_table_step;", text, re.S).group(1)
+    fields = re.findall(r"^\s*(.+?)\s*\b(\w+);", body, re.M)
+    sizes = {"void*": 8, "const void*": 8, "int": 4, "int64_t": 8, "const int64_t*": 8, "float*": 8,
+             "float": 4, "size_t": 8}
+    assert [name for _, name in fields] == [f[0] for f in em.TableStep._fields_]
+    for (ctype, name), (pname, ptype) in zip(fields, em.TableStep._fields_):
+        assert ctypes.sizeof(ptype) == sizes[ctype.replace(" *", "*")], (name, ctype, ptype)
+    # natural alignment, as the C compiler lays the struct out
+    off = 0
+    for (ctype, name), (pname, ptype) in zip(fields, em.TableStep._fields_):
+        sz = sizes[ctype.replace(" *", "*")]
+        off = (off + sz - 1) // sz * sz
+        assert getattr(em.TableStep, pname).offset == off, name
+        off += sz
+    assert ctypes.sizeof(em.TableStep) == (off + 7) // 8 * 8
