@@ -67,7 +67,12 @@ typedef enum {
     EMBER_ERR_INDEX = -6,     /* sparse step: idx holds a value outside [0, V) or a
                                  repeated value, or a device row count is out of
                                  range (reported by ember_get_error) */
-    EMBER_ERR_HIP = -7        /* a HIP runtime call failed */
+    EMBER_ERR_HIP = -7,       /* a HIP runtime call failed */
+    EMBER_ERR_DEVICE = -8     /* sparse step (reported by ember_get_error): the blocks of
+                                 the one-launch form did not all run at once, so a grid
+                                 barrier's bounded wait ran out; W, r and c are then
+                                 unspecified.  Not expected on an MI355X that the
+                                 calling process has to itself. */
 } ember_status;
 
 /* Largest supported V (row indices are kept in 31 bits) and D, and the

@@ -95,6 +95,11 @@ void set_scalars(StepArgs& a, float lr, float beta2, float eps, int64_t t, int m
 
 int run_step(StepArgs& a, float lr, float beta2, float eps, int64_t t, int maximize, hipStream_t s) {
     set_scalars(a, lr, beta2, eps, t, maximize);
+    // A sparse step whose rows fit on chip runs as one launch.
+    if (ember::onchip_fits(a)) {
+        const hipError_t e = timed("ember_sparse_onchip", s, [&] { return ember::launch_sparse_onchip(a, s); });
+        return e == hipSuccess ? EMBER_OK : EMBER_ERR_HIP;
+    }
     hipError_t e = timed("ember_stats", s, [&] { return ember::launch_stats(a, s); });
     if (e == hipSuccess) e = timed("ember_finalize", s, [&] { return ember::launch_finalize(a, s); });
     // lr == 0 leaves every weight bit unchanged, so the dense step skips the
@@ -113,6 +118,7 @@ void set_scalars(StepArgs& a, float lr, float beta2, float eps, int64_t t, int m
     const double alpha_s = maximize ? (double)lr : -(double)lr;
     a.inv_alpha = lr > 0.0f ? 1.0 / alpha_s : 0.0;
     a.eps_over_alpha = lr > 0.0f ? (float)((double)eps / alpha_s) : 0.0f;
+    a.spin_ticks = ember::kOnchipSpinTicks;
 }
 
 // LM-head step: the weight-gradient GEMM writes G and the statistics
@@ -394,29 +400,34 @@ int ember_step_multi(const ember_table_step* tables, int n_tables, hipStream_t s
     }
     std::vector<bool> row_only((size_t)n_tables);
     for (int i = 0; i < n_tables; ++i) row_only[(size_t)i] = tables[i].row_only != 0;
-    // Block order inside a launch: the statistics pass runs the sparse tables
-    // first, so that the dense tables' last rows, which the apply pass (rows
-    // high to low) reads first, are the ones left in the last-level cache; the
-    // apply pass runs the dense tables first.  A dense table with lr = 0 keeps
-    // every weight and has no apply blocks (a sparse one still clears its
-    // index-error flag there).
-    bool any_dense = false;
-    for (size_t i = 0; i < args.size(); ++i) any_dense = any_dense || (!row_only[i] && !args[i].sparse);
+    // Canonical sparse tables whose rows fit on chip take the one-launch step
+    // (the same kernel as their own call), before the shared launches: its
+    // ~116 MB of traffic would otherwise pass through the last-level cache
+    // between the dense tables' statistics and apply passes.
+    // The other canonical tables share a statistics, a finalize and an apply
+    // launch.  Statistics blocks: dense tables first (a sparse table's few
+    // blocks first would delay a whole round of the long dense blocks), then
+    // the sparse ones; the apply pass keeps that order, so the dense rows that
+    // the statistics pass read last (left in the last-level cache, read first
+    // by the apply pass going from high rows to low) come first.  A dense
+    // table with lr = 0 keeps every weight and has no apply blocks; a sparse
+    // one still clears its index-error flag there.
+    // Row-only tables: the sparse ones' id checks, then one fused pass.
+    std::vector<const StepArgs*> onchip, stats_order, apply_order, ro_sparse, ro_all;
     for (size_t i = 0; i < args.size(); ++i)
-        args[i].stats_stream = EMBER_MULTI_SPARSE_STREAM && !row_only[i] && args[i].sparse && any_dense;
-    // canonical tables: statistics, finalize and apply launches; row-only
-    // tables: the sparse ones' id checks, then one fused pass
-    std::vector<const StepArgs*> sparse_first, dense_first, ro_sparse, ro_all;
+        if (!row_only[i] && ember::onchip_fits(args[i])) onchip.push_back(&args[i]);
+    auto shared = [&](size_t i) {
+        if (row_only[i]) return false;
+        for (const StepArgs* o : onchip)
+            if (o == &args[i]) return false;
+        return true;
+    };
     for (size_t i = 0; i < args.size(); ++i)
-        if (!row_only[i] && args[i].sparse != (bool)EMBER_MULTI_DENSE_STATS_FIRST) sparse_first.push_back(&args[i]);
+        if (shared(i) && !args[i].sparse) stats_order.push_back(&args[i]);
     for (size_t i = 0; i < args.size(); ++i)
-        if (!row_only[i] && args[i].sparse == (bool)EMBER_MULTI_DENSE_STATS_FIRST) sparse_first.push_back(&args[i]);
-    for (size_t i = 0; i < args.size(); ++i)
-        if (!row_only[i] && EMBER_MULTI_SPARSE_APPLY_FIRST && args[i].sparse) dense_first.push_back(&args[i]);
-    for (size_t i = 0; i < args.size(); ++i)
-        if (!row_only[i] && !args[i].sparse && args[i].inv_alpha != 0.0) dense_first.push_back(&args[i]);
-    for (size_t i = 0; i < args.size(); ++i)
-        if (!row_only[i] && !EMBER_MULTI_SPARSE_APPLY_FIRST && args[i].sparse) dense_first.push_back(&args[i]);
+        if (shared(i) && args[i].sparse) stats_order.push_back(&args[i]);
+    for (const StepArgs* a : stats_order)
+        if (a->sparse || a->inv_alpha != 0.0) apply_order.push_back(a);
     for (size_t i = 0; i < args.size(); ++i) {
         if (!row_only[i]) continue;
         // a sparse table with no rows and a host count has no ids to check
@@ -424,22 +435,26 @@ int ember_step_multi(const ember_table_step* tables, int n_tables, hipStream_t s
         ro_all.push_back(&args[i]);
     }
     hipError_t e = hipSuccess;
-    if (!ro_sparse.empty())
+    for (const StepArgs* a : onchip) {
+        if (e == hipSuccess)
+            e = timed("ember_sparse_onchip", stream, [&] { return ember::launch_sparse_onchip(*a, stream); });
+    }
+    if (e == hipSuccess && !ro_sparse.empty())
         e = timed("ember_rowonly_validate_multi", stream, [&] {
             return run_phase(ro_sparse, [](const StepArgs&) { return 0; }, ember::launch_rowonly_validate_multi,
                              stream);
         });
-    if (e == hipSuccess && !sparse_first.empty())
+    if (e == hipSuccess && !stats_order.empty())
         e = timed("ember_stats_multi", stream, [&] {
-            return run_phase(sparse_first, ember::stats_key, ember::launch_stats_multi, stream);
+            return run_phase(stats_order, ember::stats_key, ember::launch_stats_multi, stream);
         });
-    if (e == hipSuccess && !sparse_first.empty())
+    if (e == hipSuccess && !stats_order.empty())
         e = timed("ember_finalize_multi", stream, [&] {
-            return run_phase(sparse_first, [](const StepArgs&) { return 0; }, ember::launch_finalize_multi, stream);
+            return run_phase(stats_order, [](const StepArgs&) { return 0; }, ember::launch_finalize_multi, stream);
         });
-    if (e == hipSuccess && !dense_first.empty())
+    if (e == hipSuccess && !apply_order.empty())
         e = timed("ember_apply_multi", stream, [&] {
-            return run_phase(dense_first, ember::apply_key, ember::launch_apply_multi, stream);
+            return run_phase(apply_order, ember::apply_key, ember::launch_apply_multi, stream);
         });
     if (e == hipSuccess && !ro_all.empty())
         e = timed("ember_rowonly_multi", stream, [&] {
@@ -625,7 +640,7 @@ int ember_get_error(const void* ws, hipStream_t stream, int* device_status) {
     const char* base = static_cast<const char*>(ws);
     if (hipMemcpy(&flag, base + ember::ws_layout(1, 1).status, sizeof flag, hipMemcpyDeviceToHost) != hipSuccess)
         return EMBER_ERR_HIP;
-    *device_status = flag != 0 ? EMBER_ERR_INDEX : EMBER_OK;
+    *device_status = (flag & ember::kFlagTimeout) ? EMBER_ERR_DEVICE : flag != 0 ? EMBER_ERR_INDEX : EMBER_OK;
     return EMBER_OK;
 }
 
@@ -639,6 +654,7 @@ const char* ember_strerror(int status) {
     case EMBER_ERR_WORKSPACE: return "workspace too small";
     case EMBER_ERR_INDEX: return "row index out of range or repeated";
     case EMBER_ERR_HIP: return "HIP runtime error";
+    case EMBER_ERR_DEVICE: return "device-side failure: the blocks of the one-launch sparse step were not all resident";
     default: return "unknown status";
     }
 }

@@ -23,6 +23,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+#include <mutex>
+
 #include "ember_launch.h"
 
 namespace ember {
@@ -664,7 +667,7 @@ struct FinLds {
 template <bool kSparse>
 __device__ __forceinline__ void finalize_block(const FinParams& a, int blk, int nblocks, FinLds& sh) {
     const int err = kSparse ? *a.flag : 0;
-    if (blk == 0 && threadIdx.x == 0) *a.status = err;
+    if (blk == 0 && threadIdx.x == 0) *a.status = err | (*a.status & kFlagTimeout);
     finalize_body<kSparse>(a, blk, err, sh.part, sh.lds16);
 
     // The block that finishes last derives the step scale from the per-block
@@ -795,7 +798,7 @@ __device__ __forceinline__ void apply_block(const ApplyParams& a, unsigned blk, 
     const int wave = threadIdx.x / kWave;
     if (kSparse) {
         if (blk == 0 && threadIdx.x == 0) *a.flag = 0;
-        if (*a.status != 0) return;
+        if ((*a.status & ~kFlagTimeout) != 0) return;
     }
     if (a.inv_alpha == 0.0) return;   // lr == 0: every weight keeps its bits
     bool bad_count = false;
@@ -1236,13 +1239,13 @@ __device__ __forceinline__ void rowonly_wave_block(const RowOnlyParams& a, unsig
                                                    bool sparse_rt = false) {
     const bool kSparse = kRuntime ? sparse_rt : kSparseArg;
     if (!kSparse) {
-        if (blk == 0 && threadIdx.x == 0) *a.status = 0;
+        if (blk == 0 && threadIdx.x == 0) *a.status &= kFlagTimeout;
         for (int64_t vb = blk; vb < a.nb; vb += nblk)
             rowonly_wave_rows<GT, WT, C, false, kExact, kRuntime>(a, a.rows, vb, false);
         return;
     }
     const int err = *a.flag;
-    if (blk == 0 && threadIdx.x == 0) *a.status = err;
+    if (blk == 0 && threadIdx.x == 0) *a.status = err | (*a.status & kFlagTimeout);
     bool bad_count = false;
     const int64_t nrows = active_rows(a.n_dev, a.rows, bad_count);
     for (int64_t vb = blk; vb < a.nvb; vb += nblk) {
@@ -1274,13 +1277,13 @@ __global__ __launch_bounds__(kRowOnlyMaxWaves * kWave) void ember_rowonly(RowOnl
     __shared__ float rn_lds[kRowOnlyRows];
     __shared__ int last;
     if (!kSparse) {
-        if (blockIdx.x == 0 && threadIdx.x == 0) *a.status = 0;
+        if (blockIdx.x == 0 && threadIdx.x == 0) *a.status &= kFlagTimeout;
         for (int64_t vb = blockIdx.x; vb < a.nb; vb += gridDim.x)
             rowonly_rows<GT, WT, M, S, false, kResident>(a, a.rows, vb, part, rn_lds);
         return;
     }
     const int err = *a.flag;
-    if (blockIdx.x == 0 && threadIdx.x == 0) *a.status = err;
+    if (blockIdx.x == 0 && threadIdx.x == 0) *a.status = err | (*a.status & kFlagTimeout);
     bool bad_count = false;
     const int64_t nrows = active_rows(a.n_dev, a.rows, bad_count);
     for (int64_t vb = blockIdx.x; vb < a.nvb; vb += gridDim.x) {
@@ -1329,6 +1332,462 @@ __global__ __launch_bounds__(kBlock) void ember_rowonly_validate(const int64_t* 
 __global__ __launch_bounds__(kBlock) void ember_rowonly_validate_multi(MultiParams<ValidateParams> g) {
     const int k = multi_table(g.first, g.ntab);
     rowonly_validate_block(g.p[k], blockIdx.x - g.first[k]);
+}
+
+// ---------------------------------------------------------------------------
+// sparse-row step in one launch: the rows stay on chip
+// ---------------------------------------------------------------------------
+//
+// A sparse step touches few rows (an embedding batch of 16384 tokens has
+// ~4700 distinct ids: 38 MB of bf16 gradient at D = 4096), far less than the
+// register files of the chip's 256 compute units (512 KB each).  One block
+// per compute unit loads its share of the gradient rows, and of the weight
+// rows they update, into registers once; two grid barriers separate
+//   1. the slab sums of g^2 of each row (-> mean g^2 per row), the block's
+//      column sums of g^2, and the id checks (slot marks);
+//   2. the column reduction with the c update and the column factors, and r
+//      of every row (decay, or update from the row's mean), with per-block
+//      sums of the new r and c;
+//   3. s and the step scale from the per-block sums, then the update of the
+//      weight rows held since phase 1.
+// G is read once (the three-launch path reads it twice), and no launch ramp
+// or tail separates the phases.  Wave w of a block takes column slab
+// w % nslab of the block's rows r0 + w / nslab + Q u (u < U, Q = 8 / nslab).
+// Values one block hands to another inside the launch are stored and loaded
+// at agent scope (coherent across the XCDs' L2 caches); the grid barriers'
+// waits are bounded and report kFlagTimeout when they run out.
+
+constexpr int kOnchipWaves = kOnchipThreads / kWave;   // 8: two per SIMD
+constexpr int kAgentScopeLoad = 16;                     // sc1: buffer loads at agent scope
+constexpr int kColGroups = kOnchipThreads / 16;         // phase 2: 16 columns x 32 partial groups
+
+struct OnchipParams {
+    void* W;
+    int64_t ldw;
+    const void* G;
+    int64_t ldg;
+    const int64_t* idx;
+    const int64_t* n_dev;   // device row count, or null
+    int64_t rows;           // row count (host), or the maximum of the device count
+    int64_t V;
+    int64_t D;
+    int total_chunks;
+    int slab_chunks;
+    int nslab;              // at most kOnchipWaves
+    int q_lanes;            // kOnchipWaves / nslab: waves per slab
+    float* r;
+    float* c;
+    float beta2;
+    float one_minus_beta2;
+    double inv_bias;
+    double inv_alpha;       // 0 when lr == 0 (no weight is read or written)
+    float eps_over_alpha;
+    int* slot;              // [V]: 1 + position in idx of a touched row, else 0
+    int* flag;              // error bits of this step
+    int* status;            // error bits of the last step (ember_get_error)
+    unsigned* epoch;        // launches of this step so far (numbers the barriers)
+    unsigned* arrive;       // [kOnchipBlocks * kArriveStride]: each block's last barrier number
+    float* P;               // [kOnchipBlocks][D]: per-block column sums of g^2
+    double* parts;          // [3][kOnchipBlocks]: per-block sums of the new r (untouched,
+                            // touched rows) and of the new c
+    float* qa;              // [D rounded up to 8]: column factors sqrt(c_j)
+    int64_t spin_ticks;     // bound of a barrier wait in real-time counter ticks
+};
+
+__device__ __forceinline__ int ld_agent_i(const int* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ unsigned ld_agent_u(const unsigned* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ double ld_agent_d(const double* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_agent_u(unsigned* p, unsigned v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_agent_d(double* p, double v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Grid barrier number `gen` of the one-launch step: every wave waits until
+// its own memory operations have completed, one thread publishes the block's
+// arrival in its own flag (no shared counter: 256 atomics on one address
+// serialize), and 256 threads poll one flag each until every block has
+// arrived, with a bounded wait on the real-time counter.  Flag values only
+// grow (two barriers per launch, numbered from the step's epoch), so no flag
+// is ever reset.  Returns false when a wait ran out, and records that in the
+// step's error bits and in the status word (where it stays until
+// ember_init_state: the state is then unspecified).
+__device__ bool grid_barrier(unsigned* arrive, unsigned gen, int64_t spin_ticks, int* flag, int* status,
+                             int* lds_ok) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        st_agent_u(arrive + (size_t)blockIdx.x * kArriveStride, gen);
+        *lds_ok = 1;
+    }
+    __syncthreads();
+    if (threadIdx.x < kOnchipBlocks) {
+        const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+        while ((int)(ld_agent_u(arrive + (size_t)threadIdx.x * kArriveStride) - gen) < 0) {
+            if ((int64_t)(__builtin_amdgcn_s_memrealtime() - t0) > spin_ticks) {
+                *lds_ok = 0;
+                atomicOr(flag, kFlagTimeout);
+                atomicOr(status, kFlagTimeout);
+                break;
+            }
+        }
+    }
+    __syncthreads();
+    return *lds_ok != 0;
+}
+
+// Gradient and weight rows held per wave (u < U): a unit takes two chunks of
+// G and two of W per lane (4 registers per 16-byte chunk, 8 for the 32 bytes
+// of fp32 W next to a bf16 chunk of G); U keeps them within ~160 of the 256
+// registers a wave has at two waves per SIMD.
+template <typename GT, typename WT>
+constexpr int onchip_units() {
+    constexpr int words = 2 * (4 + (16 / (int)sizeof(GT)) * (int)sizeof(WT) / 4);
+    return 160 / words < 10 ? 160 / words : 10;
+}
+
+// Sum of one double per thread of the block: waves, then waves in order.
+__device__ __forceinline__ double onchip_block_sum(double v, double* lds8) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    v = wave_sum(v);
+    if (lane == 0) lds8[wave] = v;
+    __syncthreads();
+    double t = 0.0;
+#pragma unroll
+    for (int w = 0; w < kOnchipWaves; ++w) t += lds8[w];
+    __syncthreads();
+    return t;
+}
+
+template <typename GT, typename WT, int M, int U>
+__global__ __launch_bounds__(kOnchipThreads, 1) void ember_sparse_onchip(OnchipParams a) {
+    constexpr int EPC = 16 / (int)sizeof(GT);
+    constexpr int NB = kOnchipBlocks;
+    constexpr int kRowsMax = kOnchipWaves * U;        // rows of a block at most
+    __shared__ float cl[kOnchipWaves][kWave * EPC];   // the waves' column sums, one chunk column
+    __shared__ float rsl2[kRowsMax];                  // slab sums of g^2 of the block's rows
+    __shared__ int64_t id_lds[kRowsMax];              // ids of the block's rows
+    __shared__ float ro_lds[kRowsMax];                // r of those rows before the step
+    __shared__ float rn_lds[kRowsMax];                // r of those rows after the step
+    __shared__ float part[kColGroups][16];            // column reduction
+    __shared__ double dsum[kOnchipWaves];
+    __shared__ int sh_ok, sh_err;
+    __shared__ float sh_scale;
+    __shared__ unsigned sh_epoch;
+
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int b = blockIdx.x;
+    const int64_t V = a.V, D = a.D;
+    if (threadIdx.x == 0) sh_epoch = *a.epoch;
+
+    // ---- phase 1: load the rows, row and column sums of g^2, id checks ----
+    bool bad_count = false;
+    const int64_t n = active_rows(a.n_dev, a.rows, bad_count);
+    if (bad_count && b == 0 && threadIdx.x == 0) atomicOr(a.flag, kFlagCount);
+    int64_t r0, r1;
+    row_range(n, NB, b, r0, r1);
+    const int nloc = (int)(r1 - r0);
+    const int Q = a.q_lanes;
+    const int slab = wave % a.nslab;
+    const int q = wave / a.nslab;
+    const bool on = q < Q;
+    const int cbeg = slab * a.slab_chunks;
+    const int cend = min(cbeg + a.slab_chunks, a.total_chunks);
+    const bool write_w = a.inv_alpha != 0.0;
+    const GT* G = static_cast<const GT*>(a.G);
+    WT* W = static_cast<WT*>(a.W);
+
+    // Rows go through raw buffer resources (base = the row, length = its bytes,
+    // 0 for an absent row): loads past the length return zero and stores past
+    // it are dropped.  Lanes whose chunk lies outside the wave's slab get an
+    // offset past every length.  Weight rows are only addressed through ids
+    // inside [0, V); every store further waits for the id checks of the step.
+    constexpr int kWChunkBytes = EPC * (int)sizeof(WT);
+    constexpr int kOutside = 1 << 30;   // past the length of every row on this path
+    int goff[M], woff[M];
+#pragma unroll
+    for (int m = 0; m < M; ++m) {
+        const int ch = cbeg + lane + kWave * m;
+        goff[m] = (on && ch < cend) ? ch * 16 : kOutside;
+        woff[m] = (on && ch < cend) ? ch * kWChunkBytes : kOutside;
+    }
+    const int gbytes = (int)D * (int)sizeof(GT);
+    const int wbytes = (int)D * (int)sizeof(WT);
+    // lane u holds the id of unit u: one load for all units, issued first
+    const int64_t lrow = r0 + q + (int64_t)Q * lane;
+    const bool lrv = on && lane < U && lrow < r1;
+    const int64_t lid = lrv ? a.idx[lrow] : -1;
+    const bool lin = lrv && lid >= 0 && lid < V;
+    bool rv[U], wv[U];
+    __amdgpu_buffer_rsrc_t wb[U];
+    Raw<GT, EPC> graw[U][M];
+    Raw<WT, EPC> wraw[U][M];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int64_t row = r0 + q + (int64_t)Q * u;
+        rv[u] = on && row < r1;
+        const __amdgpu_buffer_rsrc_t gb = row_buffer(G + (rv[u] ? row : 0) * a.ldg, rv[u] ? gbytes : 0);
+#pragma unroll
+        for (int m = 0; m < M; ++m) buf_load<GT, EPC>(gb, goff[m], graw[u][m]);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int64_t i = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(lid >> 32), u) << 32) |
+                                    (uint32_t)__builtin_amdgcn_readlane((int)lid, u));
+        wv[u] = rv[u] && i >= 0 && i < V;
+        wb[u] = row_buffer(W + (wv[u] ? i : 0) * a.ldw, wv[u] && write_w ? wbytes : 0);
+#pragma unroll
+        for (int m = 0; m < M; ++m) buf_load<WT, EPC>(wb[u], woff[m], wraw[u][m]);
+    }
+    // id checks: lane u of each slab-0 wave marks the row of unit u and reads
+    // its r; the result of the mark is looked at after the sums (waiting for it
+    // waits for every load issued before it)
+    int mark_bits = 0;
+    int prev_mark = 0;
+    float rold = 0.0f;
+    if (slab == 0 && lrv) {
+        if (!lin) {
+            mark_bits = kFlagRange;
+        } else {
+            prev_mark = atomicCAS(&a.slot[lid], 0, (int)(lrow + 1));
+            rold = a.r[lid];
+        }
+    }
+    // every load is issued before the first wait, and no decode moves above them
+    __builtin_amdgcn_sched_barrier(0);
+
+    float acc[M][EPC];
+#pragma unroll
+    for (int m = 0; m < M; ++m)
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) acc[m][e] = 0.0f;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        float s0 = 0.0f, s1 = 0.0f;
+#pragma unroll
+        for (int m = 0; m < M; ++m) {
+            float x[EPC];
+            decode(graw[u][m], x);
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) {
+                acc[m][e] = fmaf(x[e], x[e], acc[m][e]);
+                if (e & 1) s1 = fmaf(x[e], x[e], s1);
+                else s0 = fmaf(x[e], x[e], s0);
+            }
+        }
+        const float ss = wave_sum(s0 + s1);
+        if (lane == 0 && rv[u]) rsl2[(q + Q * u) * a.nslab + slab] = ss;
+        // The column sums are complete for this unit here (the compiler would
+        // otherwise defer the additions and keep every decoded value live), and
+        // phase 3 decodes the raw words again.
+#pragma unroll
+        for (int m = 0; m < M; ++m) {
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) asm volatile("" : "+v"(acc[m][e]));
+            launder(graw[u][m]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    if (prev_mark != 0) mark_bits |= kFlagDuplicate;
+    if (mark_bits) atomicOr(a.flag, mark_bits);
+    if (slab == 0 && lrv) {
+        const int t = q + Q * lane;
+        id_lds[t] = lin ? lid : -1;
+        ro_lds[t] = rold;
+    }
+
+    // column sums of the block: the Q waves of each slab in order -> P[b]
+    float* Pb = a.P + (int64_t)b * D;
+#pragma unroll
+    for (int m = 0; m < M; ++m) {
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) cl[wave][lane * EPC + e] = acc[m][e];
+        __syncthreads();
+        for (int x = threadIdx.x; x < a.nslab * kWave * EPC; x += kOnchipThreads) {
+            const int s = x / (kWave * EPC);
+            const int off = x - s * (kWave * EPC);
+            const int ch = s * a.slab_chunks + kWave * m + off / EPC;
+            const int send = min((s + 1) * a.slab_chunks, a.total_chunks);
+            if (ch < send) {
+                float v = cl[s][off];
+                for (int qq = 1; qq < Q; ++qq) v += cl[qq * a.nslab + s][off];
+                st_agent(Pb + (int64_t)ch * EPC + off % EPC, v);
+            }
+        }
+        __syncthreads();
+    }
+    // the block's rows: mean g^2 from the slab sums (slab order, float64),
+    // the new r, and the sum of the new r in row order
+    double tsum = 0.0;
+    {
+        const double invD = 1.0 / (double)D;
+        float rn = 0.0f;
+        if (threadIdx.x < nloc) {
+            double sum = 0.0;
+            for (int sb = 0; sb < a.nslab; ++sb) sum += (double)rsl2[threadIdx.x * a.nslab + sb];
+            const float mean = (float)(sum * invD);
+            rn = fmaf(a.beta2, ro_lds[threadIdx.x], a.one_minus_beta2 * mean);
+            rn_lds[threadIdx.x] = rn;
+        }
+        tsum = onchip_block_sum((double)rn, dsum);
+    }
+
+    const unsigned gen = 2u * sh_epoch + 1u;
+    const bool ok1 = grid_barrier(a.arrive, gen, a.spin_ticks, a.flag, a.status, &sh_ok);
+
+    // ---- phase 2: c and the column factors; r of every row ----
+    if (threadIdx.x == 0) sh_err = ld_agent_i(a.flag) | (ok1 ? 0 : kFlagTimeout);
+    __syncthreads();
+    const int err = sh_err;
+    double csum = 0.0;
+    {
+        // columns [c0, c1) in groups of 16: thread (g, x) adds the partials
+        // g, g + 32, ... of its column in that order, then the 32 group sums
+        // in group order
+        const int64_t c0 = D * b / NB, c1 = D * (b + 1) / NB;
+        const int x = threadIdx.x % 16, g = threadIdx.x / 16;
+        const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(a.P, 0, (int)(NB * D * 4), kBufferWord3);
+        const int prow = kColGroups * (int)D * 4;
+        for (int64_t j0 = c0; j0 < c1; j0 += 16) {
+            const int64_t j = j0 + x;
+            const bool jv = j < c1;
+            float s = 0.0f;
+            const int vo = jv ? (g * (int)D + (int)j) * 4 : kOutside;
+#pragma unroll
+            for (int k = 0; k < NB / kColGroups; ++k)
+                s += __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(prs, vo, k * prow, kAgentScopeLoad));
+            part[g][x] = s;
+            __syncthreads();
+            if (threadIdx.x < 16) {
+                float cn = 0.0f;
+                if (jv) {
+                    float colsum = 0.0f;
+                    for (int w = 0; w < kColGroups; ++w) colsum += part[w][x];
+                    const float mean = (float)((double)colsum / (double)V);
+                    cn = fmaf(a.beta2, a.c[j], a.one_minus_beta2 * mean);
+                    if (!err) {
+                        a.c[j] = cn;
+                        st_agent(a.qa + j, sqrtf(cn));
+                    }
+                }
+                csum += (double)cn;
+            }
+            __syncthreads();
+        }
+    }
+    double usum = 0.0;
+    {
+        // rows [v0, v1): untouched rows decay; touched rows take the value
+        // their gradient row's block computed; marks are cleared
+        const int64_t v0 = V * b / NB, v1 = V * (b + 1) / NB;
+        for (int64_t i = v0 + threadIdx.x; i < v1; i += kOnchipThreads) {
+            const int sl = ld_agent_i(a.slot + i);
+            const float ri = a.r[i];
+            if (sl != 0) {
+                a.slot[i] = 0;
+            } else if (!err) {
+                const float rn = a.beta2 * ri;
+                a.r[i] = rn;
+                usum += (double)rn;
+            }
+        }
+        if (!err && threadIdx.x < nloc && id_lds[threadIdx.x] >= 0) a.r[id_lds[threadIdx.x]] = rn_lds[threadIdx.x];
+    }
+    usum = onchip_block_sum(usum, dsum);
+    if (threadIdx.x < kWave) csum = wave_sum(csum);
+    if (threadIdx.x == 0) {
+        st_agent_d(a.parts + b, usum);
+        st_agent_d(a.parts + NB + b, tsum);
+        st_agent_d(a.parts + 2 * NB + b, csum);
+    }
+
+    const bool ok2 = grid_barrier(a.arrive, gen + 1u, a.spin_ticks, a.flag, a.status, &sh_ok);
+    // every block has read the error bits: block 0 records them (keeping a
+    // timeout bit), clears them for the next step and numbers the next
+    // step's barriers
+    if (b == 0 && threadIdx.x == 0) {
+        atomicAnd(a.status, kFlagTimeout);
+        atomicOr(a.status, err);
+        *a.flag = 0;
+        *a.epoch = sh_epoch + 1u;
+    }
+
+    // ---- phase 3: s, then the update of the held weight rows ----
+    if (!err && ok2 && write_w) {
+        // column factors of this lane's chunks, and the per-block sums, in one
+        // round trip
+        const __amdgpu_buffer_rsrc_t qrs = __builtin_amdgcn_make_buffer_rsrc(a.qa, 0, (int)((D + 7) / 8 * 8 * 4),
+                                                                             kBufferWord3);
+        u32x4 qraw[M][EPC / 4];
+#pragma unroll
+        for (int m = 0; m < M; ++m) {
+            const int ch = cbeg + lane + kWave * m;
+            const int qoff = (on && ch < cend) ? ch * EPC * 4 : kOutside;
+#pragma unroll
+            for (int k = 0; k < EPC / 4; ++k)
+                qraw[m][k] = __builtin_bit_cast(
+                    u32x4, __builtin_amdgcn_raw_buffer_load_b128(qrs, qoff + 16 * k, 0, kAgentScopeLoad));
+        }
+        // s from the per-block sums in a fixed order (every block alike)
+        double sr = 0.0, sc = 0.0;
+        if (threadIdx.x < NB) {
+            sr = ld_agent_d(a.parts + threadIdx.x) + ld_agent_d(a.parts + NB + threadIdx.x);
+            sc = ld_agent_d(a.parts + 2 * NB + threadIdx.x);
+        }
+        sr = onchip_block_sum(sr, dsum);
+        sc = onchip_block_sum(sc, dsum);
+        if (threadIdx.x == 0) {
+            const double mean_rhat = sr / (double)V * a.inv_bias;
+            const double mean_chat = sc / (double)D * a.inv_bias;
+            const double s = sqrt(mean_rhat * mean_chat);
+            sh_scale = s > 0.0 ? (float)(sqrt(a.inv_bias / s) * a.inv_alpha) : 0.0f;
+        }
+        __syncthreads();
+        const float scale = sh_scale;
+        const float epsa = a.eps_over_alpha;
+        const float ibias = (float)a.inv_bias;
+        float qv[M][EPC];
+#pragma unroll
+        for (int m = 0; m < M; ++m)
+#pragma unroll
+            for (int k = 0; k < EPC / 4; ++k) {
+                qv[m][4 * k] = __uint_as_float(qraw[m][k].x);
+                qv[m][4 * k + 1] = __uint_as_float(qraw[m][k].y);
+                qv[m][4 * k + 2] = __uint_as_float(qraw[m][k].z);
+                qv[m][4 * k + 3] = __uint_as_float(qraw[m][k].w);
+            }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (!wv[u]) continue;
+            const float ai = sqrtf(rn_lds[q + Q * u] * ibias) * scale;
+#pragma unroll
+            for (int m = 0; m < M; ++m) {
+                // the words are decoded here and nowhere earlier
+                launder(graw[u][m]);
+                launder(wraw[u][m]);
+                float gx[EPC], wx[EPC], o[EPC];
+                decode(graw[u][m], gx);
+                decode(wraw[u][m], wx);
+#pragma unroll
+                for (int e = 0; e < EPC; ++e) {
+                    const float d = fmaf(ai, qv[m][e], epsa);
+                    const float upd = fmaf(gx[e], __builtin_amdgcn_rcpf(d), wx[e]);
+                    o[e] = (gx[e] == 0.0f) ? wx[e] : upd;
+                }
+                buf_store<WT, EPC>(wb[u], woff[m], o);
+            }
+            __builtin_amdgcn_sched_barrier(0);   // one unit's decoded values at a time
+        }
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -1450,13 +1909,17 @@ WsLayout ws_layout(int64_t V, int64_t D) {
     int nb = row_blocks(V, col_plan(D, 1).nslab);
     if (row_blocks(V, col_plan(D, 0).nslab) > nb) nb = row_blocks(V, col_plan(D, 0).nslab);
     if (lp.MT > nb) nb = lp.MT;
+    if (kOnchipBlocks > nb) nb = kOnchipBlocks;
     const int nslab = nslab_for(D) > lp.NT ? nslab_for(D) : lp.NT;
     size_t off = 0;
     L.flag = off;
     L.status = off + 4;
     L.ticket = off + 8;
     L.scale = off + 12;
-    off = align256(12);
+    L.epoch = off + 16;
+    off = align256(20);
+    L.arrive = off;
+    off = align256(off + (size_t)kOnchipBlocks * kArriveStride * 4);
     L.slot = off;
     off = align256(off + (size_t)V * 4);
     L.zero_end = off;
@@ -1470,6 +1933,8 @@ WsLayout ws_layout(int64_t V, int64_t D) {
     off = align256(off + (size_t)((D + kFinCols - 1) / kFinCols) * 4);
     L.p = off;
     off = align256(off + (size_t)nb * (size_t)D * 4);
+    L.parts = off;
+    off = align256(off + (size_t)3 * kOnchipBlocks * 8);
     L.total = off;
     return L;
 }
@@ -1499,7 +1964,7 @@ static StatsParams stats_params(const StepArgs& a) {
         const double row_bytes = (double)a.D * (a.g_dtype == 0 ? 4 : 2);
         const int64_t keep = (int64_t)((double)EMBER_STATS_KEEP_MB * 1048576.0 / row_bytes);
         p.cached_from = EMBER_STATS_NT == 0 ? 0
-                      : (EMBER_STATS_NT == 1 || a.stats_stream) ? a.rows
+                      : EMBER_STATS_NT == 1 ? a.rows
                       : (keep >= a.rows ? 0 : a.rows - keep);
     }
     p.rowpart = reinterpret_cast<float*>(a.ws + L.rowpart);
@@ -1603,6 +2068,106 @@ hipError_t launch_apply(const StepArgs& a, hipStream_t s) {
                       : apply_dispatch_w<float, false>(p, a.w_dtype, cp.m, grid, s);
     return sparse ? apply_dispatch_w<uint16_t, true>(p, a.w_dtype, cp.m, grid, s)
                   : apply_dispatch_w<uint16_t, false>(p, a.w_dtype, cp.m, grid, s);
+}
+
+// ---------------------------------------------------------------------------
+// sparse-row step in one launch
+// ---------------------------------------------------------------------------
+
+namespace {
+
+template <typename GT, typename WT>
+const void* onchip_kernel_m(int m) {
+    if (m == 1) return reinterpret_cast<const void*>(&ember_sparse_onchip<GT, WT, 1, onchip_units<GT, WT>()>);
+    return reinterpret_cast<const void*>(&ember_sparse_onchip<GT, WT, 2, onchip_units<GT, WT>()>);
+}
+
+const void* onchip_kernel(int g_dtype, int w_dtype, int m) {
+    if (g_dtype == 0) return w_dtype == 0 ? onchip_kernel_m<float, float>(m) : onchip_kernel_m<float, uint16_t>(m);
+    return w_dtype == 0 ? onchip_kernel_m<uint16_t, float>(m) : onchip_kernel_m<uint16_t, uint16_t>(m);
+}
+
+int onchip_units_for(int g_dtype, int w_dtype) {
+    if (g_dtype == 0) return w_dtype == 0 ? onchip_units<float, float>() : onchip_units<float, uint16_t>();
+    return w_dtype == 0 ? onchip_units<uint16_t, float>() : onchip_units<uint16_t, uint16_t>();
+}
+
+// Whether every block of the launch can be resident at once on the current
+// device: kOnchipBlocks blocks against compute units x blocks per unit of
+// this kernel instance (checked once per device and instance).
+bool onchip_resident(int g_dtype, int w_dtype, int m) {
+    constexpr int kMaxDevices = 64;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return false;
+    const int key = (g_dtype * 2 + w_dtype) * 2 + (m - 1);
+    static std::mutex mu;
+    static signed char known[kMaxDevices][8];
+    std::lock_guard<std::mutex> lock(mu);
+    signed char& k = known[dev][key];
+    if (k == 0) {
+        int cus = 0, per_cu = 0;
+        const bool ok =
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, onchip_kernel(g_dtype, w_dtype, m),
+                                                         kOnchipThreads, 0) == hipSuccess &&
+            (int64_t)cus * per_cu >= kOnchipBlocks;
+        k = ok ? 1 : -1;
+    }
+    return k > 0;
+}
+
+} // namespace
+
+bool onchip_fits(const StepArgs& a) {
+    if (!a.sparse || a.c == nullptr) return false;
+    const ColPlan cp = col_plan(a.D, a.g_dtype);
+    // whole 16-byte chunks only (rows are read through buffer resources)
+    if (cp.nslab > kOnchipWaves || a.D % cp.epc != 0) return false;
+    const int64_t per_block = (a.rows + kOnchipBlocks - 1) / kOnchipBlocks;
+    if (per_block > (int64_t)(kOnchipWaves / cp.nslab) * onchip_units_for(a.g_dtype, a.w_dtype)) return false;
+    return onchip_resident(a.g_dtype, a.w_dtype, cp.m);
+}
+
+hipError_t launch_sparse_onchip(const StepArgs& a, hipStream_t s) {
+    const WsLayout L = ws_layout(a.V, a.D);
+    const ColPlan cp = col_plan(a.D, a.g_dtype);
+    OnchipParams p;
+    p.W = a.W;
+    p.ldw = a.ldw;
+    p.G = a.G;
+    p.ldg = a.ldg;
+    p.idx = a.idx;
+    p.n_dev = a.n_dev;
+    p.rows = a.rows;
+    p.V = a.V;
+    p.D = a.D;
+    p.total_chunks = cp.total_chunks;
+    p.slab_chunks = cp.slab_chunks;
+    p.nslab = cp.nslab;
+    p.q_lanes = kOnchipWaves / cp.nslab;
+    p.r = a.r;
+    p.c = a.c;
+    p.beta2 = a.beta2;
+    p.one_minus_beta2 = a.one_minus_beta2;
+    p.inv_bias = a.inv_bias;
+    p.inv_alpha = a.inv_alpha;
+    p.eps_over_alpha = a.eps_over_alpha;
+    p.slot = reinterpret_cast<int*>(a.ws + L.slot);
+    p.flag = reinterpret_cast<int*>(a.ws + L.flag);
+    p.status = reinterpret_cast<int*>(a.ws + L.status);
+    p.epoch = reinterpret_cast<unsigned*>(a.ws + L.epoch);
+    p.arrive = reinterpret_cast<unsigned*>(a.ws + L.arrive);
+    p.P = reinterpret_cast<float*>(a.ws + L.p);
+    p.parts = reinterpret_cast<double*>(a.ws + L.parts);
+    p.qa = reinterpret_cast<float*>(a.ws + L.qa);
+    p.spin_ticks = a.spin_ticks;
+    // A plain launch: the residency check above (blocks per compute unit x
+    // compute units >= kOnchipBlocks) is what the grid barriers rely on, and
+    // their bounded waits turn a violation into EMBER_ERR_DEVICE instead of a
+    // hang.  (hipLaunchCooperativeKernel measured ~17 us slower per step here.)
+    void* args[] = {&p};
+    return hipLaunchKernel(onchip_kernel(a.g_dtype, a.w_dtype, cp.m), dim3(kOnchipBlocks), dim3(kOnchipThreads), args,
+                           0, s);
 }
 
 hipError_t launch_rowonly_validate(const StepArgs& a, hipStream_t s) {

@@ -95,16 +95,6 @@ constexpr int kWaves = kBlock / kWave;
 #ifndef EMBER_LMHEAD_GROUP_M
 #define EMBER_LMHEAD_GROUP_M 2   // LM-head gradient GEMM: row tiles per group of the tile order
 #endif
-#ifndef EMBER_MULTI_DENSE_STATS_FIRST
-#define EMBER_MULTI_DENSE_STATS_FIRST 1  // multi-table statistics launch: dense tables' blocks first
-#endif
-#ifndef EMBER_MULTI_SPARSE_APPLY_FIRST
-#define EMBER_MULTI_SPARSE_APPLY_FIRST 0 // multi-table apply launch: sparse tables' blocks first
-#endif
-#ifndef EMBER_MULTI_SPARSE_STREAM
-#define EMBER_MULTI_SPARSE_STREAM 0      // multi-table launch with a dense table: sparse tables'
-                                         // statistics loads non-temporal
-#endif
 #ifndef EMBER_MAX_BLOCKS
 #define EMBER_MAX_BLOCKS 384        // row blocks of the statistics pass
 #endif
@@ -133,6 +123,8 @@ constexpr int kLmheadK = EMBER_LMHEAD_K;
 constexpr int kFlagRange = 1;
 constexpr int kFlagDuplicate = 2;
 constexpr int kFlagCount = 4;       // a device-side row count outside [0, max rows]
+constexpr int kFlagTimeout = 8;     // the one-launch sparse step: a grid barrier's bounded wait ran
+                                    // out (kept in the status word until ember_init_state)
 
 // Column tiling of one launch for a given gradient dtype (16-byte chunks).
 struct ColPlan {
@@ -183,14 +175,17 @@ struct WsLayout {
     size_t status;  // int32: status of the last step (read by ember_get_error)
     size_t ticket;  // int32: blocks of the finalize pass that have finished
     size_t scale;   // float: sqrt(1 / (bias s)) / alpha_s of the last step
+    size_t epoch;   // uint32: one-launch sparse steps taken (numbers their grid barriers)
+    size_t arrive;  // uint32[kOnchipBlocks * kArriveStride]: last barrier number of each block
     size_t slot;    // int32[V]: 1 + position in idx of a touched row, else 0
     size_t zero_end;// [0, zero_end) must be zero before the first step
     size_t qa;      // float[D rounded up to 8]: column factors sqrt(c_j)
     size_t rowpart; // float[max(nslab, NT)][V]: per-slab (or per-column-tile) row sums of g^2
-    size_t rsum;    // float[ceil(V / 4096)]: per-block sums of the new r
+    size_t rsum;    // float[ceil(V / 1024)]: per-block sums of the new r
     size_t csum;    // float[ceil(D / kFinCols)]: per-block sums of the new c
-    size_t p;       // float[max(row_blocks(V, nslab) over both dtypes, MT)][D]: per-block (or
-                    // per-row-tile) column sums of g^2
+    size_t p;       // float[max(row_blocks(V, nslab) over both dtypes, MT, kOnchipBlocks)][D]:
+                    // per-block (or per-row-tile) column sums of g^2
+    size_t parts;   // double[3][kOnchipBlocks]: per-block sums of the one-launch sparse step
     size_t total;
 };
 WsLayout ws_layout(int64_t V, int64_t D);
@@ -203,8 +198,8 @@ struct StepArgs {
     int g_dtype;
     int64_t ldg;
     bool sparse;        // sparse-row step: G holds `rows` rows mapped through idx
-    const int64_t* idx;
-    const int64_t* n_dev;  // sparse steps: row count in device memory (rows is then its maximum), or null // device array of `rows` row indices (sparse only)
+    const int64_t* idx;    // sparse steps: device array of `rows` row indices
+    const int64_t* n_dev;  // sparse steps: row count in device memory (rows is then its maximum), or null
     int64_t rows;       // V (dense) or n_idx (sparse)
     float* r;
     float* c;
@@ -216,12 +211,25 @@ struct StepArgs {
     double inv_alpha;   // 1 / (+lr or -lr); 0 when lr == 0 (no apply launch)
     float eps_over_alpha;
     char* ws;
-    bool stats_stream;  // statistics pass: load every gradient row non-temporally (a
-                        // small table sharing a launch with a dense one keeps out of
-                        // the last-level cache the dense table's rows are left in)
     int fin_nb;         // finalize: partial rows of P and row slabs of rowpart, when
     int fin_nslab;      // they come from the LM-head gradient GEMM (0: the statistics pass's)
+    int64_t spin_ticks; // one-launch sparse step: bound of a grid-barrier wait (real-time
+                        // counter ticks, 100 MHz)
 };
+
+// The sparse-row step in one launch (ember_kernels.hip): kOnchipBlocks blocks
+// of kOnchipThreads threads, one per compute unit, all resident at once; each
+// block holds its share of the gradient rows and of the weight rows they
+// update in registers from the statistics to the update, and two grid
+// barriers separate the statistics, the state update and the weight update.
+constexpr int kOnchipBlocks = 256;
+constexpr int kOnchipThreads = 512;
+constexpr int kArriveStride = 16;  // words between two blocks' barrier flags (64 bytes)
+constexpr int64_t kOnchipSpinTicks = 100000000;   // ~1 s: a barrier wait that long means lost residency
+// True when the step's rows fit the launch (dtypes, slabs and row count) and
+// the current device keeps every block of it resident.
+bool onchip_fits(const StepArgs& a);
+hipError_t launch_sparse_onchip(const StepArgs& a, hipStream_t s);
 
 // Each launcher enqueues one kernel on `s` and returns hipGetLastError().
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);

@@ -26,6 +26,7 @@ EMBER_ERR_DTYPE = -4
 EMBER_ERR_WORKSPACE = -5
 EMBER_ERR_INDEX = -6
 EMBER_ERR_HIP = -7
+EMBER_ERR_DEVICE = -8
 
 # Every function the C header declares, checked by the CPU test suite.
 EXPORTED = ("ember_workspace_bytes", "ember_init_state", "ember_step_dense",

@@ -44,7 +44,7 @@ def test_library_exports_every_declared_function(em):
 
 
 def test_strerror_covers_every_status(em):
-    for st in range(0, -8, -1):
+    for st in range(0, -9, -1):
         assert em.ember_strerror(st) and em.ember_strerror(st) != "unknown status"
     assert em.ember_strerror(12345) == "unknown status"
 

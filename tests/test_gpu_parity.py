@@ -93,16 +93,48 @@ def dense_lockstep(em, cfg, seed=0, steps=None, rows=None, ld_pad=0, maximize=Fa
     return W, tab
 
 
-def sparse_lockstep(em, cfg, seed=0, steps=None, shuffle=False, check_rows_all=True):
+# Kernels of the two forms of the sparse step (one launch with the rows held on
+# chip, or statistics + finalize + apply), as the library's timing records name them.
+ONCHIP = {"ember_sparse_onchip"}
+THREE_LAUNCH = {"ember_stats", "ember_finalize", "ember_apply"}
+
+
+def sparse_kernels(em, step):
+    """Runs step() with the library's kernel timing on; returns the kernel names."""
+    em.ember_profile_enable(True)
+    step()
+    torch.cuda.synchronize()
+    em.ember_profile_enable(False)
+    return set(em.ember_profile_collect())
+
+
+def sparse_lockstep(em, cfg, seed=0, steps=None, shuffle=False, check_rows_all=True, path=None):
+    """Sparse steps in lockstep with the oracle; path (ONCHIP or THREE_LAUNCH)
+    is the set of kernels the first step must launch."""
     steps = cfg.steps if steps is None else steps
     print(f"sparse lockstep {cfg.name} V={cfg.V} D={cfg.D} steps={steps} shuffle={shuffle}", flush=True)
-    W = wl.make_weights(cfg, seed=seed, device=DEV)
+    # rows of a width that is not a whole number of 16-byte chunks get a padded stride
+    ragged = lambda dt: (cfg.D * torch.empty(0, dtype=dt).element_size()) % 16 != 0
+    W = wl.make_weights(cfg, seed=seed, device=DEV,
+                        ld=_ld(cfg.D, cfg.w_dtype, 1) if ragged(cfg.w_dtype) else None)
     tab = Table(em, cfg.V, cfg.D)
     for t in range(1, steps + 1):
         idx, Gr = wl.make_sparse_batch(cfg, t, seed=seed, device=DEV, shuffle=shuffle)
+        if ragged(cfg.g_dtype):
+            Gp = torch.zeros(Gr.shape[0], _ld(cfg.D, cfg.g_dtype, 1), dtype=cfg.g_dtype, device=DEV)
+            Gp[:, :cfg.D] = Gr
+            Gr = Gp[:, :cfg.D]
         W_prev = host_bits(W)
         r_prev = tab.r.cpu().numpy()
-        em.ember_step_sparse_rows(W, Gr, idx, tab.r, tab.c, t, LR, B2, EPS, False, tab.ws)
+
+        def step():
+            em.ember_step_sparse_rows(W, Gr, idx, tab.r, tab.c, t, LR, B2, EPS, False, tab.ws)
+
+        if path is not None and t == 1:
+            got = sparse_kernels(em, step)
+            assert got == path, f"{cfg.name}: launched {sorted(got)}, expected {sorted(path)}"
+        else:
+            step()
         assert em.ember_get_error(tab.ws) == em.EMBER_OK
         idx_h = idx.cpu().numpy()
         touched = np.sort(idx_h)
@@ -178,7 +210,58 @@ def test_large_step_counter(em):
 def test_sparse_small_every_row(em):
     cfg = wl.Config("sparse_small", 5000, 320, torch.bfloat16, torch.bfloat16, 4, "sparse_zipf",
                     batch_tokens=3000)
-    sparse_lockstep(em, cfg, seed=5, shuffle=True)
+    sparse_lockstep(em, cfg, seed=5, shuffle=True, path=ONCHIP)
+
+
+@pytest.mark.parametrize("V,D,wd,gd,tokens,path", [
+    (3000, 512, torch.bfloat16, torch.float32, 2500, ONCHIP),    # bf16 W, fp32 G
+    (3000, 512, torch.float32, torch.bfloat16, 2500, ONCHIP),    # fp32 W, bf16 G: 6 rows per wave
+    (3000, 896, torch.float32, torch.float32, 2500, ONCHIP),     # two slabs of 112 chunks
+    (3000, 64, torch.float32, torch.float32, 2500, ONCHIP),      # one slab of 16 chunks
+    (3000, 1001, torch.bfloat16, torch.bfloat16, 2000, THREE_LAUNCH),  # width not whole 16-byte chunks
+    (4000, 8192, torch.bfloat16, torch.bfloat16, 30000, THREE_LAUNCH),  # ~2800 rows > 2560 held at D=8192
+    (2000, 20000, torch.bfloat16, torch.bfloat16, 800, THREE_LAUNCH),  # 20 column slabs
+])
+def test_sparse_forms_every_row(em, V, D, wd, gd, tokens, path):
+    cfg = wl.Config(f"sparse{V}x{D}", V, D, wd, gd, 3, "sparse_zipf", batch_tokens=tokens)
+    sparse_lockstep(em, cfg, seed=V + D, shuffle=True, path=path)
+
+
+@pytest.mark.parametrize("n,path", [(5120, ONCHIP), (5121, THREE_LAUNCH)])
+def test_sparse_row_capacity_boundary(em, n, path):
+    """At D = 4096 bf16 a block holds 20 rows (two waves per slab, ten rows per
+    wave): 5120 rows take the one-launch form, 5121 the three-launch form."""
+    V, D = 20000, 4096
+    cfg = wl.Config("cap", V, D, torch.bfloat16, torch.bfloat16, 1, "normal")
+    print(f"capacity boundary n={n}", flush=True)
+    W = wl.make_weights(cfg, seed=n, device=DEV)
+    tab = Table(em, V, D)
+    gen = torch.Generator(device="cpu").manual_seed(n)
+    idx = torch.randperm(V, generator=gen)[:n].to(DEV)
+    Gr = (torch.randn(n, D, generator=gen) * 1e-3).to(torch.bfloat16).to(DEV)
+    for t in (1, 2):
+        W_prev = host_bits(W)
+
+        def step():
+            em.ember_step_sparse_rows(W, Gr, idx, tab.r, tab.c, t, LR, B2, EPS, False, tab.ws)
+
+        if t == 1:
+            got = sparse_kernels(em, step)
+            assert got == path, f"n={n}: launched {sorted(got)}"
+        else:
+            step()
+        assert em.ember_get_error(tab.ws) == em.EMBER_OK
+        idx_h = idx.cpu().numpy()
+        touched = np.sort(idx_h)
+        W_ref = W_prev.copy()
+        assert oracle.step(W_ref, host_bits(Gr), tab.r_o, tab.c_o, t, idx=idx_h, w_rows=touched) == 0
+        check_state(tab.r, tab.r_o, f"r step {t}")
+        check_state(tab.c, tab.c_o, f"c step {t}")
+        W_gpu = host_bits(W)
+        check_w(W_gpu[touched], W_ref[touched], W_prev[touched], f"W step {t}")
+        mask = np.ones(V, bool)
+        mask[touched] = False
+        assert np.array_equal(W_gpu[mask], W_prev[mask]), "a row outside idx changed"
 
 
 def test_sparse_fp32_and_empty_index_list(em):
@@ -337,7 +420,7 @@ def test_full_lmhead128k_bf16(em):
 @pytest.mark.timeout(600)
 def test_full_embed128k_sparse_bf16(em):
     cfg = wl.CONFIGS["embed128k"]
-    sparse_lockstep(em, cfg, seed=13)
+    sparse_lockstep(em, cfg, seed=13, path=ONCHIP)
 
 
 @pytest.mark.timeout(600)
