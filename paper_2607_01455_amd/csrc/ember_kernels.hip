@@ -1606,21 +1606,31 @@ __global__ __launch_bounds__(kOnchipThreads, 1) void ember_sparse_onchip(OnchipP
     }
 
     // column sums of the block: the Q waves of each slab in order -> P[b]
-    float* Pb = a.P + (int64_t)b * D;
+    const __amdgpu_buffer_rsrc_t prs_w = __builtin_amdgcn_make_buffer_rsrc(a.P + (int64_t)b * D, 0, (int)(D * 4),
+                                                                           kBufferWord3);
 #pragma unroll
     for (int m = 0; m < M; ++m) {
 #pragma unroll
         for (int e = 0; e < EPC; ++e) cl[wave][lane * EPC + e] = acc[m][e];
         __syncthreads();
-        for (int x = threadIdx.x; x < a.nslab * kWave * EPC; x += kOnchipThreads) {
+        // four consecutive columns per thread, one 16-byte agent-scope store
+        for (int x4 = threadIdx.x; x4 < a.nslab * kWave * EPC / 4; x4 += kOnchipThreads) {
+            const int x = 4 * x4;
             const int s = x / (kWave * EPC);
             const int off = x - s * (kWave * EPC);
             const int ch = s * a.slab_chunks + kWave * m + off / EPC;
             const int send = min((s + 1) * a.slab_chunks, a.total_chunks);
             if (ch < send) {
-                float v = cl[s][off];
-                for (int qq = 1; qq < Q; ++qq) v += cl[qq * a.nslab + s][off];
-                st_agent(Pb + (int64_t)ch * EPC + off % EPC, v);
+                float4 v = *reinterpret_cast<const float4*>(&cl[s][off]);
+                for (int qq = 1; qq < Q; ++qq) {
+                    const float4 w = *reinterpret_cast<const float4*>(&cl[qq * a.nslab + s][off]);
+                    v.x += w.x;
+                    v.y += w.y;
+                    v.z += w.z;
+                    v.w += w.w;
+                }
+                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), prs_w,
+                                                       (ch * EPC + off % EPC) * 4, 0, kAgentScopeLoad);
             }
         }
         __syncthreads();
@@ -1645,63 +1655,67 @@ __global__ __launch_bounds__(kOnchipThreads, 1) void ember_sparse_onchip(OnchipP
     const bool ok1 = grid_barrier(a.arrive, gen, a.spin_ticks, a.flag, a.status, &sh_ok);
 
     // ---- phase 2: c and the column factors; r of every row ----
-    if (threadIdx.x == 0) sh_err = ld_agent_i(a.flag) | (ok1 ? 0 : kFlagTimeout);
-    __syncthreads();
-    const int err = sh_err;
-    double csum = 0.0;
+    // Block b owns columns [c0, c1) and rows [v0, v1).  Each round takes 16
+    // columns (thread (g, x) adds partials g, g + 32, ... of column c0 + x,
+    // then 16 threads add the 32 group sums in group order) and 512 rows (one
+    // per thread: untouched rows decay, touched rows take the value their
+    // gradient row's block computed, marks are cleared); all loads of a
+    // round, and the error bits, are issued before the first is used.
+    double csum = 0.0, usum = 0.0;
     {
-        // columns [c0, c1) in groups of 16: thread (g, x) adds the partials
-        // g, g + 32, ... of its column in that order, then the 32 group sums
-        // in group order
         const int64_t c0 = D * b / NB, c1 = D * (b + 1) / NB;
+        const int64_t v0 = V * b / NB, v1 = V * (b + 1) / NB;
         const int x = threadIdx.x % 16, g = threadIdx.x / 16;
         const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(a.P, 0, (int)(NB * D * 4), kBufferWord3);
         const int prow = kColGroups * (int)D * 4;
-        for (int64_t j0 = c0; j0 < c1; j0 += 16) {
-            const int64_t j = j0 + x;
+        // at least one round: it also reads the error bits
+        const int64_t rounds = max((int64_t)1, max((c1 - c0 + 15) / 16, (v1 - v0 + kOnchipThreads - 1) / kOnchipThreads));
+        for (int64_t k = 0; k < rounds; ++k) {
+            const int64_t j = c0 + 16 * k + x;
             const bool jv = j < c1;
-            float s = 0.0f;
             const int vo = jv ? (g * (int)D + (int)j) * 4 : kOutside;
+            uint32_t pv[NB / kColGroups];
 #pragma unroll
-            for (int k = 0; k < NB / kColGroups; ++k)
-                s += __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(prs, vo, k * prow, kAgentScopeLoad));
-            part[g][x] = s;
+            for (int q2 = 0; q2 < NB / kColGroups; ++q2)
+                pv[q2] = __builtin_amdgcn_raw_buffer_load_b32(prs, vo, q2 * prow, kAgentScopeLoad);
+            const float cold = (jv && g == 0) ? a.c[j] : 0.0f;
+            const int64_t i = v0 + k * kOnchipThreads + threadIdx.x;
+            const bool iv = i < v1;
+            const int sl = iv ? ld_agent_i(a.slot + i) : 0;
+            const float ri = iv ? a.r[i] : 0.0f;
+            if (k == 0 && threadIdx.x == 0) sh_err = ld_agent_i(a.flag) | (ok1 ? 0 : kFlagTimeout);
+            float sp = 0.0f;
+#pragma unroll
+            for (int q2 = 0; q2 < NB / kColGroups; ++q2) sp += __uint_as_float(pv[q2]);
+            part[g][x] = sp;
             __syncthreads();
-            if (threadIdx.x < 16) {
-                float cn = 0.0f;
-                if (jv) {
-                    float colsum = 0.0f;
-                    for (int w = 0; w < kColGroups; ++w) colsum += part[w][x];
-                    const float mean = (float)((double)colsum / (double)V);
-                    cn = fmaf(a.beta2, a.c[j], a.one_minus_beta2 * mean);
-                    if (!err) {
-                        a.c[j] = cn;
-                        st_agent(a.qa + j, sqrtf(cn));
-                    }
+            const int err = sh_err;
+            if (threadIdx.x < 16 && jv) {
+                float colsum = 0.0f;
+                for (int w = 0; w < kColGroups; ++w) colsum += part[w][x];
+                const float mean = (float)((double)colsum / (double)V);
+                const float cn = fmaf(a.beta2, cold, a.one_minus_beta2 * mean);
+                if (!err) {
+                    a.c[j] = cn;
+                    st_agent(a.qa + j, sqrtf(cn));
                 }
                 csum += (double)cn;
             }
-            __syncthreads();
-        }
-    }
-    double usum = 0.0;
-    {
-        // rows [v0, v1): untouched rows decay; touched rows take the value
-        // their gradient row's block computed; marks are cleared
-        const int64_t v0 = V * b / NB, v1 = V * (b + 1) / NB;
-        for (int64_t i = v0 + threadIdx.x; i < v1; i += kOnchipThreads) {
-            const int sl = ld_agent_i(a.slot + i);
-            const float ri = a.r[i];
-            if (sl != 0) {
-                a.slot[i] = 0;
-            } else if (!err) {
-                const float rn = a.beta2 * ri;
-                a.r[i] = rn;
-                usum += (double)rn;
+            if (iv) {
+                if (sl != 0) {
+                    a.slot[i] = 0;
+                } else if (!err) {
+                    const float rn = a.beta2 * ri;
+                    a.r[i] = rn;
+                    usum += (double)rn;
+                }
             }
+            if (k == 0 && !err && threadIdx.x < nloc && id_lds[threadIdx.x] >= 0)
+                a.r[id_lds[threadIdx.x]] = rn_lds[threadIdx.x];
+            __syncthreads();   // part is reused by the next round
         }
-        if (!err && threadIdx.x < nloc && id_lds[threadIdx.x] >= 0) a.r[id_lds[threadIdx.x]] = rn_lds[threadIdx.x];
     }
+    const int err = sh_err;
     usum = onchip_block_sum(usum, dsum);
     if (threadIdx.x < kWave) csum = wave_sum(csum);
     if (threadIdx.x == 0) {
@@ -1737,19 +1751,31 @@ __global__ __launch_bounds__(kOnchipThreads, 1) void ember_sparse_onchip(OnchipP
                 qraw[m][k] = __builtin_bit_cast(
                     u32x4, __builtin_amdgcn_raw_buffer_load_b128(qrs, qoff + 16 * k, 0, kAgentScopeLoad));
         }
-        // s from the per-block sums in a fixed order (every block alike)
-        double sr = 0.0, sc = 0.0;
-        if (threadIdx.x < NB) {
-            sr = ld_agent_d(a.parts + threadIdx.x) + ld_agent_d(a.parts + NB + threadIdx.x);
-            sc = ld_agent_d(a.parts + 2 * NB + threadIdx.x);
-        }
-        sr = onchip_block_sum(sr, dsum);
-        sc = onchip_block_sum(sc, dsum);
-        if (threadIdx.x == 0) {
-            const double mean_rhat = sr / (double)V * a.inv_bias;
-            const double mean_chat = sc / (double)D * a.inv_bias;
-            const double s = sqrt(mean_rhat * mean_chat);
-            sh_scale = s > 0.0 ? (float)(sqrt(a.inv_bias / s) * a.inv_alpha) : 0.0f;
+        // s from the per-block sums in a fixed order (every block alike):
+        // wave 0, lane l adds blocks 4l .. 4l + 3, then the lanes' sums
+        if (threadIdx.x < kWave) {
+            double pu[NB / kWave], pt[NB / kWave], pc[NB / kWave];
+#pragma unroll
+            for (int k = 0; k < NB / kWave; ++k) {
+                const int bb = lane * (NB / kWave) + k;
+                pu[k] = ld_agent_d(a.parts + bb);
+                pt[k] = ld_agent_d(a.parts + NB + bb);
+                pc[k] = ld_agent_d(a.parts + 2 * NB + bb);
+            }
+            double sr = 0.0, sc = 0.0;
+#pragma unroll
+            for (int k = 0; k < NB / kWave; ++k) {
+                sr += pu[k] + pt[k];
+                sc += pc[k];
+            }
+            sr = wave_sum(sr);
+            sc = wave_sum(sc);
+            if (threadIdx.x == 0) {
+                const double mean_rhat = sr / (double)V * a.inv_bias;
+                const double mean_chat = sc / (double)D * a.inv_bias;
+                const double s = sqrt(mean_rhat * mean_chat);
+                sh_scale = s > 0.0 ? (float)(sqrt(a.inv_bias / s) * a.inv_alpha) : 0.0f;
+            }
         }
         __syncthreads();
         const float scale = sh_scale;
