@@ -164,6 +164,43 @@ int ember_step_sparse_rows_devn(void* W, int w_dtype, int64_t ldw,
                                 void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * The sparse-row step without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation.  The step is ember_step_sparse_rows's
+ * one-launch form (same kernel, same bits as that call with a workspace); its
+ * scratch (row marks, barrier flags, per-block partial sums, column factors)
+ * is a 16 MiB array inside the library, one per GPU, held until the process
+ * ends.  Each call enqueues a small zero fill of that array's first part and
+ * of *status, then the step; nothing is allocated.
+ *
+ * Arguments as for ember_step_sparse_rows (W, G_rows, idx, n_idx, r, c, V, D,
+ * t and the scalars), without ws/ws_bytes, plus:
+ *   status  device int32 (4-byte aligned, required): set to 0 by the call's
+ *           fill, then the step ORs its error bits into it (1: an id outside
+ *           [0, V), 2: a repeated id; W, r and c are then unchanged; 8: the
+ *           step's blocks did not all run at once, W, r and c unspecified).
+ *           Read it after the stream has reached the step.
+ * r and c start at zero (Algorithm 1's r_0, c_0) and are the caller's, as is t.
+ *
+ * Limits (checked on the host before anything is enqueued):
+ *   the step's scratch, about 4 V + 1028 D bytes + 23 KiB, at most 16 MiB
+ *   (e.g. V up to 3.1 million rows at D = 4096): EMBER_ERR_WORKSPACE otherwise;
+ *   the one-launch form must take the step: D a whole number of 16-byte chunks
+ *   of G, at most 8 column slabs of 2 KiB (bf16 D <= 8192, fp32 D <= 4096),
+ *   n_idx within the rows held on chip (5120 at 4096 bf16 columns), and a
+ *   device that keeps 256 blocks of the kernel resident: EMBER_ERR_SHAPE
+ *   otherwise.
+ * Calls that overlap on one GPU (two streams, or two threads) share the array
+ * and race; calls must be ordered.
+ */
+int ember_step_sparse_rows_static(void* W, int w_dtype, int64_t ldw,
+                                  const void* G_rows, int g_dtype, int64_t ldg,
+                                  const int64_t* idx, int64_t n_idx,
+                                  float* r, float* c, int64_t V, int64_t D, int64_t t,
+                                  float lr, float beta2, float eps, int maximize,
+                                  int32_t* status, hipStream_t stream);
+
+/*
  * Several Ember steps in one call: the tables of a model (for example the
  * LM head, dense, and the input embedding, sparse rows) each take the step
  * Algorithm 1 defines for them (or the row-only step of Section 2.1), exactly

@@ -97,7 +97,9 @@ int run_step(StepArgs& a, float lr, float beta2, float eps, int64_t t, int maxim
     set_scalars(a, lr, beta2, eps, t, maximize);
     // A sparse step whose rows fit on chip runs as one launch.
     if (ember::onchip_fits(a)) {
-        const hipError_t e = timed("ember_sparse_onchip", s, [&] { return ember::launch_sparse_onchip(a, s); });
+        const hipError_t e = timed("ember_sparse_onchip", s, [&] {
+            return ember::launch_sparse_onchip(a, ember::onchip_space(a), s);
+        });
         return e == hipSuccess ? EMBER_OK : EMBER_ERR_HIP;
     }
     hipError_t e = timed("ember_stats", s, [&] { return ember::launch_stats(a, s); });
@@ -437,7 +439,9 @@ int ember_step_multi(const ember_table_step* tables, int n_tables, hipStream_t s
     hipError_t e = hipSuccess;
     for (const StepArgs* a : onchip) {
         if (e == hipSuccess)
-            e = timed("ember_sparse_onchip", stream, [&] { return ember::launch_sparse_onchip(*a, stream); });
+            e = timed("ember_sparse_onchip", stream, [&] {
+                return ember::launch_sparse_onchip(*a, ember::onchip_space(*a), stream);
+            });
     }
     if (e == hipSuccess && !ro_sparse.empty())
         e = timed("ember_rowonly_validate_multi", stream, [&] {
@@ -460,6 +464,47 @@ int ember_step_multi(const ember_table_step* tables, int n_tables, hipStream_t s
         e = timed("ember_rowonly_multi", stream, [&] {
             return run_phase(ro_all, ember::rowonly_key, ember::launch_rowonly_multi, stream);
         });
+    return e == hipSuccess ? EMBER_OK : EMBER_ERR_HIP;
+}
+
+int ember_step_sparse_rows_static(void* W, int w_dtype, int64_t ldw, const void* G_rows, int g_dtype, int64_t ldg,
+                                  const int64_t* idx, int64_t n_idx, float* r, float* c, int64_t V, int64_t D,
+                                  int64_t t, float lr, float beta2, float eps, int maximize, int32_t* status,
+                                  hipStream_t stream) {
+    int st = check_shape(V, D);
+    if (st == EMBER_OK && (n_idx < 0 || n_idx > V)) st = EMBER_ERR_SHAPE;
+    if (st == EMBER_OK) st = check_matrix(W, w_dtype, ldw, D, false);
+    if (st == EMBER_OK) st = check_matrix(G_rows, g_dtype, ldg, D, n_idx == 0);
+    if (st == EMBER_OK && ((n_idx > 0 && idx == nullptr) || r == nullptr || c == nullptr || status == nullptr))
+        st = EMBER_ERR_ARG;
+    if (st == EMBER_OK && ((idx != nullptr && !aligned(idx, 8)) || !aligned(r, 4) || !aligned(c, 4) ||
+                           !aligned(status, 4)))
+        st = EMBER_ERR_ALIGN;
+    if (st == EMBER_OK) st = check_scalars(t, lr, beta2, eps);
+    ember::OnchipSpace sp{};
+    if (st == EMBER_OK && ember::static_layout(V, D, &sp) > ember::kStaticScratchBytes) st = EMBER_ERR_WORKSPACE;
+    if (st != EMBER_OK) return st;
+    StepArgs a{};
+    a.sparse = true;
+    a.W = W;
+    a.w_dtype = w_dtype;
+    a.ldw = ldw;
+    a.G = G_rows;
+    a.g_dtype = g_dtype;
+    a.ldg = ldg;
+    a.idx = idx;
+    a.rows = n_idx;
+    a.r = r;
+    a.c = c;
+    a.V = V;
+    a.D = D;
+    set_scalars(a, lr, beta2, eps, t, maximize);
+    if (!ember::onchip_fits(a)) return EMBER_ERR_SHAPE;
+    if (ember::static_scratch(&sp.base) != hipSuccess) return EMBER_ERR_HIP;
+    sp.status_ptr = status;
+    hipError_t e = ember::launch_static_prep(sp.base, sp.zero_end, status, stream);
+    if (e == hipSuccess)
+        e = timed("ember_sparse_onchip", stream, [&] { return ember::launch_sparse_onchip(a, sp, stream); });
     return e == hipSuccess ? EMBER_OK : EMBER_ERR_HIP;
 }
 

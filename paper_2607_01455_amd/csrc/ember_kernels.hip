@@ -2154,8 +2154,23 @@ bool onchip_fits(const StepArgs& a) {
     return onchip_resident(a.g_dtype, a.w_dtype, cp.m);
 }
 
-hipError_t launch_sparse_onchip(const StepArgs& a, hipStream_t s) {
+OnchipSpace onchip_space(const StepArgs& a) {
     const WsLayout L = ws_layout(a.V, a.D);
+    OnchipSpace sp;
+    sp.base = a.ws;
+    sp.flag = L.flag;
+    sp.status = L.status;
+    sp.epoch = L.epoch;
+    sp.arrive = L.arrive;
+    sp.slot = L.slot;
+    sp.qa = L.qa;
+    sp.p = L.p;
+    sp.parts = L.parts;
+    sp.status_ptr = nullptr;
+    return sp;
+}
+
+hipError_t launch_sparse_onchip(const StepArgs& a, const OnchipSpace& sp, hipStream_t s) {
     const ColPlan cp = col_plan(a.D, a.g_dtype);
     OnchipParams p;
     p.W = a.W;
@@ -2178,14 +2193,14 @@ hipError_t launch_sparse_onchip(const StepArgs& a, hipStream_t s) {
     p.inv_bias = a.inv_bias;
     p.inv_alpha = a.inv_alpha;
     p.eps_over_alpha = a.eps_over_alpha;
-    p.slot = reinterpret_cast<int*>(a.ws + L.slot);
-    p.flag = reinterpret_cast<int*>(a.ws + L.flag);
-    p.status = reinterpret_cast<int*>(a.ws + L.status);
-    p.epoch = reinterpret_cast<unsigned*>(a.ws + L.epoch);
-    p.arrive = reinterpret_cast<unsigned*>(a.ws + L.arrive);
-    p.P = reinterpret_cast<float*>(a.ws + L.p);
-    p.parts = reinterpret_cast<double*>(a.ws + L.parts);
-    p.qa = reinterpret_cast<float*>(a.ws + L.qa);
+    p.slot = reinterpret_cast<int*>(sp.base + sp.slot);
+    p.flag = reinterpret_cast<int*>(sp.base + sp.flag);
+    p.status = sp.status_ptr ? sp.status_ptr : reinterpret_cast<int*>(sp.base + sp.status);
+    p.epoch = reinterpret_cast<unsigned*>(sp.base + sp.epoch);
+    p.arrive = reinterpret_cast<unsigned*>(sp.base + sp.arrive);
+    p.P = reinterpret_cast<float*>(sp.base + sp.p);
+    p.parts = reinterpret_cast<double*>(sp.base + sp.parts);
+    p.qa = reinterpret_cast<float*>(sp.base + sp.qa);
     p.spin_ticks = a.spin_ticks;
     // A plain launch: the residency check above (blocks per compute unit x
     // compute units >= kOnchipBlocks) is what the grid barriers rely on, and
@@ -2194,6 +2209,74 @@ hipError_t launch_sparse_onchip(const StepArgs& a, hipStream_t s) {
     void* args[] = {&p};
     return hipLaunchKernel(onchip_kernel(a.g_dtype, a.w_dtype, cp.m), dim3(kOnchipBlocks), dim3(kOnchipThreads), args,
                            0, s);
+}
+
+// ---------------------------------------------------------------------------
+// the one-launch sparse step with its scratch inside the library
+// ---------------------------------------------------------------------------
+
+namespace {
+
+// Scratch of ember_step_sparse_rows_static.  In host code this name is a
+// host-side stand-in, not a device address: kernels and fills only ever get
+// the address hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+// Zero fill of the scratch's first `words` words and the caller's status.
+__global__ __launch_bounds__(kBlock) void ember_static_prep(uint32_t* p, int64_t words, int* status) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) *status = 0;
+    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < words; i += (int64_t)gridDim.x * kBlock)
+        p[i] = 0u;
+}
+
+} // namespace
+
+size_t static_layout(int64_t V, int64_t D, OnchipSpace* sp) {
+    size_t off = 0;
+    sp->flag = 0;
+    sp->status = 4;
+    sp->epoch = 16;
+    off = align256(20);
+    sp->arrive = off;
+    off = align256(off + (size_t)kOnchipBlocks * kArriveStride * 4);
+    sp->slot = off;
+    off = align256(off + (size_t)V * 4);
+    sp->zero_end = off;
+    sp->qa = off;
+    off = align256(off + (size_t)((D + 7) / 8 * 8) * 4);
+    sp->p = off;
+    off = align256(off + (size_t)kOnchipBlocks * (size_t)D * 4);
+    sp->parts = off;
+    off = align256(off + (size_t)3 * kOnchipBlocks * 8);
+    return off;
+}
+
+hipError_t static_scratch(char** out) {
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static char* addr[kMaxDevices];
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (addr[dev] == nullptr) {
+        void* ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        addr[dev] = static_cast<char*>(ptr);
+    }
+    *out = addr[dev];
+    return hipSuccess;
+}
+
+hipError_t launch_static_prep(char* base, size_t zero_bytes, int* status, hipStream_t s) {
+    const int64_t words = (int64_t)(zero_bytes / 4);
+    int64_t blocks = (words + kBlock - 1) / kBlock;
+    if (blocks < 1) blocks = 1;
+    if (blocks > 1024) blocks = 1024;
+    ember_static_prep<<<dim3((unsigned)blocks), kBlock, 0, s>>>(reinterpret_cast<uint32_t*>(base), words, status);
+    return hipGetLastError();
 }
 
 hipError_t launch_rowonly_validate(const StepArgs& a, hipStream_t s) {

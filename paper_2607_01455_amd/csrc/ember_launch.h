@@ -229,7 +229,24 @@ constexpr int64_t kOnchipSpinTicks = 100000000;   // ~1 s: a barrier wait that l
 // True when the step's rows fit the launch (dtypes, slabs and row count) and
 // the current device keeps every block of it resident.
 bool onchip_fits(const StepArgs& a);
-hipError_t launch_sparse_onchip(const StepArgs& a, hipStream_t s);
+// Byte offsets (from base) of the regions the one-launch step uses.
+struct OnchipSpace {
+    char* base;
+    size_t flag, status, epoch, arrive, slot, zero_end, qa, p, parts;
+    int* status_ptr;    // if set, the status word (else base + status)
+};
+OnchipSpace onchip_space(const StepArgs& a);       // in the caller's workspace
+hipError_t launch_sparse_onchip(const StepArgs& a, const OnchipSpace& sp, hipStream_t s);
+
+// The one-launch step without a workspace (ember_step_sparse_rows_static): its
+// regions sit in a kStaticScratchBytes array inside the library, one per
+// device.  static_layout gives the offsets and the bytes a (V, D) step needs;
+// static_scratch the array's device address on the current device;
+// launch_static_prep zeroes [0, zero_bytes) of it and the caller's status word.
+constexpr size_t kStaticScratchBytes = (size_t)16 << 20;
+size_t static_layout(int64_t V, int64_t D, OnchipSpace* sp);
+hipError_t static_scratch(char** out);
+hipError_t launch_static_prep(char* base, size_t zero_bytes, int* status, hipStream_t s);
 
 // Each launcher enqueues one kernel on `s` and returns hipGetLastError().
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);

@@ -34,7 +34,8 @@ EXPORTED = ("ember_workspace_bytes", "ember_init_state", "ember_step_dense",
             "ember_rowonly_step_sparse_rows", "ember_step_sparse_rows_devn",
             "ember_rowonly_step_sparse_rows_devn", "ember_coalesce_workspace_bytes", "ember_coalesce_rows",
             "ember_lmhead_step", "ember_step_multi", "ember_get_error", "ember_strerror",
-            "ember_profile_enable", "ember_profile_collect", "ember_stream_probe")
+            "ember_profile_enable", "ember_profile_collect", "ember_stream_probe",
+            "ember_step_sparse_rows_static")
 
 
 class EmberError(RuntimeError):
@@ -93,6 +94,8 @@ def _load(path: str = _LIB_PATH) -> ctypes.CDLL:
     lib.ember_profile_enable.argtypes = [i32]
     lib.ember_profile_collect.argtypes = [ctypes.POINTER(_KernelStat), i32, ctypes.POINTER(i32)]
     lib.ember_stream_probe.argtypes = [i32, vp, vp, vp, sz, vp]
+    lib.ember_step_sparse_rows_static.argtypes = [vp, i32, i64, vp, i32, i64, vp, i64, vp, vp, i64, i64, i64,
+                                                  f32, f32, f32, i32, vp, vp]
     for name in EXPORTED:
         if name != "ember_strerror":
             getattr(lib, name).restype = i32
@@ -173,6 +176,23 @@ def ember_step_sparse_rows(W: torch.Tensor, G_rows: torch.Tensor, idx: torch.Ten
                                       float(beta2), float(eps), int(bool(maximize)), _ptr(ws),
                                       ws.numel() * ws.element_size(), _stream(W)),
            "ember_step_sparse_rows")
+
+
+def ember_step_sparse_rows_static(W: torch.Tensor, G_rows: torch.Tensor, idx: torch.Tensor,
+                                  r: torch.Tensor, c: torch.Tensor, t: int, status: torch.Tensor,
+                                  lr: float = 1e-3, beta2: float = 0.999, eps: float = 1e-8,
+                                  maximize: bool = False) -> None:
+    """Sparse-row step whose scratch is the library's own array (no workspace);
+    status: a device int32 tensor of one element that receives the error bits."""
+    V, D = W.shape
+    n = idx.numel()
+    if idx.dtype != torch.int64 or status.dtype != torch.int32:
+        raise TypeError("idx must be int64 and status int32")
+    ldg = _ld(G_rows) if G_rows.numel() else D
+    _check(LIB.ember_step_sparse_rows_static(_ptr(W), _dtype(W), _ld(W), _ptr(G_rows), _dtype(G_rows), ldg,
+                                             _ptr(idx), n, _ptr(r), _ptr(c), V, D, int(t), float(lr),
+                                             float(beta2), float(eps), int(bool(maximize)), status.data_ptr(),
+                                             _stream(W)), "ember_step_sparse_rows_static")
 
 
 def ember_rowonly_init_state(r: torch.Tensor, D: int, ws: torch.Tensor) -> None:
