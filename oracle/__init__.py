@@ -29,7 +29,7 @@ _lib = None
 
 def build() -> str:
     """Compile the oracle with gcc (no fast-math, no FMA contraction)."""
-    cmd = ["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math",
+    cmd = ["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fopenmp",
            "-fPIC", "-shared", _SRC, "-o", _LIB + ".tmp", "-lm"]
     subprocess.run(cmd, check=True)
     os.replace(_LIB + ".tmp", _LIB)
@@ -57,6 +57,8 @@ def _load():
     lib.ember_oracle_coalesce.restype = i32
     lib.ember_oracle_lmhead_grad.argtypes = [vp, i64, vp, i64, i64, i64, i64, vp, i32, i64]
     lib.ember_oracle_lmhead_grad.restype = i32
+    lib.ember_oracle_set_threads.argtypes = [i32]
+    lib.ember_oracle_set_threads.restype = i32
     _lib = lib
     return lib
 
@@ -165,6 +167,12 @@ def lmhead_grad(dY: np.ndarray, H: np.ndarray, out_dtype=np.uint16) -> np.ndarra
     if st != OK:
         raise ValueError("bad arguments for the LM-head gradient")
     return G
+
+
+def set_threads(n: int = 0) -> int:
+    """Threads the oracle's row and column loops use (0: leave as is); returns
+    the count in effect.  Results are the same bits for every count."""
+    return _load().ember_oracle_set_threads(int(n))
 
 
 def bf16_to_f64(bits: int) -> float:

@@ -53,8 +53,15 @@
  * correction of Algorithm 1 unchanged, vtil_ij = rhat_i (no column factor and
  * no normaliser, since rhat already has the units of g^2), and the same update
  * theta +/- alpha g / (sqrt(vtil) + eps).  c is neither read nor written.
+ *
+ * Threads (OpenMP): the loops over independent rows (row statistic, update)
+ * and over independent column ranges (column statistic, each column still
+ * summed over rows in ascending order) may run on several threads; every
+ * float64 sum keeps the order written here, so the results are the same bits
+ * for any thread count.  The O(V + D) sums of the normaliser stay serial.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -103,6 +110,14 @@ uint16_t ember_oracle_f64_to_bf16(double x)
     uint32_t u;
     memcpy(&u, &f, sizeof u);
     return (uint16_t)(sign | (uint16_t)(u >> 16));
+}
+
+/* Threads the loops below may use (OpenMP); returns the count now in effect. */
+int ember_oracle_set_threads(int n)
+{
+    if (n > 0)
+        omp_set_num_threads(n);
+    return omp_get_max_threads();
 }
 
 /* Bytes of Ember state for one V x D table: r (V floats) and c (D floats). */
@@ -191,6 +206,7 @@ int ember_oracle_step(void* W, int w_dtype, int64_t ldw,
     const double one_minus_b2 = 1.0 - b2;
 
     /* Row second moment: r_i <- beta2 r_i + (1-beta2) mean_j g_ij^2. */
+#pragma omp parallel for schedule(static)
     for (int64_t i = 0; i < V; ++i) {
         double sumsq = 0.0;
         if (grow[i] >= 0) {
@@ -206,12 +222,16 @@ int ember_oracle_step(void* W, int w_dtype, int64_t ldw,
     /* Column second moment: c_j <- beta2 c_j + (1-beta2) mean_i g_ij^2,
      * summing rows in ascending row order. */
     if (!row_only) {
-        for (int64_t i = 0; i < V; ++i) {
-            if (grow[i] < 0)
-                continue;
-            for (int64_t j = 0; j < D; ++j) {
-                double g = load_elem(G, g_dtype, grow[i] * ldg + j);
-                colsum[j] += g * g;
+#pragma omp parallel for schedule(static)
+        for (int64_t j0 = 0; j0 < D; j0 += 64) {
+            const int64_t j1 = j0 + 64 < D ? j0 + 64 : D;
+            for (int64_t i = 0; i < V; ++i) {
+                if (grow[i] < 0)
+                    continue;
+                for (int64_t j = j0; j < j1; ++j) {
+                    double g = load_elem(G, g_dtype, grow[i] * ldg + j);
+                    colsum[j] += g * g;
+                }
             }
         }
         for (int64_t j = 0; j < D; ++j) {
@@ -238,6 +258,7 @@ int ember_oracle_step(void* W, int w_dtype, int64_t ldw,
     const double alpha = (double)lr;
     const double e = (double)eps;
     const int64_t n_out = (w_rows != NULL) ? n_w_rows : V;
+#pragma omp parallel for schedule(static)
     for (int64_t k = 0; k < n_out; ++k) {
         const int64_t i = (w_rows != NULL) ? w_rows[k] : k;
         if (grow[i] < 0)
@@ -348,17 +369,27 @@ int ember_oracle_lmhead_grad(const uint16_t* dY, int64_t ldy, const uint16_t* H,
     if (V < 1 || D < 1 || T < 0 || ldy < V || ldh < D || ldg < D || G == NULL) return -1;
     if (T > 0 && (dY == NULL || H == NULL)) return -1;
     if (g_dtype != ORACLE_F32 && g_dtype != ORACLE_BF16) return -1;
-    double* acc = (double*)malloc((size_t)D * sizeof(double));
-    if (acc == NULL) return -1;
-    for (int64_t i = 0; i < V; ++i) {
-        for (int64_t j = 0; j < D; ++j) acc[j] = 0.0;
-        for (int64_t m = 0; m < T; ++m) {
-            const double y = ember_oracle_bf16_to_f64(dY[m * ldy + i]);
-            const uint16_t* h = H + m * ldh;
-            for (int64_t j = 0; j < D; ++j) acc[j] += y * ember_oracle_bf16_to_f64(h[j]);
+    int failed = 0;
+#pragma omp parallel
+    {
+        double* acc = (double*)malloc((size_t)D * sizeof(double));
+        if (acc == NULL) {
+#pragma omp atomic write
+            failed = 1;
         }
-        for (int64_t j = 0; j < D; ++j) store_elem(G, g_dtype, i * ldg + j, acc[j]);
+#pragma omp for schedule(static)
+        for (int64_t i = 0; i < V; ++i) {
+            if (acc == NULL)
+                continue;
+            for (int64_t j = 0; j < D; ++j) acc[j] = 0.0;
+            for (int64_t m = 0; m < T; ++m) {
+                const double y = ember_oracle_bf16_to_f64(dY[m * ldy + i]);
+                const uint16_t* h = H + m * ldh;
+                for (int64_t j = 0; j < D; ++j) acc[j] += y * ember_oracle_bf16_to_f64(h[j]);
+            }
+            for (int64_t j = 0; j < D; ++j) store_elem(G, g_dtype, i * ldg + j, acc[j]);
+        }
+        free(acc);
     }
-    free(acc);
-    return 0;
+    return failed ? -1 : 0;
 }
