@@ -8,17 +8,18 @@ scales), the input embedding a sparse-row step (8 x 2048 Zipf(1.1) token ids
 per step, ~4650 distinct rows).  All inputs are synthetic, made before the
 timed region and resident in HBM.
 
-By default both tables take their step in one ember_step_multi call (three
-launches shared by the two tables; the same bits as one call per table);
---schedule sequential times one call per table instead, and the line reports
-both schedules.
+By default both tables take their step in one ember_step_multi call (the
+sparse table's one-launch step, then statistics, finalize and apply launches
+of the dense table; the same bits as one call per table); --schedule
+sequential times one call per table instead, and the line reports both.
 
 Prints one JSON line: whole-step throughput in algorithmic GB/s (the bytes
 the method must move, see paper_2607_01455_amd.workloads.algorithmic_bytes),
-ms per step, per-part times, the roofline of the dominant kernel (the apply
-pass of the timed schedule, timed with HIP events around each launch; the
-single-table dense apply pass is reported beside it), torch's device copy
-for reference, the other table shapes, and the CPU oracle timed on a sample.
+ms per step, the dense LM-head step and the sparse embedding step each with
+its own ms, % of peak and kernel roofline, the roofline of the dominant
+kernel (the dense apply pass, timed with HIP events around each launch),
+torch's device copy and the library's streaming probe as reference rates,
+the other table shapes, and the CPU oracle on every host thread and on one.
 """
 import argparse
 import hashlib
@@ -41,6 +42,7 @@ MULTI_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ember_apply_multi_lmhead128
 ROWONLY_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ember_rowonly_lmhead128k_traffic.txt")
 LMHEAD_SRC = (os.path.join(CSRC, "ember_lmhead.hip"), os.path.join(CSRC, "ember_launch.h"))
 LMHEAD_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ember_lmhead_grad_lmhead128k_wgrad_traffic.txt")
+SPARSE_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ember_sparse_onchip_embed128k_traffic.txt")
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 
 
@@ -50,13 +52,13 @@ def parse():
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-rows", type=int, default=65536, help="rows of the oracle's sample")
+    p.add_argument("--cpu-rows", type=int, default=32768, help="rows of the single-thread oracle sample")
     p.add_argument("--no-other-configs", action="store_true")
     p.add_argument("--no-row-only", action="store_true")
     p.add_argument("--no-coalesce", action="store_true")
     p.add_argument("--no-lmhead-wgrad", action="store_true")
     p.add_argument("--schedule", choices=("multi", "sequential"), default="multi",
-                   help="multi: both tables in one ember_step_multi call (three launches); "
+                   help="multi: both tables in one ember_step_multi call; "
                         "sequential: ember_step_dense, then ember_step_sparse_rows")
     return p.parse_args()
 
@@ -95,31 +97,45 @@ def traffic_rate(traffic, ms):
     return None if traffic is None or not ms else round(traffic / (ms * 1e-3) / 1e9, 1)
 
 
-def cpu_baseline(rows: int, steps: int = 3):
-    """The oracle on the first `rows` rows of the LM-head table (dense, bf16)."""
+def cpu_baseline(dev, rows_1t: int, steps: int = 2):
+    """The oracle (float64 C, OpenMP over rows and column ranges) on the dense
+    LM-head step: on every thread it is given (the whole 128256-row table) and
+    on one thread (the first rows_1t rows), each for `steps` steps.  Inputs are
+    made on the device (the same generators as the GPU timing) and copied to
+    host memory before the oracle's timed calls."""
     import numpy as np
     import torch
 
     import oracle
     from paper_2607_01455_amd import workloads as wl
 
-    cfg = wl.Config("cpu_sample", rows, D, torch.bfloat16, torch.bfloat16, steps, "zipf_rows")
-    W = wl.make_weights(cfg, seed=21, device="cpu").contiguous().view(torch.int16).numpy().view(np.uint16).copy()
-    scales = (wl.zipf_probs(V) * V).float()[:rows]
-    r = np.zeros(rows, np.float32)
-    c = np.zeros(D, np.float32)
-    times = []
-    for t in range(1, steps + 1):
-        G = wl.make_dense_grad(cfg, t, seed=21, device="cpu", scales=scales)
-        G = G.contiguous().view(torch.int16).numpy().view(np.uint16)
-        t0 = time.perf_counter()
-        assert oracle.step(W, G, r, c, t) == 0
-        times.append(time.perf_counter() - t0)
-    sec = sum(times) / len(times)
-    gbps = wl.algorithmic_bytes(rows, D, 2, 2) / sec / 1e9
-    return {"value": round(gbps, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"dense bf16 step on the first {rows} of {V} LM-head rows x {D}, "
-                      f"{steps} steps, float64 C oracle, single thread; {sec * 1e3:.0f} ms/step"}
+    def run(rows, threads):
+        used = oracle.set_threads(threads)
+        cfg = wl.Config("cpu_sample", rows, D, torch.bfloat16, torch.bfloat16, steps, "zipf_rows")
+        W = wl.make_weights(cfg, seed=21, device=dev).contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+        scales = (wl.zipf_probs(V, device=dev) * V).float()[:rows]
+        r = np.zeros(rows, np.float32)
+        c = np.zeros(D, np.float32)
+        times = []
+        for t in range(1, steps + 1):
+            G = wl.make_dense_grad(cfg, t, seed=21, device=dev, scales=scales)
+            G = G.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+            t0 = time.perf_counter()
+            assert oracle.step(W, G, r, c, t) == 0
+            times.append(time.perf_counter() - t0)
+        sec = sum(times) / len(times)
+        return used, sec, wl.algorithmic_bytes(rows, D, 2, 2) / sec / 1e9
+
+    all_threads = oracle.set_threads(0)
+    used, sec, gbps = run(V, all_threads)
+    _, sec1, gbps1 = run(rows_1t, 1)
+    oracle.set_threads(all_threads)
+    return {"value": round(gbps, 4), "unit": "GB/s", "cores": used, "kind": "oracle",
+            "sample": f"dense bf16 LM-head step, all {V} rows x {D}, {steps} steps, float64 C oracle on "
+                      f"{used} threads: {sec * 1e3:.0f} ms/step",
+            "single_thread": {"value": round(gbps1, 4), "unit": "GB/s", "cores": 1,
+                              "sample": f"the first {rows_1t} of the {V} rows, {steps} steps: "
+                                        f"{sec1 * 1e3:.0f} ms/step"}}
 
 
 def other_configs(ember, wl, torch, dev, K):
@@ -481,15 +497,13 @@ def main():
     # apply pass: G read, W read and written, r and the column factors read
     apply_bytes = V * D * (2 + 2 * 2) + 4 * (V + D)
     apply_gbps = apply_bytes / (apply_avg_ms * 1e-3) / 1e9
-    # the multi-table apply launch: the dense pass above plus the sparse rows
-    # (G rows, W rows read and written, their r entries and int64 ids, column factors)
-    sparse_apply_bytes = sum(n * D * (2 + 2 * 2) + 12 * n + 4 * D for n in n_rows) / K
+    # the dense table's apply launch of the multi-table call (the sparse table
+    # takes its one-launch step in the same call)
     mapply_launches, mapply_ms = mstats["ember_apply_multi"]
     mapply_avg_ms = mapply_ms / mapply_launches
-    mapply_bytes = apply_bytes + sparse_apply_bytes
-    mapply_gbps = mapply_bytes / (mapply_avg_ms * 1e-3) / 1e9
+    mapply_gbps = apply_bytes / (mapply_avg_ms * 1e-3) / 1e9
     dense_roofline = {
-        "kernel": "ember_apply (dense LM-head step)",
+        "kernel": "ember_apply (dense LM-head step, apply pass)",
         "bound": "hbm",
         "achieved": round(apply_gbps, 1),
         "peak": PEAK_GBPS,
@@ -501,7 +515,7 @@ def main():
         "algorithmic_bytes_per_launch": apply_bytes,
     }
     multi_roofline = {
-        "kernel": "ember_apply_multi (LM head dense + embedding sparse rows, one launch)",
+        "kernel": "ember_apply_multi (dense LM-head table's apply pass inside the two-table call)",
         "bound": "hbm",
         "achieved": round(mapply_gbps, 1),
         "peak": PEAK_GBPS,
@@ -510,7 +524,30 @@ def main():
         "traffic": traffic_for_current_kernel(MULTI_TRAFFIC_FILE),
         "traffic_GBps": traffic_rate(traffic_for_current_kernel(MULTI_TRAFFIC_FILE), mapply_avg_ms),
         "avg_launch_ms": round(mapply_avg_ms, 5),
-        "algorithmic_bytes_per_launch": int(mapply_bytes),
+        "algorithmic_bytes_per_launch": apply_bytes,
+    }
+    # the sparse step's one launch: algorithmic bytes as the method counts them
+    # (G read twice, W rows read and written, r read and written, ids); the
+    # launch keeps its gradient rows in registers and reads them once, so it
+    # moves one G read less (bytes_moved_min)
+    sparse_launches, sparse_k_ms = sstats["ember_sparse_onchip"]
+    sparse_avg_ms = sparse_k_ms / sparse_launches
+    sparse_step_bytes = sum(sparse_bytes) / K
+    sparse_min_bytes = sum(wl.algorithmic_bytes(V, D, 2, 2, rows=n) - n * D * 2 for n in n_rows) / K
+    sparse_gbps = sparse_step_bytes / (sparse_avg_ms * 1e-3) / 1e9
+    sparse_roofline = {
+        "kernel": "ember_sparse_onchip (whole sparse step, one launch)",
+        "bound": "hbm",
+        "achieved": round(sparse_gbps, 1),
+        "peak": PEAK_GBPS,
+        "unit": "GB/s",
+        "frac": round(sparse_gbps / PEAK_GBPS, 4),
+        "traffic": traffic_for_current_kernel(SPARSE_TRAFFIC_FILE),
+        "traffic_GBps": traffic_rate(traffic_for_current_kernel(SPARSE_TRAFFIC_FILE), sparse_avg_ms),
+        "avg_launch_ms": round(sparse_avg_ms, 5),
+        "algorithmic_bytes_per_launch": int(sparse_step_bytes),
+        "bytes_moved_min": int(sparse_min_bytes),
+        "bytes_moved_min_GBps": round(sparse_min_bytes / (sparse_avg_ms * 1e-3) / 1e9, 1),
     }
 
     # --- plain device copy over a W-sized buffer: practical ceiling ----------
@@ -526,8 +563,10 @@ def main():
     c1.record(stream)
     torch.cuda.synchronize()
     copy_gbps = 2 * src.numel() * 2 / (c0.elapsed_time(c1) / 10 * 1e-3) / 1e9
-    # the library's streaming probe over the same bytes: practical ceilings of a
-    # pure read, a copy and two reads + one write (the apply pass's pattern)
+    # the library's streaming probe over the same bytes: rates of a plain
+    # grid-stride read, copy and two reads + one write (reference points, not
+    # ceilings: the apply pass, with several rows in flight per wavefront and
+    # part of G in the last-level cache, runs faster than the third)
     src2 = torch.empty_like(src).fill_(2.0)
     ceilings = {}
     for mode, name, ops in ((0, "read", 1), (1, "copy", 2), (2, "two_reads_one_write", 3)):
@@ -553,6 +592,7 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
+        "storage": "bf16 W and G, fp32 r and c",
         "data": "synthetic",
         "config": {
             "workload": "Ember step of both untied token tables, V=128256 x D=4096: "
@@ -568,11 +608,19 @@ def main():
         "schedules_ms_per_step": schedule_ms,
         "pct_of_peak": round(100.0 * value / PEAK_GBPS, 2),
         "parts": {
-            "dense_lmhead": {"ms": round(dense_ms, 4), "bytes": dense_bytes,
+            "dense_lmhead": {"workload": "LM head 128256 x 4096 bf16, dense step (three launches)",
+                             "ms": round(dense_ms, 4), "bytes": dense_bytes,
                              "GBps": round(dense_bytes / (dense_ms * 1e-3) / 1e9, 1),
-                             "pct_of_peak": round(100.0 * dense_bytes / (dense_ms * 1e-3) / 1e9 / PEAK_GBPS, 2)},
-            "sparse_embedding": {"ms": round(sparse_ms, 4), "bytes": int(sum(sparse_bytes) / K),
-                                 "GBps": round(sum(sparse_bytes) / K / (sparse_ms * 1e-3) / 1e9, 1)},
+                             "pct_of_peak": round(100.0 * dense_bytes / (dense_ms * 1e-3) / 1e9 / PEAK_GBPS, 2),
+                             "roofline": dense_roofline},
+            "sparse_embedding": {"workload": "input embedding 128256 x 4096 bf16, sparse-row step of an "
+                                             "8 x 2048-token Zipf(1.1) batch (one launch)",
+                                 "ms": round(sparse_ms, 4), "bytes": int(sparse_step_bytes),
+                                 "GBps": round(sparse_step_bytes / (sparse_ms * 1e-3) / 1e9, 1),
+                                 "pct_of_peak": round(100.0 * sparse_step_bytes / (sparse_ms * 1e-3) / 1e9
+                                                      / PEAK_GBPS, 2),
+                                 "rows_per_step": round(sum(n_rows) / K, 1),
+                                 "roofline": sparse_roofline},
         },
         "kernels_ms_avg": {
             "dense": {k: round(v[1] / v[0], 5) for k, v in dstats.items()},
@@ -582,9 +630,8 @@ def main():
         "ms_with_kernel_events": {"dense": round(dense_ms_events, 4), "sparse": round(sparse_ms_events, 4),
                                   "multi": round(multi_ms_events, 4)},
         "roofline": multi_roofline if args.schedule == "multi" else dense_roofline,
-        "roofline_dense_apply": dense_roofline,
         "torch_device_copy_GBps": round(copy_gbps, 1),
-        "stream_ceilings_GBps": ceilings,
+        "stream_probe_GBps": ceilings,
         "row_only": None,
         "coalesce": None,
         "lmhead_wgrad": None,
@@ -604,7 +651,7 @@ def main():
     if not args.no_other_configs:
         out["other_configs"] = other_configs(ember, wl, torch, dev, K)
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(args.cpu_rows)
+        out["cpu_baseline"] = cpu_baseline(dev, args.cpu_rows)
     print(json.dumps(out), flush=True)
 
 

@@ -1382,8 +1382,10 @@ struct OnchipParams {
     double inv_bias;
     double inv_alpha;       // 0 when lr == 0 (no weight is read or written)
     float eps_over_alpha;
-    int* slot;              // [V]: 1 + position in idx of a touched row, else 0
-    int* flag;              // error bits of this step
+    int* slot;              // [V]: marks of the rows of idx (0 between steps)
+    int* flag;              // error bits of the launches with an even epoch
+    int* flag_odd;          // error bits of the launches with an odd epoch (words of
+                            // their own: the other sparse paths keep theirs at zero)
     int* status;            // error bits of the last step (ember_get_error)
     unsigned* epoch;        // launches of this step so far (numbers the barriers)
     unsigned* arrive;       // [kOnchipBlocks * kArriveStride]: each block's last barrier number
@@ -1391,6 +1393,7 @@ struct OnchipParams {
     double* parts;          // [3][kOnchipBlocks]: per-block sums of the new r (untouched,
                             // touched rows) and of the new c
     float* qa;              // [D rounded up to 8]: column factors sqrt(c_j)
+    float* cnew;            // [D]: the new c, stored in phase 3
     int64_t spin_ticks;     // bound of a barrier wait in real-time counter ticks
 };
 
@@ -1474,7 +1477,7 @@ __global__ __launch_bounds__(kOnchipThreads, 1) void ember_sparse_onchip(OnchipP
     constexpr int kRowsMax = kOnchipWaves * U;        // rows of a block at most
     __shared__ float cl[kOnchipWaves][kWave * EPC];   // the waves' column sums, one chunk column
     __shared__ float rsl2[kRowsMax];                  // slab sums of g^2 of the block's rows
-    __shared__ int64_t id_lds[kRowsMax];              // ids of the block's rows
+    __shared__ int64_t id_lds[kRowsMax];              // ids of the block's rows (-1: out of range)
     __shared__ float ro_lds[kRowsMax];                // r of those rows before the step
     __shared__ float rn_lds[kRowsMax];                // r of those rows after the step
     __shared__ float part[kColGroups][16];            // column reduction
@@ -1488,11 +1491,16 @@ __global__ __launch_bounds__(kOnchipThreads, 1) void ember_sparse_onchip(OnchipP
     const int b = blockIdx.x;
     const int64_t V = a.V, D = a.D;
     if (threadIdx.x == 0) sh_epoch = *a.epoch;
+    __syncthreads();
+    // The error bits alternate between two words by launch, so block 0 can
+    // clear the next launch's word while this launch still reads its own.
+    const unsigned epoch = sh_epoch;
+    int* flag = (epoch & 1u) ? a.flag_odd : a.flag;
 
-    // ---- phase 1: load the rows, row and column sums of g^2, id checks ----
+    // ---- phase 1: load the rows, row and column sums of g^2, row marks ----
     bool bad_count = false;
     const int64_t n = active_rows(a.n_dev, a.rows, bad_count);
-    if (bad_count && b == 0 && threadIdx.x == 0) atomicOr(a.flag, kFlagCount);
+    if (bad_count && b == 0 && threadIdx.x == 0) atomicOr(flag, kFlagCount);
     int64_t r0, r1;
     row_range(n, NB, b, r0, r1);
     const int nloc = (int)(r1 - r0);
@@ -1510,7 +1518,8 @@ __global__ __launch_bounds__(kOnchipThreads, 1) void ember_sparse_onchip(OnchipP
     // 0 for an absent row): loads past the length return zero and stores past
     // it are dropped.  Lanes whose chunk lies outside the wave's slab get an
     // offset past every length.  Weight rows are only addressed through ids
-    // inside [0, V); every store further waits for the id checks of the step.
+    // inside [0, V), and nothing is stored before the step's error bits are
+    // final (phase 3).
     constexpr int kWChunkBytes = EPC * (int)sizeof(WT);
     constexpr int kOutside = 1 << 30;   // past the length of every row on this path
     int goff[M], woff[M];
@@ -1539,6 +1548,19 @@ __global__ __launch_bounds__(kOnchipThreads, 1) void ember_sparse_onchip(OnchipP
 #pragma unroll
         for (int m = 0; m < M; ++m) buf_load<GT, EPC>(gb, goff[m], graw[u][m]);
     }
+    // Row marks (lane u of each slab-0 wave, unit u's row): a count per id,
+    // read in phase 2 (0: untouched, 1: touched, more: a repeated id), so no
+    // result has to come back here; and r of the row, loaded before the weight
+    // rows so that waiting for it waits for the gradient rows only.
+    float rold = 0.0f;
+    if (slab == 0 && lrv) {
+        if (!lin) {
+            atomicOr(flag, kFlagRange);
+        } else {
+            __hip_atomic_fetch_add(a.slot + lid, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            rold = a.r[lid];
+        }
+    }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const int64_t i = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(lid >> 32), u) << 32) |
@@ -1547,20 +1569,6 @@ __global__ __launch_bounds__(kOnchipThreads, 1) void ember_sparse_onchip(OnchipP
         wb[u] = row_buffer(W + (wv[u] ? i : 0) * a.ldw, wv[u] && write_w ? wbytes : 0);
 #pragma unroll
         for (int m = 0; m < M; ++m) buf_load<WT, EPC>(wb[u], woff[m], wraw[u][m]);
-    }
-    // id checks: lane u of each slab-0 wave marks the row of unit u and reads
-    // its r; the result of the mark is looked at after the sums (waiting for it
-    // waits for every load issued before it)
-    int mark_bits = 0;
-    int prev_mark = 0;
-    float rold = 0.0f;
-    if (slab == 0 && lrv) {
-        if (!lin) {
-            mark_bits = kFlagRange;
-        } else {
-            prev_mark = atomicCAS(&a.slot[lid], 0, (int)(lrow + 1));
-            rold = a.r[lid];
-        }
     }
     // every load is issued before the first wait, and no decode moves above them
     __builtin_amdgcn_sched_barrier(0);
@@ -1597,13 +1605,6 @@ __global__ __launch_bounds__(kOnchipThreads, 1) void ember_sparse_onchip(OnchipP
         }
         __builtin_amdgcn_sched_barrier(0);
     }
-    if (prev_mark != 0) mark_bits |= kFlagDuplicate;
-    if (mark_bits) atomicOr(a.flag, mark_bits);
-    if (slab == 0 && lrv) {
-        const int t = q + Q * lane;
-        id_lds[t] = lin ? lid : -1;
-        ro_lds[t] = rold;
-    }
 
     // column sums of the block: the Q waves of each slab in order -> P[b]
     const __amdgpu_buffer_rsrc_t prs_w = __builtin_amdgcn_make_buffer_rsrc(a.P + (int64_t)b * D, 0, (int)(D * 4),
@@ -1635,6 +1636,12 @@ __global__ __launch_bounds__(kOnchipThreads, 1) void ember_sparse_onchip(OnchipP
         }
         __syncthreads();
     }
+    if (slab == 0 && lrv) {
+        const int t = q + Q * lane;
+        id_lds[t] = lin ? lid : -1;
+        ro_lds[t] = rold;
+    }
+    __syncthreads();
     // the block's rows: mean g^2 from the slab sums (slab order, float64),
     // the new r, and the sum of the new r in row order
     double tsum = 0.0;
@@ -1651,25 +1658,29 @@ __global__ __launch_bounds__(kOnchipThreads, 1) void ember_sparse_onchip(OnchipP
         tsum = onchip_block_sum((double)rn, dsum);
     }
 
-    const unsigned gen = 2u * sh_epoch + 1u;
-    const bool ok1 = grid_barrier(a.arrive, gen, a.spin_ticks, a.flag, a.status, &sh_ok);
+    const unsigned gen = 2u * epoch + 1u;
+    const bool ok1 = grid_barrier(a.arrive, gen, a.spin_ticks, flag, a.status, &sh_ok);
 
-    // ---- phase 2: c and the column factors; r of every row ----
+    // ---- phase 2: c and the column factors; r of every row (kept until phase 3) ----
     // Block b owns columns [c0, c1) and rows [v0, v1).  Each round takes 16
     // columns (thread (g, x) adds partials g, g + 32, ... of column c0 + x,
     // then 16 threads add the 32 group sums in group order) and 512 rows (one
-    // per thread: untouched rows decay, touched rows take the value their
-    // gradient row's block computed, marks are cleared); all loads of a
-    // round, and the error bits, are issued before the first is used.
+    // per thread: untouched rows decay, a count above one is a repeated id,
+    // marks are cleared); all loads of a round are issued before the first is
+    // used.  The new c and r are stored in phase 3, once the error bits are
+    // final.
+    const int64_t c0 = D * b / NB, c1 = D * (b + 1) / NB;
+    const int64_t v0 = V * b / NB, v1 = V * (b + 1) / NB;
+    // at least one round; the new values of the first round stay in registers
+    const int64_t rounds = max((int64_t)1, max((c1 - c0 + 15) / 16, (v1 - v0 + kOnchipThreads - 1) / kOnchipThreads));
+    float rn0 = 0.0f;
+    bool rn0_set = false;
     double csum = 0.0, usum = 0.0;
+    int dup = 0;
     {
-        const int64_t c0 = D * b / NB, c1 = D * (b + 1) / NB;
-        const int64_t v0 = V * b / NB, v1 = V * (b + 1) / NB;
         const int x = threadIdx.x % 16, g = threadIdx.x / 16;
         const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(a.P, 0, (int)(NB * D * 4), kBufferWord3);
         const int prow = kColGroups * (int)D * 4;
-        // at least one round: it also reads the error bits
-        const int64_t rounds = max((int64_t)1, max((c1 - c0 + 15) / 16, (v1 - v0 + kOnchipThreads - 1) / kOnchipThreads));
         for (int64_t k = 0; k < rounds; ++k) {
             const int64_t j = c0 + 16 * k + x;
             const bool jv = j < c1;
@@ -1681,138 +1692,151 @@ __global__ __launch_bounds__(kOnchipThreads, 1) void ember_sparse_onchip(OnchipP
             const float cold = (jv && g == 0) ? a.c[j] : 0.0f;
             const int64_t i = v0 + k * kOnchipThreads + threadIdx.x;
             const bool iv = i < v1;
-            const int sl = iv ? ld_agent_i(a.slot + i) : 0;
+            const int cnt = iv ? ld_agent_i(a.slot + i) : 0;
             const float ri = iv ? a.r[i] : 0.0f;
-            if (k == 0 && threadIdx.x == 0) sh_err = ld_agent_i(a.flag) | (ok1 ? 0 : kFlagTimeout);
             float sp = 0.0f;
 #pragma unroll
             for (int q2 = 0; q2 < NB / kColGroups; ++q2) sp += __uint_as_float(pv[q2]);
             part[g][x] = sp;
             __syncthreads();
-            const int err = sh_err;
             if (threadIdx.x < 16 && jv) {
                 float colsum = 0.0f;
                 for (int w = 0; w < kColGroups; ++w) colsum += part[w][x];
                 const float mean = (float)((double)colsum / (double)V);
                 const float cn = fmaf(a.beta2, cold, a.one_minus_beta2 * mean);
-                if (!err) {
-                    a.c[j] = cn;
-                    st_agent(a.qa + j, sqrtf(cn));
-                }
+                st_agent(a.qa + j, sqrtf(cn));
+                a.cnew[j] = cn;
                 csum += (double)cn;
             }
             if (iv) {
-                if (sl != 0) {
-                    a.slot[i] = 0;
-                } else if (!err) {
-                    const float rn = a.beta2 * ri;
-                    a.r[i] = rn;
-                    usum += (double)rn;
+                dup |= cnt > 1;
+                if (cnt == 0) usum += (double)(a.beta2 * ri);
+                // the first round's rows: the mark is cleared and the new r kept
+                // here; later rounds read their marks again in phase 3
+                if (k == 0) {
+                    if (cnt != 0) {
+                        a.slot[i] = 0;
+                    } else {
+                        rn0 = a.beta2 * ri;
+                        rn0_set = true;
+                    }
                 }
             }
-            if (k == 0 && !err && threadIdx.x < nloc && id_lds[threadIdx.x] >= 0)
-                a.r[id_lds[threadIdx.x]] = rn_lds[threadIdx.x];
             __syncthreads();   // part is reused by the next round
         }
     }
-    const int err = sh_err;
+    if (dup) atomicOr(flag, kFlagDuplicate);
     usum = onchip_block_sum(usum, dsum);
     if (threadIdx.x < kWave) csum = wave_sum(csum);
     if (threadIdx.x == 0) {
         st_agent_d(a.parts + b, usum);
         st_agent_d(a.parts + NB + b, tsum);
         st_agent_d(a.parts + 2 * NB + b, csum);
+        // the next launch's error bits start from zero
+        if (b == 0) *((epoch & 1u) ? a.flag : a.flag_odd) = 0;
     }
 
-    const bool ok2 = grid_barrier(a.arrive, gen + 1u, a.spin_ticks, a.flag, a.status, &sh_ok);
-    // every block has read the error bits: block 0 records them (keeping a
-    // timeout bit), clears them for the next step and numbers the next
-    // step's barriers
-    if (b == 0 && threadIdx.x == 0) {
-        atomicAnd(a.status, kFlagTimeout);
-        atomicOr(a.status, err);
-        *a.flag = 0;
-        *a.epoch = sh_epoch + 1u;
-    }
+    const bool ok2 = grid_barrier(a.arrive, gen + 1u, a.spin_ticks, flag, a.status, &sh_ok);
 
-    // ---- phase 3: s, then the update of the held weight rows ----
-    if (!err && ok2 && write_w) {
-        // column factors of this lane's chunks, and the per-block sums, in one
-        // round trip
-        const __amdgpu_buffer_rsrc_t qrs = __builtin_amdgcn_make_buffer_rsrc(a.qa, 0, (int)((D + 7) / 8 * 8 * 4),
-                                                                             kBufferWord3);
-        u32x4 qraw[M][EPC / 4];
+    // ---- phase 3: error bits, s, then every store of the step ----
+    // wave 0: the error bits and the per-block sums, then s and the step scale
+    // in a fixed order (every block alike); every wave: its column factors
+    const __amdgpu_buffer_rsrc_t qrs = __builtin_amdgcn_make_buffer_rsrc(a.qa, 0, (int)((D + 7) / 8 * 8 * 4),
+                                                                         kBufferWord3);
+    u32x4 qraw[M][EPC / 4];
+#pragma unroll
+    for (int m = 0; m < M; ++m) {
+        const int ch = cbeg + lane + kWave * m;
+        const int qoff = (on && ch < cend && write_w) ? ch * EPC * 4 : kOutside;
+#pragma unroll
+        for (int k = 0; k < EPC / 4; ++k)
+            qraw[m][k] = __builtin_bit_cast(u32x4,
+                                            __builtin_amdgcn_raw_buffer_load_b128(qrs, qoff + 16 * k, 0, kAgentScopeLoad));
+    }
+    if (threadIdx.x < kWave) {
+        const int fl = ld_agent_i(flag);
+        double pu[NB / kWave], pt[NB / kWave], pc[NB / kWave];
+#pragma unroll
+        for (int k = 0; k < NB / kWave; ++k) {
+            const int bb = lane * (NB / kWave) + k;
+            pu[k] = ld_agent_d(a.parts + bb);
+            pt[k] = ld_agent_d(a.parts + NB + bb);
+            pc[k] = ld_agent_d(a.parts + 2 * NB + bb);
+        }
+        double sr = 0.0, sc = 0.0;
+#pragma unroll
+        for (int k = 0; k < NB / kWave; ++k) {
+            sr += pu[k] + pt[k];
+            sc += pc[k];
+        }
+        sr = wave_sum(sr);
+        sc = wave_sum(sc);
+        if (threadIdx.x == 0) {
+            const int err = fl | (ok1 && ok2 ? 0 : kFlagTimeout);
+            sh_err = err;
+            const double mean_rhat = sr / (double)V * a.inv_bias;
+            const double mean_chat = sc / (double)D * a.inv_bias;
+            const double s = sqrt(mean_rhat * mean_chat);
+            sh_scale = s > 0.0 ? (float)(sqrt(a.inv_bias / s) * a.inv_alpha) : 0.0f;
+            // block 0 records the step's error bits (keeping a timeout bit) and
+            // numbers the next launch's barriers
+            if (b == 0) {
+                atomicAnd(a.status, kFlagTimeout);
+                atomicOr(a.status, err);
+                *a.epoch = epoch + 1u;
+            }
+        }
+    }
+    __syncthreads();
+    const int err = sh_err;
+    // rows beyond the first round: marks read again, cleared, r decayed
+    for (int64_t k = 1; k < rounds; ++k) {
+        const int64_t i = v0 + k * kOnchipThreads + threadIdx.x;
+        if (i >= v1) continue;
+        if (ld_agent_i(a.slot + i) != 0) a.slot[i] = 0;
+        else if (!err) a.r[i] = a.beta2 * a.r[i];
+    }
+    if (err) return;
+    // the state: this block's columns and rows
+    for (int64_t j = c0 + threadIdx.x; j < c1; j += kOnchipThreads) a.c[j] = a.cnew[j];
+    if (rn0_set) a.r[v0 + threadIdx.x] = rn0;
+    if (threadIdx.x < nloc && id_lds[threadIdx.x] >= 0) a.r[id_lds[threadIdx.x]] = rn_lds[threadIdx.x];
+    if (!write_w) return;
+    // the weight rows held since phase 1
+    const float scale = sh_scale;
+    const float epsa = a.eps_over_alpha;
+    const float ibias = (float)a.inv_bias;
+    float qv[M][EPC];
+#pragma unroll
+    for (int m = 0; m < M; ++m)
+#pragma unroll
+        for (int k = 0; k < EPC / 4; ++k) {
+            qv[m][4 * k] = __uint_as_float(qraw[m][k].x);
+            qv[m][4 * k + 1] = __uint_as_float(qraw[m][k].y);
+            qv[m][4 * k + 2] = __uint_as_float(qraw[m][k].z);
+            qv[m][4 * k + 3] = __uint_as_float(qraw[m][k].w);
+        }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        if (!wv[u]) continue;
+        const float ai = sqrtf(rn_lds[q + Q * u] * ibias) * scale;
 #pragma unroll
         for (int m = 0; m < M; ++m) {
-            const int ch = cbeg + lane + kWave * m;
-            const int qoff = (on && ch < cend) ? ch * EPC * 4 : kOutside;
+            // the words are decoded here and nowhere earlier
+            launder(graw[u][m]);
+            launder(wraw[u][m]);
+            float gx[EPC], wx[EPC], o[EPC];
+            decode(graw[u][m], gx);
+            decode(wraw[u][m], wx);
 #pragma unroll
-            for (int k = 0; k < EPC / 4; ++k)
-                qraw[m][k] = __builtin_bit_cast(
-                    u32x4, __builtin_amdgcn_raw_buffer_load_b128(qrs, qoff + 16 * k, 0, kAgentScopeLoad));
+            for (int e = 0; e < EPC; ++e) {
+                const float d = fmaf(ai, qv[m][e], epsa);
+                const float upd = fmaf(gx[e], __builtin_amdgcn_rcpf(d), wx[e]);
+                o[e] = (gx[e] == 0.0f) ? wx[e] : upd;
+            }
+            buf_store<WT, EPC>(wb[u], woff[m], o);
         }
-        // s from the per-block sums in a fixed order (every block alike):
-        // wave 0, lane l adds blocks 4l .. 4l + 3, then the lanes' sums
-        if (threadIdx.x < kWave) {
-            double pu[NB / kWave], pt[NB / kWave], pc[NB / kWave];
-#pragma unroll
-            for (int k = 0; k < NB / kWave; ++k) {
-                const int bb = lane * (NB / kWave) + k;
-                pu[k] = ld_agent_d(a.parts + bb);
-                pt[k] = ld_agent_d(a.parts + NB + bb);
-                pc[k] = ld_agent_d(a.parts + 2 * NB + bb);
-            }
-            double sr = 0.0, sc = 0.0;
-#pragma unroll
-            for (int k = 0; k < NB / kWave; ++k) {
-                sr += pu[k] + pt[k];
-                sc += pc[k];
-            }
-            sr = wave_sum(sr);
-            sc = wave_sum(sc);
-            if (threadIdx.x == 0) {
-                const double mean_rhat = sr / (double)V * a.inv_bias;
-                const double mean_chat = sc / (double)D * a.inv_bias;
-                const double s = sqrt(mean_rhat * mean_chat);
-                sh_scale = s > 0.0 ? (float)(sqrt(a.inv_bias / s) * a.inv_alpha) : 0.0f;
-            }
-        }
-        __syncthreads();
-        const float scale = sh_scale;
-        const float epsa = a.eps_over_alpha;
-        const float ibias = (float)a.inv_bias;
-        float qv[M][EPC];
-#pragma unroll
-        for (int m = 0; m < M; ++m)
-#pragma unroll
-            for (int k = 0; k < EPC / 4; ++k) {
-                qv[m][4 * k] = __uint_as_float(qraw[m][k].x);
-                qv[m][4 * k + 1] = __uint_as_float(qraw[m][k].y);
-                qv[m][4 * k + 2] = __uint_as_float(qraw[m][k].z);
-                qv[m][4 * k + 3] = __uint_as_float(qraw[m][k].w);
-            }
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            if (!wv[u]) continue;
-            const float ai = sqrtf(rn_lds[q + Q * u] * ibias) * scale;
-#pragma unroll
-            for (int m = 0; m < M; ++m) {
-                // the words are decoded here and nowhere earlier
-                launder(graw[u][m]);
-                launder(wraw[u][m]);
-                float gx[EPC], wx[EPC], o[EPC];
-                decode(graw[u][m], gx);
-                decode(wraw[u][m], wx);
-#pragma unroll
-                for (int e = 0; e < EPC; ++e) {
-                    const float d = fmaf(ai, qv[m][e], epsa);
-                    const float upd = fmaf(gx[e], __builtin_amdgcn_rcpf(d), wx[e]);
-                    o[e] = (gx[e] == 0.0f) ? wx[e] : upd;
-                }
-                buf_store<WT, EPC>(wb[u], woff[m], o);
-            }
-            __builtin_amdgcn_sched_barrier(0);   // one unit's decoded values at a time
-        }
+        __builtin_amdgcn_sched_barrier(0);   // one unit's decoded values at a time
     }
 }
 
@@ -1943,7 +1967,8 @@ WsLayout ws_layout(int64_t V, int64_t D) {
     L.ticket = off + 8;
     L.scale = off + 12;
     L.epoch = off + 16;
-    off = align256(20);
+    L.oflag = off + 20;
+    off = align256(28);
     L.arrive = off;
     off = align256(off + (size_t)kOnchipBlocks * kArriveStride * 4);
     L.slot = off;
@@ -1961,6 +1986,8 @@ WsLayout ws_layout(int64_t V, int64_t D) {
     off = align256(off + (size_t)nb * (size_t)D * 4);
     L.parts = off;
     off = align256(off + (size_t)3 * kOnchipBlocks * 8);
+    L.cnew = off;
+    off = align256(off + (size_t)D * 4);
     L.total = off;
     return L;
 }
@@ -2158,12 +2185,14 @@ OnchipSpace onchip_space(const StepArgs& a) {
     const WsLayout L = ws_layout(a.V, a.D);
     OnchipSpace sp;
     sp.base = a.ws;
-    sp.flag = L.flag;
+    sp.flag = L.oflag;
+    sp.flag_odd = L.oflag + 4;
     sp.status = L.status;
     sp.epoch = L.epoch;
     sp.arrive = L.arrive;
     sp.slot = L.slot;
     sp.qa = L.qa;
+    sp.cnew = L.cnew;
     sp.p = L.p;
     sp.parts = L.parts;
     sp.status_ptr = nullptr;
@@ -2195,12 +2224,14 @@ hipError_t launch_sparse_onchip(const StepArgs& a, const OnchipSpace& sp, hipStr
     p.eps_over_alpha = a.eps_over_alpha;
     p.slot = reinterpret_cast<int*>(sp.base + sp.slot);
     p.flag = reinterpret_cast<int*>(sp.base + sp.flag);
+    p.flag_odd = reinterpret_cast<int*>(sp.base + sp.flag_odd);
     p.status = sp.status_ptr ? sp.status_ptr : reinterpret_cast<int*>(sp.base + sp.status);
     p.epoch = reinterpret_cast<unsigned*>(sp.base + sp.epoch);
     p.arrive = reinterpret_cast<unsigned*>(sp.base + sp.arrive);
     p.P = reinterpret_cast<float*>(sp.base + sp.p);
     p.parts = reinterpret_cast<double*>(sp.base + sp.parts);
     p.qa = reinterpret_cast<float*>(sp.base + sp.qa);
+    p.cnew = reinterpret_cast<float*>(sp.base + sp.cnew);
     p.spin_ticks = a.spin_ticks;
     // A plain launch: the residency check above (blocks per compute unit x
     // compute units >= kOnchipBlocks) is what the grid barriers rely on, and
@@ -2233,10 +2264,11 @@ __global__ __launch_bounds__(kBlock) void ember_static_prep(uint32_t* p, int64_t
 
 size_t static_layout(int64_t V, int64_t D, OnchipSpace* sp) {
     size_t off = 0;
-    sp->flag = 0;
     sp->status = 4;
     sp->epoch = 16;
-    off = align256(20);
+    sp->flag = 20;
+    sp->flag_odd = 24;
+    off = align256(28);
     sp->arrive = off;
     off = align256(off + (size_t)kOnchipBlocks * kArriveStride * 4);
     sp->slot = off;
@@ -2248,6 +2280,8 @@ size_t static_layout(int64_t V, int64_t D, OnchipSpace* sp) {
     off = align256(off + (size_t)kOnchipBlocks * (size_t)D * 4);
     sp->parts = off;
     off = align256(off + (size_t)3 * kOnchipBlocks * 8);
+    sp->cnew = off;
+    off = align256(off + (size_t)D * 4);
     return off;
 }
 

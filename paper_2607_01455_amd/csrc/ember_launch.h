@@ -176,6 +176,7 @@ struct WsLayout {
     size_t ticket;  // int32: blocks of the finalize pass that have finished
     size_t scale;   // float: sqrt(1 / (bias s)) / alpha_s of the last step
     size_t epoch;   // uint32: one-launch sparse steps taken (numbers their grid barriers)
+    size_t oflag;   // int32[2]: error bits of the one-launch sparse steps, by epoch parity
     size_t arrive;  // uint32[kOnchipBlocks * kArriveStride]: last barrier number of each block
     size_t slot;    // int32[V]: 1 + position in idx of a touched row, else 0
     size_t zero_end;// [0, zero_end) must be zero before the first step
@@ -186,6 +187,7 @@ struct WsLayout {
     size_t p;       // float[max(row_blocks(V, nslab) over both dtypes, MT, kOnchipBlocks)][D]:
                     // per-block (or per-row-tile) column sums of g^2
     size_t parts;   // double[3][kOnchipBlocks]: per-block sums of the one-launch sparse step
+    size_t cnew;    // float[D]: the new c of the one-launch sparse step until its stores
     size_t total;
 };
 WsLayout ws_layout(int64_t V, int64_t D);
@@ -232,7 +234,7 @@ bool onchip_fits(const StepArgs& a);
 // Byte offsets (from base) of the regions the one-launch step uses.
 struct OnchipSpace {
     char* base;
-    size_t flag, status, epoch, arrive, slot, zero_end, qa, p, parts;
+    size_t flag, flag_odd, status, epoch, arrive, slot, zero_end, qa, p, parts, cnew;
     int* status_ptr;    // if set, the status word (else base + status)
 };
 OnchipSpace onchip_space(const StepArgs& a);       // in the caller's workspace
