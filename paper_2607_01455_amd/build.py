@@ -37,7 +37,7 @@ def _run(cmd, verbose: bool) -> None:
 
 def build(verbose: bool = False, extra_flags=(), out: str = LIB) -> str:
     """Compile and link the library to `out`; extra_flags go to every compile
-    (e.g. -DEMBER_APPLY_ROWS=8 to try another tuning constant)."""
+    (e.g. -O2, or -save-temps to inspect the code)."""
     objs = []
     tag = str(abs(hash((tuple(extra_flags), out))))
     try:

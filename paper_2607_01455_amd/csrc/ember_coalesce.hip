@@ -39,13 +39,14 @@ namespace {
 
 constexpr int kCoalThreads = 256;                    // 4 wavefronts
 constexpr int kCoalWaves = kCoalThreads / kWave;
-constexpr int kCoalItems = EMBER_COAL_ITEMS;         // keys per thread per tile
+constexpr int kCoalItems = 4;                        // keys per thread per tile
 constexpr int kTile = kCoalThreads * kCoalItems;     // keys per tile
 constexpr int kMaxDigitBits = 10;
 constexpr int kMaxBins = 1 << kMaxDigitBits;         // digits of up to 10 bits
 constexpr int kInBlockOffsetTiles = 64;              // up to this many tiles the
                                                      // scatter derives its own offsets
-constexpr int kRunRows = EMBER_COAL_RUN_ROWS;        // rows a wavefront holds at once
+constexpr int kRunRows = 16;                         // rows a wavefront holds at once
+constexpr int kMinChunkBatches = 2;                  // a chunk is at least this many batches
 constexpr int kMaxChunks = 4096;                     // bound on the chunks ...
 constexpr int64_t kMaxPartialElems = (int64_t)1 << 25; // ... and on chunks x D
 constexpr int kColsPerLane = 4;
@@ -86,12 +87,17 @@ __global__ __launch_bounds__(kCoalThreads) void coal_hist(SortPass a) {
     __syncthreads();
     const int64_t base = (int64_t)blockIdx.x * kTile;
     int bad = 0;
+    // every item's key is loaded before the first is counted
+    uint32_t key[kCoalItems];
+#pragma unroll
     for (int j = 0; j < kCoalItems; ++j) {
         const int64_t i = base + (int64_t)j * kCoalThreads + threadIdx.x;
-        if (i < a.P) {
-            const uint32_t key = key_of(a, i, bad);
-            atomicAdd(&h[(key >> a.shift) & (uint32_t)(bins - 1)], 1u);
-        }
+        key[j] = i < a.P ? key_of(a, i, bad) : 0u;
+    }
+#pragma unroll
+    for (int j = 0; j < kCoalItems; ++j) {
+        const int64_t i = base + (int64_t)j * kCoalThreads + threadIdx.x;
+        if (i < a.P) atomicAdd(&h[(key[j] >> a.shift) & (uint32_t)(bins - 1)], 1u);
     }
     if (bad) any_bad = 1;
     __syncthreads();
@@ -159,6 +165,21 @@ __global__ __launch_bounds__(kCoalThreads) void coal_scatter(SortPass a) {
     const int lane = t & (kWave - 1);
     const int wave = t / kWave;
 
+    // the tile's keys and values, loaded before the offsets are worked out
+    const int64_t base = (int64_t)tile * kTile;
+    uint32_t key[kCoalItems], val[kCoalItems];
+#pragma unroll
+    for (int j = 0; j < kCoalItems; ++j) {
+        const int64_t i = base + (int64_t)j * kCoalThreads + t;
+        int bad = 0;
+        key[j] = 0;
+        val[j] = 0;
+        if (i < a.P) {
+            key[j] = key_of(a, i, bad);
+            val[j] = a.tok != nullptr ? (uint32_t)i : a.vals_in[i];
+        }
+    }
+
     if (a.offs != nullptr) {
         for (int b = t; b < bins; b += kCoalThreads) off[b] = a.offs[(int64_t)b * a.ntiles + tile];
     } else {
@@ -173,6 +194,7 @@ __global__ __launch_bounds__(kCoalThreads) void coal_scatter(SortPass a) {
             tot[q] = 0;
             before[q] = 0;
             if (b < bins) {
+#pragma unroll 16
                 for (int k = 0; k < a.ntiles; ++k) {
                     const uint32_t c = a.hist[(int64_t)b * a.ntiles + k];
                     tot[q] += c;
@@ -197,17 +219,11 @@ __global__ __launch_bounds__(kCoalThreads) void coal_scatter(SortPass a) {
     __syncthreads();
 
     const uint64_t below = lane == 0 ? 0ull : (~0ull >> (kWave - lane));
-    const int64_t base = (int64_t)tile * kTile;
+#pragma unroll
     for (int j = 0; j < kCoalItems; ++j) {
         const int64_t i = base + (int64_t)j * kCoalThreads + t;
         const bool valid = i < a.P;
-        uint32_t key = 0, val = 0;
-        int bad = 0;
-        if (valid) {
-            key = key_of(a, i, bad);
-            val = a.tok != nullptr ? (uint32_t)i : a.vals_in[i];
-        }
-        const uint32_t d = (key >> a.shift) & (uint32_t)(bins - 1);
+        const uint32_t d = (key[j] >> a.shift) & (uint32_t)(bins - 1);
         uint64_t peers = __ballot(valid);
         for (int b = 0; b < a.bits; ++b) {
             const bool bit = (d >> b) & 1u;
@@ -230,8 +246,8 @@ __global__ __launch_bounds__(kCoalThreads) void coal_scatter(SortPass a) {
         __syncthreads();
         if (valid) {
             const uint32_t dst = off[d] + wexcl[wave][d] + rank;
-            a.keys_out[dst] = key;
-            a.vals_out[dst] = val;
+            a.keys_out[dst] = key[j];
+            a.vals_out[dst] = val[j];
         }
     }
 }
@@ -255,7 +271,23 @@ struct HeadParams {
     int* status;
 };
 
-__device__ __forceinline__ bool is_head(const uint32_t* K, int64_t k) { return k == 0 || K[k] != K[k - 1]; }
+// Head flags of a thread's kCoalItems sorted entries k0, k0 + 1, ...: the
+// entries and the one before them are loaded before any is compared.
+__device__ __forceinline__ uint32_t head_bits(const uint32_t* K, int64_t k0, int64_t P) {
+    uint32_t v[kCoalItems + 1];
+#pragma unroll
+    for (int e = 0; e <= kCoalItems; ++e) {
+        const int64_t k = k0 - 1 + e;
+        v[e] = (k >= 0 && k < P) ? K[k] : 0u;
+    }
+    uint32_t bits = 0;
+#pragma unroll
+    for (int e = 0; e < kCoalItems; ++e) {
+        const int64_t k = k0 + e;
+        if (k < P && (k == 0 || v[e + 1] != v[e])) bits |= 1u << e;
+    }
+    return bits;
+}
 
 // Tiles here are kTile consecutive sorted entries, kCoalItems per thread.
 // This launch also clears the count of chunks listed for the fixup.
@@ -263,9 +295,7 @@ __global__ __launch_bounds__(kCoalThreads) void coal_heads_count(HeadParams a) {
     __shared__ uint32_t lds[kCoalThreads];
     if (blockIdx.x == 0 && threadIdx.x == 0) *a.fix_count = 0;
     const int64_t k0 = (int64_t)blockIdx.x * kTile + (int64_t)threadIdx.x * kCoalItems;
-    uint32_t c = 0;
-    for (int e = 0; e < kCoalItems; ++e)
-        if (k0 + e < a.P && is_head(a.K, k0 + e)) ++c;
+    const uint32_t c = (uint32_t)__popc(head_bits(a.K, k0, a.P));
     uint32_t total;
     (void)block_excl_scan(c, lds, &total);
     if (threadIdx.x == 0) a.tilecnt[blockIdx.x] = total;
@@ -274,6 +304,8 @@ __global__ __launch_bounds__(kCoalThreads) void coal_heads_count(HeadParams a) {
 __global__ __launch_bounds__(kCoalThreads) void coal_heads_write(HeadParams a) {
     __shared__ uint32_t lds[kCoalThreads];
     __shared__ uint32_t tile_base;
+    const int64_t k0 = (int64_t)blockIdx.x * kTile + (int64_t)threadIdx.x * kCoalItems;
+    const uint32_t hb = head_bits(a.K, k0, a.P);
     if (a.tileoff != nullptr) {
         if (threadIdx.x == 0) tile_base = a.tileoff[blockIdx.x];
     } else {
@@ -284,22 +316,20 @@ __global__ __launch_bounds__(kCoalThreads) void coal_heads_write(HeadParams a) {
         if (threadIdx.x == 0) tile_base = total;
     }
     __syncthreads();
-    const int64_t k0 = (int64_t)blockIdx.x * kTile + (int64_t)threadIdx.x * kCoalItems;
-    uint32_t c = 0;
-    for (int e = 0; e < kCoalItems; ++e)
-        if (k0 + e < a.P && is_head(a.K, k0 + e)) ++c;
     uint32_t total;
-    const uint32_t excl = block_excl_scan(c, lds, &total);
+    const uint32_t excl = block_excl_scan((uint32_t)__popc(hb), lds, &total);
     uint32_t u = tile_base + excl;   // segment number of the next head
+#pragma unroll
     for (int e = 0; e < kCoalItems; ++e) {
         const int64_t k = k0 + e;
-        if (k >= a.P) break;
-        if (is_head(a.K, k)) {
-            a.idx[u] = (int64_t)a.K[k];
-            a.seg_start[u] = (uint32_t)k;
-            ++u;
+        if (k < a.P) {
+            if ((hb >> e) & 1u) {
+                a.idx[u] = (int64_t)a.K[k];
+                a.seg_start[u] = (uint32_t)k;
+                ++u;
+            }
+            a.uid[k] = u - 1;
         }
-        a.uid[k] = u - 1;
     }
     if (blockIdx.x == a.ntiles - 1) {
         // index errors (marked per tile by the first sort pass) -> status, n = -1
@@ -478,28 +508,37 @@ __global__ __launch_bounds__(kCoalThreads) void coal_segsum(SumParams a) {
     bool ends_crossing = false;
     if constexpr (kExact) {
         const int64_t colc = col_ok ? col : 0;
+        // ids, positions and segment numbers of a batch, one per lane (lane nr
+        // holds the id after the batch, if any); read back per row with lane
+        // reads instead of a memory round trip per row.  The next batch's are
+        // loaded behind the current batch's rows.
+        auto batch_meta = [&](int64_t s0, uint32_t& kv, uint32_t& pv, uint32_t& uv) {
+            const int nr = (int)min((int64_t)kRunRows, k1 - s0);
+            const int64_t kl = s0 + min(lane, nr);
+            const bool in = s0 < k1;
+            kv = in && lane <= nr && kl < a.P ? a.K[kl] : 0xFFFFFFFFu;
+            pv = in && lane < nr ? a.pos[kl] : 0u;
+            uv = in && lane < nr ? a.uid[kl] : 0u;
+        };
+        uint32_t kv, pv, uv;
+        batch_meta(k0, kv, pv, uv);
+        uint32_t kprev = 0;   // id of the row before the batch (read only past the chunk's first row)
         for (int64_t s0 = k0; s0 < k1; s0 += kRunRows) {
             const int nr = (int)min((int64_t)kRunRows, k1 - s0);
-            // ids, positions and segment numbers of the batch, one per lane (lane
-            // nr holds the id after the batch, if any); read back per row with
-            // lane reads instead of a memory round trip per row
-            const int64_t kl = s0 + min(lane, nr);
-            const bool have = lane <= nr && kl < a.P;
-            const uint32_t kv = have ? a.K[kl] : 0xFFFFFFFFu;
-            const uint32_t pv = lane < nr ? a.pos[kl] : 0u;
-            const uint32_t uv = lane < nr ? a.uid[kl] : 0u;
             raw rows[kRunRows];
 #pragma unroll
             for (int r = 0; r < kRunRows; ++r) {
                 const uint32_t p = (uint32_t)__builtin_amdgcn_readlane((int)pv, r < nr ? r : 0);
                 rows[r] = *reinterpret_cast<const raw*>(U + (int64_t)p * a.ldu + colc);
             }
+            uint32_t kn, pn, un;
+            batch_meta(s0 + kRunRows, kn, pn, un);
 #pragma unroll
             for (int r = 0; r < kRunRows; ++r) {
                 const int64_t k = s0 + r;
                 if (r < nr) {
                     const uint32_t kr = (uint32_t)__builtin_amdgcn_readlane((int)kv, r);
-                    if (k > run0 && (r == 0 ? a.K[k - 1] != kr
+                    if (k > run0 && (r == 0 ? kprev != kr
                                             : (uint32_t)__builtin_amdgcn_readlane((int)kv, r - 1) != kr)) {
                         run0 = k;
 #pragma unroll
@@ -522,6 +561,10 @@ __global__ __launch_bounds__(kCoalThreads) void coal_segsum(SumParams a) {
                     }
                 }
             }
+            kprev = (uint32_t)__builtin_amdgcn_readlane((int)kv, kRunRows - 1);
+            kv = kn;
+            pv = pn;
+            uv = un;
         }
     } else {
         for (int64_t k = k0; k < k1; ++k) {
@@ -556,6 +599,7 @@ __global__ __launch_bounds__(kCoalThreads) void coal_segsum(SumParams a) {
 // at a time; the grid walks the (listed chunk, column slab) items.  The
 // list order varies from run to run; each item's result does not.
 constexpr int kFixBatch = 64;
+constexpr int kFixBlocks = 1024;
 
 template <typename GT>
 __global__ __launch_bounds__(kCoalThreads) void coal_fixup(SumParams a) {
@@ -616,8 +660,9 @@ CoalPlan coal_plan(int64_t P, int64_t V, int64_t D) {
     c.digit_bits = (bits + c.passes - 1) / c.passes;
     int64_t maxc = kMaxPartialElems / (D > 0 ? D : 1);
     maxc = maxc < 1 ? 1 : (maxc > kMaxChunks ? kMaxChunks : maxc);
-    const int64_t m = (P + (int64_t)kRunRows * maxc - 1) / ((int64_t)kRunRows * maxc);
-    c.L = (int64_t)kRunRows * (m < 1 ? 1 : m);
+    int64_t m = (P + (int64_t)kRunRows * maxc - 1) / ((int64_t)kRunRows * maxc);
+    if (m < kMinChunkBatches) m = kMinChunkBatches;
+    c.L = (int64_t)kRunRows * m;
     c.nchunks = (int)((P + c.L - 1) / c.L);
     c.nslabs = (int)((D + kSlabCols - 1) / kSlabCols);
     size_t off = 256;   // status words, shared layout with the step workspace
@@ -762,7 +807,9 @@ hipError_t launch_coalesce(const CoalArgs& a, hipStream_t s) {
     if (e != hipSuccess) return e;
     // one (listed chunk, 64-column slab) item per wavefront in the worst case
     const int64_t fix_items = (int64_t)c.nchunks * ((a.D + kWave - 1) / kWave);
-    const unsigned fix_blocks = (unsigned)min((fix_items + kCoalWaves - 1) / kCoalWaves, (int64_t)16384);
+    // (a grid-stride loop: the listed chunks are few, and a block that finds no
+    // item costs a launch slot)
+    const unsigned fix_blocks = (unsigned)min((fix_items + kCoalWaves - 1) / kCoalWaves, (int64_t)kFixBlocks);
     if (a.g_dtype == 0) coal_fixup<float><<<fix_blocks, kCoalThreads, 0, s>>>(m);
     else coal_fixup<uint16_t><<<fix_blocks, kCoalThreads, 0, s>>>(m);
     return hipGetLastError();

@@ -158,7 +158,7 @@ __device__ __forceinline__ void load_raw(const T* row, int64_t col, bool valid, 
 // 0) need no branch.  Lengths here are multiples of 16 bytes, so a chunk is
 // wholly inside or wholly outside.
 constexpr int kBufferWord3 = 0x00020000;  // raw 32-bit data format, gfx9 family
-constexpr int kCachePolicy = EMBER_ROWONLY_NT ? 2 : 0;  // 2: non-temporal
+constexpr int kCachePolicy = kRowOnlyNT ? 2 : 0;  // 2: non-temporal
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t row_buffer(const void* row, int bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(row), 0, bytes, kBufferWord3);
@@ -364,25 +364,17 @@ __device__ __forceinline__ int64_t active_rows(const int64_t* n_dev, int64_t row
     return bad ? 0 : n;
 }
 
-// Rows of row block b: b, b + nb, b + 2 nb, ... (interleaved: all blocks sweep
-// G together from low to high rows), or a contiguous range.  Either way the
-// set and order of rows of each block is fixed by (rows, nb).
+// Rows of row block b: a contiguous range, fixed by (rows, nb).
 struct RowSet {
     int64_t first, stride, count;
 };
 __device__ __forceinline__ RowSet stats_rows(int64_t rows, int nb, int b) {
     RowSet rs;
-    if (EMBER_STATS_INTERLEAVE) {
-        rs.first = b;
-        rs.stride = nb;
-        rs.count = rows > b ? (rows - b + nb - 1) / nb : 0;
-    } else {
-        int64_t r0, r1;
-        row_range(rows, nb, b, r0, r1);
-        rs.first = r0;
-        rs.stride = 1;
-        rs.count = r1 - r0;
-    }
+    int64_t r0, r1;
+    row_range(rows, nb, b, r0, r1);
+    rs.first = r0;
+    rs.stride = 1;
+    rs.count = r1 - r0;
     return rs;
 }
 
@@ -487,7 +479,7 @@ __device__ __forceinline__ void stats_block(const StatsParams& a, unsigned blk, 
         }
         // the registers of this batch are free: start the next batch's loads
         // before the cross-lane reduction
-        if (EMBER_STATS_PIPE && k0 + R < nk) load_batch(k0 + R);
+        if (k0 + R < nk) load_batch(k0 + R);
         const float tot = rows_sum<R>(rs, lane);
         constexpr int kLanesPerRow = kWave / R;
         const int j = lane / kLanesPerRow;
@@ -503,7 +495,6 @@ __device__ __forceinline__ void stats_block(const StatsParams& a, unsigned blk, 
                 }
             }
         }
-        if (!EMBER_STATS_PIPE && k0 + R < nk) load_batch(k0 + R);
         if (kWide && (k0 / R + 1) % (kWideRowsPerWave / R) == 0) gather();
     }
     if constexpr (kWide) {
@@ -850,8 +841,8 @@ __device__ __forceinline__ void apply_block(const ApplyParams& a, unsigned blk, 
 #pragma unroll
                 for (int m = 0; m < M; ++m) {
                     const int ch = cbeg + lane + kWave * m;
-                    load_raw<GT, EPC, EMBER_APPLY_NT>(grow, (int64_t)ch * EPC, rv && ch < cend, a.D, graw[j][m]);
-                    load_raw<WT, EPC, EMBER_APPLY_WNT>(wr[j], (int64_t)ch * EPC, rv && ch < cend, a.D, wraw[j][m]);
+                    load_raw<GT, EPC, kApplyNT>(grow, (int64_t)ch * EPC, rv && ch < cend, a.D, graw[j][m]);
+                    load_raw<WT, EPC, kApplyWNT>(wr[j], (int64_t)ch * EPC, rv && ch < cend, a.D, wraw[j][m]);
                 }
             }
 #pragma unroll
@@ -869,7 +860,7 @@ __device__ __forceinline__ void apply_block(const ApplyParams& a, unsigned blk, 
                         const float upd = fmaf(g[e], __builtin_amdgcn_rcpf(d), w[e]);
                         o[e] = (g[e] == 0.0f) ? w[e] : upd;
                     }
-                    if (ch < cend) store_chunk<WT, EPC, EMBER_APPLY_NT>(wr[j], (int64_t)ch * EPC, a.D, o);
+                    if (ch < cend) store_chunk<WT, EPC, kApplyNT>(wr[j], (int64_t)ch * EPC, a.D, o);
                 }
             }
         }
@@ -895,10 +886,10 @@ __global__ __launch_bounds__(kBlock) void ember_apply_multi(MultiParams<ApplyPar
 // over the rows, W += g / (sqrt(rhat_i) / alpha_s + eps / alpha_s)
 // ---------------------------------------------------------------------------
 
-constexpr int kRowOnlyRows = EMBER_ROWONLY_ROWS;         // rows in flight per block
+constexpr int kRowOnlyRows = 2;                          // rows in flight per block
 constexpr int kRowOnlyMaxWaves = 8;                      // waves per block
-constexpr int kRowOnlyRowsPerBlock = EMBER_ROWONLY_RPB;  // rows per block
-constexpr int kRowOnlyWaveRows = EMBER_ROWONLY_WAVE_ROWS; // rows in flight per wave (one-wave rows)
+constexpr int kRowOnlyRowsPerBlock = 16;                 // rows per block
+constexpr int kRowOnlyWaveRows = 2;                      // rows in flight per wave (one-wave rows)
 constexpr int kRowOnlyWaveChunks = 16 * kWave;           // longest row held by one wave, in chunks
 
 struct RowOnlyParams {
@@ -983,7 +974,7 @@ __device__ __forceinline__ void rowonly_rows(const RowOnlyParams& a, int64_t nro
                 const float upd = fmaf(g[e], rc, w[e]);
                 o[e] = (g[e] == 0.0f) ? w[e] : upd;
             }
-            store_chunk<WT, EPC, EMBER_ROWONLY_NT>(wrow_ptr, (int64_t)ch * EPC, a.D, o);
+            store_chunk<WT, EPC, kRowOnlyNT>(wrow_ptr, (int64_t)ch * EPC, a.D, o);
         };
 
         Raw<GT, EPC> graw[R][S][M];
@@ -1000,8 +991,8 @@ __device__ __forceinline__ void rowonly_rows(const RowOnlyParams& a, int64_t nro
                     for (int m = 0; m < M; ++m) {
                         const int ch = cbeg + lane + kWave * m;
                         const bool v = rv[j] && slab < a.nslab && ch < cend;
-                        load_raw<GT, EPC, EMBER_ROWONLY_NT>(gr[j], (int64_t)ch * EPC, v, a.D, graw[j][q][m]);
-                        load_raw<WT, EPC, EMBER_ROWONLY_NT>(wr[j], (int64_t)ch * EPC, v && update, a.D,
+                        load_raw<GT, EPC, kRowOnlyNT>(gr[j], (int64_t)ch * EPC, v, a.D, graw[j][q][m]);
+                        load_raw<WT, EPC, kRowOnlyNT>(wr[j], (int64_t)ch * EPC, v && update, a.D,
                                                             wraw[j][q][m]);
                     }
                 }
@@ -1154,7 +1145,7 @@ __device__ __forceinline__ void rowonly_wave_rows(const RowOnlyParams& a, int64_
             for (int c = 0; c < C; ++c) {
                 const int ch = lane + kWave * c;
                 if constexpr (kExact) buf_load<GT, EPC>(gb[j], ch * 16, graw[j][c]);
-                else load_raw<GT, EPC, EMBER_ROWONLY_NT>(gr[j], (int64_t)ch * EPC, rv[j] && ch < a.total_chunks,
+                else load_raw<GT, EPC, kRowOnlyNT>(gr[j], (int64_t)ch * EPC, rv[j] && ch < a.total_chunks,
                                                          a.D, graw[j][c]);
             }
 #pragma unroll
@@ -1163,7 +1154,7 @@ __device__ __forceinline__ void rowonly_wave_rows(const RowOnlyParams& a, int64_
             for (int c = 0; c < C; ++c) {
                 const int ch = lane + kWave * c;
                 if constexpr (kExact) buf_load<WT, EPC>(wb[j], ch * kWBytes, wraw[j][c]);
-                else load_raw<WT, EPC, EMBER_ROWONLY_NT>(wr[j], (int64_t)ch * EPC,
+                else load_raw<WT, EPC, kRowOnlyNT>(wr[j], (int64_t)ch * EPC,
                                                          rv[j] && ch < a.total_chunks && update, a.D, wraw[j][c]);
             }
         // Keep every load of the rows issued before the first wait.
@@ -1203,7 +1194,7 @@ __device__ __forceinline__ void rowonly_wave_rows(const RowOnlyParams& a, int64_
                     o[e] = (g[e] == 0.0f) ? w[e] : upd;
                 }
                 if constexpr (kExact) buf_store<WT, EPC>(wb[j], ch * kWBytes, o);
-                else store_chunk<WT, EPC, EMBER_ROWONLY_NT>(wr[j], (int64_t)ch * EPC, a.D, o);
+                else store_chunk<WT, EPC, kRowOnlyNT>(wr[j], (int64_t)ch * EPC, a.D, o);
             }
         }
     }
@@ -2015,10 +2006,8 @@ static StatsParams stats_params(const StepArgs& a) {
     p.nb = a.fin_nb > 0 ? a.fin_nb : row_blocks(a.rows, col_plan(a.D, a.g_dtype).nslab, a.sparse);
     {
         const double row_bytes = (double)a.D * (a.g_dtype == 0 ? 4 : 2);
-        const int64_t keep = (int64_t)((double)EMBER_STATS_KEEP_MB * 1048576.0 / row_bytes);
-        p.cached_from = EMBER_STATS_NT == 0 ? 0
-                      : EMBER_STATS_NT == 1 ? a.rows
-                      : (keep >= a.rows ? 0 : a.rows - keep);
+        const int64_t keep = (int64_t)((double)kStatsKeepMB * 1048576.0 / row_bytes);
+        p.cached_from = keep >= a.rows ? 0 : a.rows - keep;
     }
     p.rowpart = reinterpret_cast<float*>(a.ws + L.rowpart);
     p.P = reinterpret_cast<float*>(a.ws + L.p);

@@ -15,98 +15,22 @@ constexpr int kWave = 64;           // CDNA wavefront width
 constexpr int kBlock = 256;         // threads per block: 4 waves
 constexpr int kWaves = kBlock / kWave;
 
-// Tuning constants of the streaming kernels (compile-time).
-#ifndef EMBER_SLAB_CHUNKS
-#define EMBER_SLAB_CHUNKS 128       // 16-byte chunks of a row per block (2 KiB)
-#endif
-#ifndef EMBER_STATS_ROWS
-#define EMBER_STATS_ROWS 4          // rows in flight per wave, statistics pass
-#endif
-#ifndef EMBER_APPLY_ROWS
-#define EMBER_APPLY_ROWS 2          // rows in flight per wave, apply pass
-#endif
-#ifndef EMBER_APPLY_BATCHES
-#define EMBER_APPLY_BATCHES 1       // row batches per wave, apply pass
-#endif
-#ifndef EMBER_STATS_NT
-#define EMBER_STATS_NT 2            // gradient loads of the statistics pass: 0 cached,
-                                    // 1 non-temporal, 2 non-temporal except the last
-                                    // EMBER_STATS_KEEP_MB of rows (reused by apply)
-#endif
-#ifndef EMBER_STATS_KEEP_MB
-#define EMBER_STATS_KEEP_MB 224
-#endif
-#ifndef EMBER_APPLY_NT
-#define EMBER_APPLY_NT 1            // non-temporal gradient loads and weight stores in apply
-#endif
-#ifndef EMBER_STATS_INTERLEAVE
-#define EMBER_STATS_INTERLEAVE 0    // statistics pass: block b takes rows b, b + nb, ...
-                                    // (all blocks sweep G together), else a contiguous range
-#endif
-#ifndef EMBER_STATS_PIPE
-#define EMBER_STATS_PIPE 1          // statistics pass: issue the next batch's loads before
-                                    // reducing the current batch across lanes
-#endif
-#ifndef EMBER_SPARSE_ROWS_PER_BLOCK
-#define EMBER_SPARSE_ROWS_PER_BLOCK 32  // minimum gradient rows per block, sparse step
-#endif
-#ifndef EMBER_SPARSE_APPLY_BATCHES
-#define EMBER_SPARSE_APPLY_BATCHES 1  // row batches per wave, apply pass of the sparse step
-#endif
-#ifndef EMBER_APPLY_WNT
-#define EMBER_APPLY_WNT 1           // non-temporal weight loads in apply
-#endif
-#ifndef EMBER_ROWONLY_ROWS
-#define EMBER_ROWONLY_ROWS 2     // row-only kernel: rows in flight per block
-#endif
-#ifndef EMBER_ROWONLY_RPB
-#define EMBER_ROWONLY_RPB 16     // row-only kernel: rows per block
-#endif
-#ifndef EMBER_ROWONLY_WAVE_ROWS
-#define EMBER_ROWONLY_WAVE_ROWS 2 // row-only kernel, one wave per row: rows in flight per wave
-#endif
-#ifndef EMBER_ROWONLY_NT
-#define EMBER_ROWONLY_NT 1       // row-only kernel: non-temporal G/W loads and W stores
-#endif
-#ifndef EMBER_FIN_ROWS
-#define EMBER_FIN_ROWS 1         // finalize: rows of r per thread
-#endif
-#ifndef EMBER_FIN_COLS
-#define EMBER_FIN_COLS 64        // finalize: columns per column block (16, 32 or 64)
-#endif
-#ifndef EMBER_COAL_ITEMS
-#define EMBER_COAL_ITEMS 4       // gradient coalescing: keys per thread per sort tile
-#endif
-#ifndef EMBER_COAL_RUN_ROWS
-#define EMBER_COAL_RUN_ROWS 32   // gradient coalescing: rows a wavefront sums per batch of loads
-#endif
-#ifndef EMBER_LMHEAD_STAGES
-#define EMBER_LMHEAD_STAGES 2    // LM-head gradient GEMM: LDS stages (token steps in flight)
-#endif
-#ifndef EMBER_LMHEAD_SCHED
-#define EMBER_LMHEAD_SCHED 1     // LM-head gradient GEMM: interleave MFMAs with the next operand reads
-#endif
-#ifndef EMBER_LMHEAD_DMA_ASM
-#define EMBER_LMHEAD_DMA_ASM 1   // LM-head gradient GEMM: LDS-direct loads as inline assembly
-#endif
-#ifndef EMBER_LMHEAD_WAVES
-#define EMBER_LMHEAD_WAVES 8     // LM-head gradient GEMM: wavefronts per 256 x 256 tile (4 or 8)
-#endif
-#ifndef EMBER_LMHEAD_GROUP_M
-#define EMBER_LMHEAD_GROUP_M 2   // LM-head gradient GEMM: row tiles per group of the tile order
-#endif
-#ifndef EMBER_MAX_BLOCKS
-#define EMBER_MAX_BLOCKS 384        // row blocks of the statistics pass
-#endif
-
-constexpr int kSlabChunks = EMBER_SLAB_CHUNKS;
-constexpr int kStatsRows = EMBER_STATS_ROWS;
-constexpr int kApplyRows = EMBER_APPLY_ROWS;
-constexpr int kApplyBatches = EMBER_APPLY_BATCHES;
-constexpr int kMaxBlocks = EMBER_MAX_BLOCKS;
+// Tuning constants of the kernels (measured choices; compile-time).
+constexpr int kSlabChunks = 128;    // 16-byte chunks of a row per block (2 KiB)
+constexpr int kStatsRows = 4;       // rows in flight per wave, statistics pass
+constexpr int kApplyRows = 2;       // rows in flight per wave, apply pass
+constexpr int kApplyBatches = 1;    // row batches per wave, apply pass
+constexpr int kStatsKeepMB = 224;   // the statistics pass loads G non-temporally except its last
+                                    // kStatsKeepMB of rows, which stay cached for the apply pass
+constexpr bool kApplyNT = true;     // apply pass: non-temporal gradient loads and weight stores
+constexpr bool kApplyWNT = true;    // apply pass: non-temporal weight loads
+constexpr int kSparseRowsPerBlock = 32;   // minimum gradient rows per block, sparse step
+constexpr int kSparseApplyBatches = 1;    // row batches per wave, apply pass of the sparse step
+constexpr bool kRowOnlyNT = true;   // row-only kernels: non-temporal G/W loads and W stores
+constexpr int kMaxBlocks = 384;     // row blocks of the statistics pass
 constexpr int kRowsPerBlockMin = 8; // fewer rows than this per block: fewer blocks
-constexpr int kVRowsPerThread = EMBER_FIN_ROWS;  // rows per thread in the r pass of finalize
-constexpr int kFinCols = EMBER_FIN_COLS;         // columns per column block of finalize
+constexpr int kVRowsPerThread = 1; // rows per thread in the r pass of finalize
+constexpr int kFinCols = 64;        // columns per column block of finalize (16, 32 or 64)
 constexpr int kDecayRows = 1024;    // rows per decay block of the row-only sparse step
 constexpr int64_t kMaxGridBlocks = (int64_t)1 << 20;  // launched blocks per kernel at most
 int64_t capped_blocks(int64_t blocks);
@@ -114,10 +38,7 @@ int64_t capped_blocks(int64_t blocks);
 // LM-head gradient GEMM tiles (ember_lmhead.hip): kLmheadTile x kLmheadTile
 // tiles of G, kLmheadK tokens per step.
 constexpr int kLmheadTile = 256;
-#ifndef EMBER_LMHEAD_K
-#define EMBER_LMHEAD_K 64        // LM-head gradient GEMM: tokens per step
-#endif
-constexpr int kLmheadK = EMBER_LMHEAD_K;
+constexpr int kLmheadK = 64;        // tokens per step
 
 // Status bits written by the sparse statistics pass.
 constexpr int kFlagRange = 1;
@@ -146,7 +67,7 @@ struct ColPlan {
 // produce more column partials than gradient.
 constexpr int64_t kStatsMinBlocks = 1024;
 inline int row_blocks(int64_t rows, int nslab, bool sparse = false) {
-    const int64_t per = sparse ? EMBER_SPARSE_ROWS_PER_BLOCK : kRowsPerBlockMin;
+    const int64_t per = sparse ? kSparseRowsPerBlock : kRowsPerBlockMin;
     int64_t nb = (rows + per - 1) / per;
     int64_t cap = kStatsMinBlocks / (nslab > 0 ? nslab : 1);
     if (cap < kMaxBlocks) cap = kMaxBlocks;
@@ -162,7 +83,7 @@ inline int nslab_for(int64_t D) {
 // Row blocks of the apply pass (any count gives the same bits).  The sparse
 // step has few rows, so its blocks are smaller to spread them over the chip.
 inline int apply_blocks(int64_t rows, bool sparse = false) {
-    const int64_t per = (int64_t)kWaves * kApplyRows * (sparse ? EMBER_SPARSE_APPLY_BATCHES : kApplyBatches);
+    const int64_t per = (int64_t)kWaves * kApplyRows * (sparse ? kSparseApplyBatches : kApplyBatches);
     int64_t nb = (rows + per - 1) / per;
     return (int)(nb < 1 ? 1 : nb);
 }

@@ -44,20 +44,21 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
-constexpr int kGemmWaves = EMBER_LMHEAD_WAVES;  // wavefronts per block: 4 or 8
+constexpr int kGemmWaves = 8;                   // wavefronts per block
 constexpr int kThreads = kGemmWaves * kWave;
 constexpr int kWavesN = 2;                      // wave grid over the tile: kWavesM x 2
 constexpr int kWavesM = kGemmWaves / kWavesN;
 constexpr int kBM = kLmheadTile;        // rows of G per block (vocabulary)
 constexpr int kBN = kLmheadTile;        // columns of G per block (hidden)
 constexpr int kBK = kLmheadK;           // tokens per step
-constexpr int kStages = EMBER_LMHEAD_STAGES;  // LDS stages (steps in flight)
+constexpr int kStages = 2;                      // LDS stages (steps in flight)
+constexpr int kGroupM = 2;                      // row tiles per group of the tile order
 constexpr int kRowBytes = kBM * 2;              // one token's 256 bf16 of one operand
 constexpr int kOperandBytes = kBK * kRowBytes;  // one operand's slice of a step
 constexpr int kStageBytes = 2 * kOperandBytes;  // dY slice, then H slice
 constexpr int kRowsPerLoad = kWave * 16 / kRowBytes;            // rows one wave-wide load fills (2)
 constexpr int kLoadsPerWave = kBK / kRowsPerLoad / kGemmWaves;  // per operand and step
-constexpr int kWaveRows = kBM / kWavesM;        // rows of one wave's part of the tile (128 or 64)
+constexpr int kWaveRows = kBM / kWavesM;        // rows of one wave's part of the tile (64)
 constexpr int kWaveCols = kBN / kWavesN;        // its columns (128)
 constexpr int kMT = kWaveRows / 32;             // 32 x 32 MFMA tiles per wave: kMT x kNT
 constexpr int kNT = kWaveCols / 32;
@@ -66,11 +67,11 @@ constexpr int kBufferWord3 = 0x00020000;  // raw 32-bit data format, gfx9 family
 
 static_assert(kBM == kBN, "both operand slices share one LDS layout");
 static_assert(kBM == 256 && kBK % 16 == 0, "wave tiling assumes 256 x 256 tiles");
-static_assert(kGemmWaves == 4 || kGemmWaves == 8, "4 or 8 wavefronts per block");
+static_assert(kGemmWaves == 8, "8 wavefronts per block");
 static_assert(kStages >= 2 && kLoadsPerWave * kRowsPerLoad * kGemmWaves == kBK, "load split");
 static_assert(kStages * kStageBytes <= 160 * 1024, "LDS of one CU");
 static_assert((kStages - 2) * 2 * kLoadsPerWave < 64, "vmcnt range");
-static_assert(kStages == 2 || kStages == 4 || kStages == 5, "stage rings of 2, 4 or 5");
+static_assert(kStages == 2, "a ring of two stages");
 
 struct Params {
     const uint16_t* dY;   // [T][ldy] bf16
@@ -128,7 +129,7 @@ __device__ __forceinline__ void tile_of(const Params& a, int64_t l, int& tm, int
 // that share a row.  Last, the waves that share rows (or columns) add their
 // partials in a fixed order through LDS.
 template <typename GT>
-constexpr int kStripRows = (kGemmWaves == 8 && sizeof(GT) == 4) ? 16 : 32;
+constexpr int kStripRows = sizeof(GT) == 4 ? 16 : 32;
 template <typename GT>
 constexpr int kStripPitch = 128 * (int)sizeof(GT) + 16;    // bytes per strip row (padded)
 template <typename GT>
@@ -258,7 +259,6 @@ __device__ __forceinline__ void epilogue(const Params& a, int tm, int tn, f32x16
 // the LDS base (wave-uniform) for the load and is restored afterwards; one
 // wait state separates its write from the load.
 __device__ __forceinline__ void load_to_lds(__amdgpu_buffer_rsrc_t rs, const void* lds_base, int voffset) {
-#if EMBER_LMHEAD_DMA_ASM
     const uint32_t base = __builtin_amdgcn_readfirstlane(
         (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)lds_base);
     uint32_t saved;
@@ -267,9 +267,6 @@ __device__ __forceinline__ void load_to_lds(__amdgpu_buffer_rsrc_t rs, const voi
                  : "=&s"(saved)
                  : "s"(base), "v"(voffset), "s"(rs)
                  : "memory");
-#else
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)lds_base, 16, voffset, 0, 0, 0);
-#endif
 }
 
 // Wait until at most N vector-memory loads of this wave are outstanding
@@ -294,29 +291,10 @@ __global__ __launch_bounds__(kThreads) void ember_lmhead_grad(Params a) {
     // whole rows, as the LDS-direct load requires (lane l -> base + 16 l).
     __shared__ __attribute__((aligned(1024))) uint8_t lds0[kStageBytes];
     __shared__ __attribute__((aligned(1024))) uint8_t lds1[kStageBytes];
-#if EMBER_LMHEAD_STAGES > 2
-    __shared__ __attribute__((aligned(1024))) uint8_t lds2[kStageBytes];
-#endif
-#if EMBER_LMHEAD_STAGES > 3
-    __shared__ __attribute__((aligned(1024))) uint8_t lds3[kStageBytes];
-#endif
-#if EMBER_LMHEAD_STAGES > 4
-    __shared__ __attribute__((aligned(1024))) uint8_t lds4[kStageBytes];
-#endif
     auto stage = [&](auto sc) -> uint8_t* {
         constexpr int k = decltype(sc)::value;
         if constexpr (k == 0) return lds0;
-        else if constexpr (k == 1) return lds1;
-#if EMBER_LMHEAD_STAGES > 2
-        else if constexpr (k == 2) return lds2;
-#endif
-#if EMBER_LMHEAD_STAGES > 3
-        else if constexpr (k == 3) return lds3;
-#endif
-#if EMBER_LMHEAD_STAGES > 4
-        else if constexpr (k == 4) return lds4;
-#endif
-        else return nullptr;
+        else return lds1;
     };
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
@@ -433,9 +411,7 @@ __global__ __launch_bounds__(kThreads) void ember_lmhead_grad(Params a) {
                 for (int nt = 0; nt < kNT; ++nt)
                     acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][mt], bfr[cur][nt], acc[mt][nt],
                                                                           0, 0, 0);
-#if EMBER_LMHEAD_SCHED
-            // each MFMA followed by its share of the next sub-step's transpose
-            // reads (one with 4 wavefronts, two with 8)
+            // each MFMA followed by its share of the next sub-step's transpose reads
             if (kk + 1 < kBK / 16) {
                 constexpr int kM = kMT * kNT, kR = 2 * (kMT + kNT);
                 constexpr int kRpm = (kR + kM - 1) / kM;   // reads after each MFMA
@@ -447,32 +423,17 @@ __global__ __launch_bounds__(kThreads) void ember_lmhead_grad(Params a) {
                         if (i * kRpm + q < kR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
                 }
             }
-#endif
             __builtin_amdgcn_sched_barrier(0);
         }
     };
-    // steps 0 .. kStages - 2 before the loop; step kStages - 1 is issued by step 0
+    // step 0 before the loop; step 1 is issued by step 0
     issue(0, lds0);
-#if EMBER_LMHEAD_STAGES > 2
-    issue(1, lds1);
-    issue(2, lds2);
-#endif
-#if EMBER_LMHEAD_STAGES > 4
-    issue(3, lds3);
-#endif
     // whole rounds of kStages steps (one loop exit keeps the accumulators in
     // place); the up to kStages - 1 steps past the last one multiply the zeros
     // their loads wrote, which adds exact zeros
     for (int64_t kt = 0; kt < nk; kt += kStages) {
         step(kt, std::integral_constant<int, 0>{});
         step(kt + 1, std::integral_constant<int, 1>{});
-#if EMBER_LMHEAD_STAGES > 2
-        step(kt + 2, std::integral_constant<int, 2>{});
-        step(kt + 3, std::integral_constant<int, 3>{});
-#endif
-#if EMBER_LMHEAD_STAGES > 4
-        step(kt + 4, std::integral_constant<int, 4>{});
-#endif
     }
     wait_vmcnt<0>();   // the zero-filling loads past the end, before the LDS is reused
     // epilogue scratch: wave w's strip in stage array w % kStages (after the
@@ -482,14 +443,7 @@ __global__ __launch_bounds__(kThreads) void ember_lmhead_grad(Params a) {
     constexpr int kStripsPerArray = (kGemmWaves + kStages - 1) / kStages;
     static_assert(kStripsPerArray * kStrip + kRedBytes <= kStageBytes, "epilogue scratch fits the stages");
     const int sarr = wave % kStages;
-    uint8_t* const sbase = sarr == 0 ? lds0 : sarr == 1 ? lds1
-#if EMBER_LMHEAD_STAGES > 2
-                                   : sarr == 2 ? lds2 : sarr == 3 ? lds3
-#endif
-#if EMBER_LMHEAD_STAGES > 4
-                                   : sarr == 4 ? lds4
-#endif
-                                   : lds0;
+    uint8_t* const sbase = sarr == 0 ? lds0 : lds1;
     uint8_t* const strip = sbase + (wave / kStages) * kStrip;
     uint8_t* const red = lds1 + kStripsPerArray * kStrip;
     epilogue<GT>(a, tm, tn, acc, strip, red);
@@ -520,7 +474,7 @@ hipError_t launch_lmhead_grad(const LmheadArgs& x, hipStream_t s) {
     p.P = x.P;
     p.MT = pl.MT;
     p.NT = pl.NT;
-    p.group_m = EMBER_LMHEAD_GROUP_M;
+    p.group_m = kGroupM;
     const int64_t total = (int64_t)pl.MT * pl.NT;
     const int64_t per_launch = kMaxGridBlocks;   // a multiple of kXcds
     for (int64_t t0 = 0; t0 < total; t0 += per_launch) {
