@@ -231,9 +231,10 @@ int ember_step_sparse_rows_static(void* W, int w_dtype, int64_t ldw,
  * add launches of their own.
  *
  * Errors: each table is checked as its own call would be, and additionally
- * the tables' workspaces, state vectors and weight matrices must not overlap
- * one another (EMBER_ERR_ARG); 1 <= n_tables <= EMBER_MAX_TABLES
- * (EMBER_ERR_ARG).  A failed check enqueues nothing for any table.  Index
+ * no memory one table writes (workspace, r, c, W) may overlap memory another
+ * table reads or writes (those, and G, idx, the device row count), since the
+ * tables share launches (EMBER_ERR_ARG); memory the tables only read may be
+ * shared.  1 <= n_tables <= EMBER_MAX_TABLES (EMBER_ERR_ARG).  A failed check enqueues nothing for any table.  Index
  * errors of a sparse table leave that table untouched (the others step
  * normally) and are reported by ember_get_error on its workspace.
  */

@@ -199,13 +199,43 @@ int check_table(const ember_table_step& x) {
     return st;
 }
 
-// The memory one table writes: workspace, r, c and W.
-void table_spans(const ember_table_step& x, Span out[4]) {
+// Bytes of a rows x D matrix with leading dimension ld (0 rows: none).
+size_t matrix_bytes(int64_t rows, int64_t ld, int64_t D, int dtype) {
+    return rows > 0 ? ((size_t)(rows - 1) * (size_t)ld + (size_t)D) * dtype_size(dtype) : 0;
+}
+
+// The memory one table writes: workspace, r, c and W ...
+constexpr int kWriteSpans = 4;
+void table_write_spans(const ember_table_step& x, Span out[kWriteSpans]) {
     out[0] = span_of(x.ws, ember::ws_layout(x.V, x.D).total);
     out[1] = span_of(x.r, (size_t)x.V * 4);
     out[2] = x.row_only ? span_of(nullptr, 0) : span_of(x.c, (size_t)x.D * 4);
-    const size_t es = dtype_size(x.w_dtype);
-    out[3] = span_of(x.W, ((size_t)(x.V - 1) * (size_t)x.ldw + (size_t)x.D) * es);
+    out[3] = span_of(x.W, matrix_bytes(x.V, x.ldw, x.D, x.w_dtype));
+}
+
+// ... and the memory it only reads: G (V rows, or the n_idx rows of a sparse
+// step), the id list and the device row count.
+constexpr int kReadSpans = 3;
+void table_read_spans(const ember_table_step& x, Span out[kReadSpans]) {
+    const int64_t rows = x.sparse ? x.n_idx : x.V;
+    out[0] = span_of(x.G, matrix_bytes(rows, x.ldg, x.D, x.g_dtype));
+    out[1] = x.sparse ? span_of(x.idx, (size_t)(x.n_idx > 0 ? x.n_idx : 0) * 8) : span_of(nullptr, 0);
+    out[2] = x.sparse && x.n_idx_dev != nullptr ? span_of(x.n_idx_dev, 8) : span_of(nullptr, 0);
+}
+
+// Whether a span table i writes overlaps any span of table j.
+bool writes_overlap(const ember_table_step& i, const ember_table_step& j) {
+    Span wi[kWriteSpans], wj[kWriteSpans], rj[kReadSpans];
+    table_write_spans(i, wi);
+    table_write_spans(j, wj);
+    table_read_spans(j, rj);
+    for (const Span& a : wi) {
+        for (const Span& b : wj)
+            if (overlap(a, b)) return true;
+        for (const Span& b : rj)
+            if (overlap(a, b)) return true;
+    }
+    return false;
 }
 
 // Launches of one phase: tables in `order`, grouped by kernel key in order of
@@ -367,17 +397,11 @@ int ember_step_multi(const ember_table_step* tables, int n_tables, hipStream_t s
         const int st = check_table(tables[i]);
         if (st != EMBER_OK) return st;
     }
-    for (int i = 0; i < n_tables; ++i) {
-        Span si[4];
-        table_spans(tables[i], si);
-        for (int j = i + 1; j < n_tables; ++j) {
-            Span sj[4];
-            table_spans(tables[j], sj);
-            for (int x = 0; x < 4; ++x)
-                for (int y = 0; y < 4; ++y)
-                    if (overlap(si[x], sj[y])) return EMBER_ERR_ARG;
-        }
-    }
+    // no table may write memory another table reads or writes (the tables
+    // share launches, so such a pair would race); read-only spans may be shared
+    for (int i = 0; i < n_tables; ++i)
+        for (int j = 0; j < n_tables; ++j)
+            if (i != j && writes_overlap(tables[i], tables[j])) return EMBER_ERR_ARG;
     std::vector<StepArgs> args((size_t)n_tables);
     for (int i = 0; i < n_tables; ++i) {
         const ember_table_step& x = tables[i];

@@ -26,3 +26,17 @@ def pytest_collection_modifyitems(config, items):
     for item in items:
         if "gpu" in item.keywords:
             item.add_marker(skip)
+
+
+def pytest_terminal_summary(terminalreporter):
+    # how many W elements the parity tests let through on the update-size bar
+    mod = sys.modules.get("parity_checks")
+    if mod is None:
+        return
+    for kind, (calls, checked, through) in mod.cancel_tally.items():
+        if not calls:
+            continue
+        cap = f"; cap {mod.CANCEL_CAP:.0e} per call" if kind == "bf16" else ""
+        terminalreporter.write_line(
+            f"W {kind}: {through} of {checked} checked elements passed through the update-size bar "
+            f"({through / max(checked, 1):.2e}{cap}) over {calls} comparisons")

@@ -26,21 +26,58 @@ def ordered16(b: np.ndarray) -> np.ndarray:
     return np.where(b & 0x8000, 0x8000 - (b & 0x7FFF), 0x8000 + b)
 
 
-def check_w(got: np.ndarray, want: np.ndarray, prev: np.ndarray, what: str) -> None:
+# W bars.  The library's update term g / (sqrt(rhat chat / s) + eps) uses its
+# own r and c, which agree with the oracle's to 1e-5 (check_state), so the
+# term itself may differ by ~1e-5 of its size; the fp32 arithmetic around it
+# adds ~2^-23 of |W_prev|.  Hence:
+# * fp32: |W - W_ref| <= 1e-5 max(|W_ref|, |W_prev - W_ref|), the update's
+#   size standing in when the update cancels most of W_prev; elements that
+#   pass only through the update's size are counted and printed.
+# * bf16: within one ulp of W_ref (the final rounding dominates), except where
+#   the update cancelled the previous weight, |W_ref| < 2^-7 |W_prev| (the
+#   error above reaches one bf16 ulp only far below that), and then within
+#   1e-5 max(|W_ref|, |W_prev - W_ref|).  These elements are counted and
+#   capped: at most CANCEL_CAP of the checked elements per call, with a floor
+#   of CANCEL_FLOOR elements for small samples (at the ~1e-6 rate seen over
+#   whole tables, 5 or more in 3e5 elements has a chance of about 1e-4).
+# Session totals are printed at the end of the run.
+CANCEL_RATIO_BF16 = 2.0 ** -7
+CANCEL_CAP = 2e-6
+CANCEL_FLOOR = 4
+cancel_tally = {"bf16": [0, 0, 0], "fp32": [0, 0, 0]}   # calls, checked, through the update bar
+
+
+def check_w(got: np.ndarray, want: np.ndarray, prev: np.ndarray, what: str) -> int:
+    """W against the oracle by the bars above; returns the number of elements
+    that passed through the update-size bar."""
     if got.dtype == np.uint16:
-        d = np.abs(ordered16(got) - ordered16(want))
-        bad = d > 1
-        if bad.any():
-            gv, wv, pv = (bf16_values(x[bad]) for x in (got, want, prev))
-            cancel_ok = np.abs(gv - wv) <= 1e-5 * np.maximum(np.abs(wv), np.abs(pv))
-            assert cancel_ok.all(), (
-                f"{what}: {(~cancel_ok).sum()} bf16 elements differ by > 1 ulp outside cancellation "
-                f"(max {d.max()} ulp); first: got {gv[~cancel_ok][:3]} want {wv[~cancel_ok][:3]} prev {pv[~cancel_ok][:3]}")
+        beyond = np.abs(ordered16(got) - ordered16(want)) > 1
+        gv, wv, pv = (bf16_values(x[beyond]) for x in (got, want, prev))
+        upd_ok = np.abs(gv - wv) <= 1e-5 * np.maximum(np.abs(wv), np.abs(pv - wv))
+        ok = (np.abs(wv) < CANCEL_RATIO_BF16 * np.abs(pv)) & upd_ok
+        assert ok.all(), (
+            f"{what}: {(~ok).sum()} bf16 elements beyond one ulp without cancellation; "
+            f"first: got {gv[~ok][:3]} want {wv[~ok][:3]} prev {pv[~ok][:3]}")
+        cap = max(CANCEL_FLOOR, int(np.ceil(CANCEL_CAP * got.size)))
     else:
-        tol = 1e-5 * np.maximum(np.abs(want), np.abs(prev))
-        err = np.abs(got.astype(np.float64) - want.astype(np.float64))
-        bad = ~(err <= tol)
-        assert not bad.any(), f"{what}: {bad.sum()} fp32 elements out of tolerance (max err {err.max()})"
+        g64, w64, p64 = got.astype(np.float64), want.astype(np.float64), prev.astype(np.float64)
+        err = np.abs(g64 - w64)
+        ok = err <= 1e-5 * np.maximum(np.abs(w64), np.abs(p64 - w64))
+        assert ok.all(), (f"{what}: {(~ok).sum()} fp32 elements beyond 1e-5 of max(|W_ref|, |update|); "
+                          f"max err {err.max()}")
+        beyond = ~(err <= 1e-5 * np.abs(w64))
+        cap = None
+    k = int(beyond.sum())
+    tally = cancel_tally["bf16" if got.dtype == np.uint16 else "fp32"]
+    tally[0] += 1
+    tally[1] += int(got.size)
+    tally[2] += k
+    if k:
+        print(f"  {what}: {k} of {got.size} elements passed through the update-size bar"
+              + (f" (cap {cap})" if cap is not None else ""), flush=True)
+    if cap is not None:
+        assert k <= cap, f"{what}: {k} cancellation elements of {got.size}, above the cap of {cap}"
+    return k
 
 
 def check_state(got: torch.Tensor, want: np.ndarray, what: str) -> None:

@@ -353,6 +353,14 @@ def test_multi_step_rejects_table_counts_and_overlaps(em):
     assert _multi(em, [good, _table(em, base=16 * A, W=W_ + 128)]) == em.EMBER_ERR_ARG
     assert _multi(em, [good, _table(em, base=16 * A, c=WS_ + 256)]) == em.EMBER_ERR_ARG
     assert _multi(em, [good, good]) == em.EMBER_ERR_ARG
+    # one table's written memory over another table's gradient, id list or row count
+    assert _multi(em, [good, _table(em, base=16 * A, W=G_)]) == em.EMBER_ERR_ARG
+    assert _multi(em, [good, _table(em, base=16 * A, G=W_ + 256)]) == em.EMBER_ERR_ARG
+    sparse = dict(sparse=1, idx=IDX_ + 16 * A, n_idx=3)
+    assert _multi(em, [good, _table(em, base=16 * A, **dict(sparse, idx=R_))]) == em.EMBER_ERR_ARG
+    assert _multi(em, [_table(em, base=16 * A, **sparse), _table(em, r=IDX_ + 16 * A + 8)]) == em.EMBER_ERR_ARG
+    devn = dict(sparse, n_idx_dev=IDX_ + 17 * A)
+    assert _multi(em, [_table(em, base=16 * A, **devn), _table(em, c=IDX_ + 17 * A)]) == em.EMBER_ERR_ARG
 
 
 def test_stream_probe_rejects_bad_arguments_on_host(em):

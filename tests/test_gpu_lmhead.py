@@ -114,6 +114,41 @@ def test_lmhead_step_matches_the_oracle(em, T, V, D, gd, wd, steps):
     run_steps(em, T, V, D, gd, wd, steps, seed=T + V + D)
 
 
+@pytest.mark.parametrize("T,V,D,gd", [
+    (1, 1, 1, torch.bfloat16),
+    (64, 256, 256, torch.bfloat16),
+    (200, 600, 520, torch.bfloat16),   # ragged rows, columns and tokens
+    (130, 513, 264, torch.float32),
+    (70, 300, 1001, torch.float32),    # D not a multiple of 8
+    (300, 1000, 72, torch.bfloat16),
+])
+def test_lmhead_grad_exact_sums_are_bitwise_the_oracle(em, T, V, D, gd):
+    """Entries k / 16 with integer |k| <= 32 (exact in bf16): every product is a
+    multiple of 2^-8 of magnitude <= 4, so every fp32 partial sum of up to 300
+    of them is exact, in any order.  The library's G is then the exact sum
+    rounded once, which is what oracle.lmhead_grad computes: bit for bit."""
+    print(f"lmhead exact sums T={T} V={V} D={D} G={gd}", flush=True)
+    gen = torch.Generator().manual_seed(T * 7 + V + D)
+    dY = _padded(T, V, torch.bfloat16, 1)
+    H = _padded(T, D, torch.bfloat16, 2)
+    dY.copy_((torch.randint(-32, 33, (T, V), generator=gen).float() / 16).to(DEV))
+    H.copy_((torch.randint(-32, 33, (T, D), generator=gen).float() / 16).to(DEV))
+    cfg = wl.Config("lmh_exact", V, D, torch.bfloat16, gd, 1, "logits", batch_tokens=T)
+    W = _padded(V, D, torch.bfloat16, 1)
+    W.copy_(wl.make_weights(cfg, seed=T, device=DEV))
+    G = _padded(V, D, gd, 1)
+    tab = em.EmberTable(V, D, device=DEV)
+    em.ember_lmhead_step(W, dY, H, G, tab.r, tab.c, 1, LR, B2, EPS, False, tab.ws)
+    torch.cuda.synchronize()
+    want = oracle.lmhead_grad(host_bits(dY), host_bits(H), np.uint16 if gd == torch.bfloat16 else np.float32)
+    got = host_bits(G)
+    if gd == torch.float32:
+        got, want = got.view(np.uint32), want.view(np.uint32)
+    diff = got != want
+    assert not diff.any(), (f"{int(diff.sum())} of {got.size} G elements differ from the exactly summed oracle; "
+                            f"first at {np.argwhere(diff)[:3].tolist()}")
+
+
 def test_padding_never_reaches_a_stored_value(em):
     run_steps(em, 100, 700, 300, torch.bfloat16, torch.bfloat16, 2, seed=9, ldy_pad=3, ldh_pad=5, nan_pad=True)
 
