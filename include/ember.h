@@ -418,13 +418,15 @@ typedef struct {
 int ember_profile_enable(int enable);
 
 /*
- * Streaming probe (diagnostics): the practical HBM ceilings the passes above
- * are measured against.  Enqueues one grid-stride kernel with 16-byte
- * non-temporal accesses over `bytes` bytes of each operand:
+ * Streaming probe (diagnostics): reference rates of plain streaming kernels
+ * over the same bytes as the passes above (not ceilings: the passes keep more
+ * rows in flight per wavefront, and the apply pass finds part of G in the
+ * last-level cache, so it runs faster than mode 2).  Enqueues one grid-stride
+ * kernel with 16-byte non-temporal accesses over `bytes` bytes of each operand:
  *   mode 0: reads a (dst receives at most 4 bytes, in practice none);
  *   mode 1: dst <- a (copy);
- *   mode 2: dst <- a + b in 32-bit integer lanes (two reads, one write: the
- *           apply pass's access pattern).
+ *   mode 2: dst <- a + b in 32-bit integer lanes (two reads, one write, as
+ *           the apply pass reads G and W and writes W).
  * dst, a (and b for mode 2) are device pointers, 16-byte aligned, each
  * covering `bytes`, which must be a multiple of 16; dst must not overlap a
  * or b.  Returns EMBER_ERR_ARG (mode or null pointer), EMBER_ERR_SHAPE,

@@ -49,7 +49,7 @@ constexpr int kRunRows = 16;                         // rows a wavefront holds a
 constexpr int kMinChunkBatches = 2;                  // a chunk is at least this many batches
 constexpr int kMaxChunks = 4096;                     // bound on the chunks ...
 constexpr int64_t kMaxPartialElems = (int64_t)1 << 25; // ... and on chunks x D
-constexpr int kColsPerLane = 4;
+constexpr int kColsPerLane = 4;                      // columns per lane (4 or 8)
 constexpr int kSlabCols = kWave * kColsPerLane;      // columns per wavefront
 
 struct SortPass {
@@ -370,22 +370,21 @@ struct SumParams {
     uint32_t* fix_count;      // entries of fix_list (cleared by the heads launch)
 };
 
-template <typename T> struct Cols;
-template <> struct Cols<float> {
-    using raw = uint32_t __attribute__((ext_vector_type(4)));
+// One lane's kColsPerLane columns of a row: its words, widened to float64.
+template <typename T> struct Cols {
+    static constexpr int kWords = kColsPerLane * (int)sizeof(T) / 4;
+    using raw = uint32_t __attribute__((ext_vector_type(kWords)));
     static __device__ __forceinline__ void widen(const raw& r, double (&x)[kColsPerLane]) {
-        x[0] = (double)__uint_as_float(r.x); x[1] = (double)__uint_as_float(r.y);
-        x[2] = (double)__uint_as_float(r.z); x[3] = (double)__uint_as_float(r.w);
+#pragma unroll
+        for (int w = 0; w < kWords; ++w) {
+            if constexpr (sizeof(T) == 4) {
+                x[w] = (double)__uint_as_float(r[w]);
+            } else {
+                x[2 * w] = (double)__uint_as_float(r[w] << 16);
+                x[2 * w + 1] = (double)__uint_as_float(r[w] & 0xFFFF0000u);
+            }
+        }
     }
-    static __device__ __forceinline__ float elem(const float* p) { return *p; }
-};
-template <> struct Cols<uint16_t> {
-    using raw = uint32_t __attribute__((ext_vector_type(2)));
-    static __device__ __forceinline__ void widen(const raw& r, double (&x)[kColsPerLane]) {
-        x[0] = (double)__uint_as_float(r.x << 16); x[1] = (double)__uint_as_float(r.x & 0xFFFF0000u);
-        x[2] = (double)__uint_as_float(r.y << 16); x[3] = (double)__uint_as_float(r.y & 0xFFFF0000u);
-    }
-    static __device__ __forceinline__ float elem(const uint16_t* p) { return __uint_as_float((uint32_t)*p << 16); }
 };
 
 // float64 -> bf16, one round-to-nearest-even: round to fp32 with round-to-odd
@@ -447,16 +446,24 @@ __device__ __forceinline__ void buf_store_cols(void* G, int64_t ldg, uint32_t u,
                                                const double (&x)[kColsPerLane]) {
     GT* row = static_cast<GT*>(G) + (int64_t)u * ldg;
     const __amdgpu_buffer_rsrc_t rs = row_rsrc(row, D * (int64_t)sizeof(GT));
+    using v4 = decltype(__builtin_amdgcn_raw_buffer_load_b128(rs, 0, 0, 0));
+    using v2 = decltype(__builtin_amdgcn_raw_buffer_load_b64(rs, 0, 0, 0));
     if constexpr (sizeof(GT) == 4) {
-        using v4 = decltype(__builtin_amdgcn_raw_buffer_load_b128(rs, 0, 0, 0));
-        const uint32_t w0 = __float_as_uint((float)x[0]), w1 = __float_as_uint((float)x[1]);
-        const uint32_t w2 = __float_as_uint((float)x[2]), w3 = __float_as_uint((float)x[3]);
-        __builtin_amdgcn_raw_buffer_store_b128(v4{w0, w1, w2, w3}, rs, col * 4, 0, 0);
+#pragma unroll
+        for (int g = 0; g < kColsPerLane; g += 4) {
+            const uint32_t w0 = __float_as_uint((float)x[g]), w1 = __float_as_uint((float)x[g + 1]);
+            const uint32_t w2 = __float_as_uint((float)x[g + 2]), w3 = __float_as_uint((float)x[g + 3]);
+            __builtin_amdgcn_raw_buffer_store_b128(v4{w0, w1, w2, w3}, rs, (col + g) * 4, 0, 0);
+        }
     } else {
-        using v2 = decltype(__builtin_amdgcn_raw_buffer_load_b64(rs, 0, 0, 0));
-        const uint32_t w0 = (uint32_t)f64_to_bf16(x[0]) | ((uint32_t)f64_to_bf16(x[1]) << 16);
-        const uint32_t w1 = (uint32_t)f64_to_bf16(x[2]) | ((uint32_t)f64_to_bf16(x[3]) << 16);
-        __builtin_amdgcn_raw_buffer_store_b64(v2{w0, w1}, rs, col * 2, 0, 0);
+        uint32_t w[kColsPerLane / 2];
+#pragma unroll
+        for (int e = 0; e < kColsPerLane / 2; ++e)
+            w[e] = (uint32_t)f64_to_bf16(x[2 * e]) | ((uint32_t)f64_to_bf16(x[2 * e + 1]) << 16);
+        if constexpr (kColsPerLane == 8)
+            __builtin_amdgcn_raw_buffer_store_b128(v4{w[0], w[1], w[2], w[3]}, rs, col * 2, 0, 0);
+        else
+            __builtin_amdgcn_raw_buffer_store_b64(v2{w[0], w[1]}, rs, col * 2, 0, 0);
     }
 }
 
@@ -501,7 +508,7 @@ __global__ __launch_bounds__(kCoalThreads) void coal_segsum(SumParams a) {
     const bool began_before = k0 > 0 && a.K[k0] == a.K[k0 - 1];
     const bool ends_after = k1 < a.P && a.K[k1] == a.K[k1 - 1];
 
-    double acc[kColsPerLane] = {0.0, 0.0, 0.0, 0.0};
+    double acc[kColsPerLane] = {};
     int64_t run0 = k0;
     // the chunk's first segment began earlier and ends here: list the chunk
     // for the launch that adds the pieces (once, from the first slab)

@@ -1,10 +1,12 @@
-// Streaming probe kernels: the practical HBM ceilings that the Ember passes
-// are measured against (a diagnostic beside the method, not part of it).
+// Streaming probe kernels: reference rates of plain streaming over the same
+// bytes as the Ember passes (a diagnostic beside the method, not part of it,
+// and not a ceiling: the passes keep more rows in flight per wavefront, and
+// the apply pass finds part of G in the last-level cache).
 //
 // mode 0 reads a; mode 1 copies a to dst; mode 2 writes dst = a + b (32-bit
-// integer lanes): two reads and one write, the access pattern of the apply
-// pass.  16-byte non-temporal accesses, eight in flight per thread and operand,
-// over contiguous 32 KiB tiles.
+// integer lanes): two reads and one write, as the apply pass reads G and W
+// and writes W.  16-byte non-temporal accesses, eight in flight per thread
+// and operand, over contiguous 32 KiB tiles.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>

@@ -1,4 +1,4 @@
-"""GPU test of the streaming probe kernels (the ceilings the benchmark reports
+"""GPU test of the streaming probe kernels (the reference rates the benchmark reports
 beside the Ember passes): copy and two-operand add are checked element by
 element against torch, over sizes with a ragged grid-stride tail."""
 import pytest
