@@ -92,6 +92,17 @@ def traffic_for_current_kernel(path=TRAFFIC_FILE, src=KERNEL_SRC):
         return None
 
 
+def stats_kept_bytes(V: int, D: int, g_size: int) -> int:
+    """Bytes of G rows the statistics pass loads through the caches for the
+    apply pass to find in the last-level cache (its kStatsKeepMB tail, read
+    from the launch header), at most the whole of G."""
+    import re
+    with open(os.path.join(CSRC, "ember_launch.h")) as f:
+        mb = int(re.search(r"constexpr int kStatsKeepMB = (\d+);", f.read()).group(1))
+    row = D * g_size
+    return min(V, int(mb * 1048576 // row)) * row
+
+
 def traffic_rate(traffic, ms):
     """HBM GB/s from the PMC bytes per launch and the launch's average duration."""
     return None if traffic is None or not ms else round(traffic / (ms * 1e-3) / 1e9, 1)
@@ -502,6 +513,7 @@ def main():
     mapply_launches, mapply_ms = mstats["ember_apply_multi"]
     mapply_avg_ms = mapply_ms / mapply_launches
     mapply_gbps = apply_bytes / (mapply_avg_ms * 1e-3) / 1e9
+    kept_bytes = stats_kept_bytes(V, D, 2)
     dense_roofline = {
         "kernel": "ember_apply (dense LM-head step, apply pass)",
         "bound": "hbm",
@@ -513,6 +525,13 @@ def main():
         "traffic_GBps": traffic_rate(traffic_for_current_kernel(), apply_avg_ms),
         "avg_launch_ms": round(apply_avg_ms, 5),
         "algorithmic_bytes_per_launch": apply_bytes,
+        # achieved/frac count every algorithmic byte as HBM traffic; the G rows
+        # the statistics pass leaves in the last-level cache are read from it
+        # (no counter separates them), so the HBM-only estimate subtracts them
+        "llc_kept_bytes": kept_bytes,
+        "hbm_bytes_est": apply_bytes - kept_bytes,
+        "hbm_GBps_est": round((apply_bytes - kept_bytes) / (apply_avg_ms * 1e-3) / 1e9, 1),
+        "hbm_frac_est": round((apply_bytes - kept_bytes) / (apply_avg_ms * 1e-3) / 1e9 / PEAK_GBPS, 4),
     }
     multi_roofline = {
         "kernel": "ember_apply_multi (dense LM-head table's apply pass inside the two-table call)",
@@ -525,6 +544,10 @@ def main():
         "traffic_GBps": traffic_rate(traffic_for_current_kernel(MULTI_TRAFFIC_FILE), mapply_avg_ms),
         "avg_launch_ms": round(mapply_avg_ms, 5),
         "algorithmic_bytes_per_launch": apply_bytes,
+        "llc_kept_bytes": kept_bytes,
+        "hbm_bytes_est": apply_bytes - kept_bytes,
+        "hbm_GBps_est": round((apply_bytes - kept_bytes) / (mapply_avg_ms * 1e-3) / 1e9, 1),
+        "hbm_frac_est": round((apply_bytes - kept_bytes) / (mapply_avg_ms * 1e-3) / 1e9 / PEAK_GBPS, 4),
     }
     # the sparse step's one launch: algorithmic bytes as the method counts them
     # (G read twice, W rows read and written, r read and written, ids); the
