@@ -52,6 +52,8 @@ def parse():
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-configs", action="store_true",
+                   help="only time the oracle on every configuration (one thread and all threads) and print that")
     p.add_argument("--cpu-rows", type=int, default=32768, help="rows of the single-thread oracle sample")
     p.add_argument("--no-other-configs", action="store_true")
     p.add_argument("--no-row-only", action="store_true")
@@ -147,6 +149,77 @@ def cpu_baseline(dev, rows_1t: int, steps: int = 2):
             "single_thread": {"value": round(gbps1, 4), "unit": "GB/s", "cores": 1,
                               "sample": f"the first {rows_1t} of the {V} rows, {steps} steps: "
                                         f"{sec1 * 1e3:.0f} ms/step"}}
+
+
+def cpu_configs(dev, budget_s: float = 10.0):
+    """The oracle on every configuration (C1-C5 of the benchmark table): ms per
+    step on every host thread it is given and on one thread, the first step
+    from zero state.  On one thread a table whose step would take longer than
+    about budget_s is timed on its first rows (stated in the output).  Inputs
+    are the benchmark's generators, made on the device and copied to host
+    memory before the timed calls."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from paper_2607_01455_amd import workloads as wl
+
+    def host(t):
+        t = t.contiguous()
+        if t.dtype == torch.bfloat16:
+            return t.view(torch.int16).cpu().numpy().view(np.uint16)
+        return t.cpu().numpy()
+
+    def timed(fn, min_s=0.2):
+        n, t0 = 0, time.perf_counter()
+        while True:
+            fn()
+            n += 1
+            el = time.perf_counter() - t0
+            if el >= min_s or n >= 50:
+                return el / n * 1e3
+
+    all_threads = oracle.set_threads(0)
+    out = {"threads": all_threads}
+    for key, name in (("C1", "tiny"), ("C2", "lmhead32k"), ("C3", "lmhead128k"), ("C4", "embed128k"),
+                      ("C5a", "tied152k"), ("C5b", "wide262k")):
+        cfg = wl.CONFIGS[name]
+        W = host(wl.make_weights(cfg, seed=51, device=dev))
+        V_, D_ = W.shape
+        if key == "C4":
+            idx_d, G_d = wl.make_sparse_batch(cfg, 1, seed=51, device=dev)
+            idx, G = idx_d.cpu().numpy(), host(G_d)
+            n = int(idx.shape[0])
+            nbytes = wl.algorithmic_bytes(V_, D_, W.itemsize, G.itemsize, rows=n)
+        else:
+            G = host(wl.make_dense_grad(cfg, 1, seed=51, device=dev, scales=wl.row_scales(cfg, 51, dev)))
+            idx, n = None, V_
+            nbytes = wl.algorithmic_bytes(V_, D_, W.itemsize, G.itemsize)
+
+        def run(rows=None):
+            Wc = W if rows is None else W[:rows]
+            Gc = G if rows is None or idx is not None else G[:rows]
+            r = np.zeros(Wc.shape[0], np.float32)
+            c = np.zeros(D_, np.float32)
+            return lambda: oracle.step(Wc.copy() if Wc.size < (1 << 22) else Wc, Gc, r, c, 1, idx=idx)
+
+        oracle.set_threads(all_threads)
+        ms_all = timed(run())
+        oracle.set_threads(1)
+        t0 = time.perf_counter()
+        run(min(V_, 4096) if idx is None else None)()
+        probe_ms = (time.perf_counter() - t0) * 1e3
+        est_full = probe_ms * (V_ / min(V_, 4096) if idx is None else 1.0)
+        rows_1t = V_ if est_full <= budget_s * 1e3 or idx is not None else max(4096, int(V_ * budget_s * 1e3 / est_full))
+        ms_1t = timed(run(None if rows_1t == V_ else rows_1t), min_s=0.0)
+        out[key] = {"config": name, "V": V_, "D": D_, "rows_with_gradient": n,
+                    "ms_all_threads": round(ms_all, 3), "GBps_all_threads": round(nbytes / (ms_all * 1e-3) / 1e9, 4),
+                    "ms_one_thread": round(ms_1t, 3), "one_thread_rows": rows_1t,
+                    "ms_one_thread_whole_table": round(ms_1t * V_ / rows_1t, 1)}
+        print(f"cpu oracle {key} {name}: {out[key]}", file=sys.stderr, flush=True)
+        del W, G
+    oracle.set_threads(all_threads)
+    return out
 
 
 def other_configs(ember, wl, torch, dev, K):
@@ -405,6 +478,9 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.cpu_configs:
+        print(json.dumps({"cpu_oracle_configs": cpu_configs(dev)}), flush=True)
+        return
     K, Wm = args.steps, args.warmup
     head_cfg = wl.CONFIGS["lmhead128k"]
     emb_cfg = wl.CONFIGS["embed128k"]
