@@ -23,8 +23,9 @@
 //      segment is longer than L); a wavefront sums one chunk for 256 columns
 //      in float64, position by position, and writes every segment that lies
 //      inside the chunk; the pieces of the segments longer than L go to
-//      float64 partial rows; the chunks where such segments end are listed,
-//      and a last launch adds each one's pieces in chunk order.
+//      float64 partial rows; the chunks where such segments end are listed
+//      with the chunk each began in, and a last launch adds each one's pieces
+//      in chunk order.
 // A segment of at most L positions is therefore summed exactly in ascending
 // position order; a longer one is summed in that order within each piece of L
 // positions and then piece by piece.
@@ -366,7 +367,8 @@ struct SumParams {
     int nslabs;
     double* partA;            // [nchunks][D]: the first segment of a chunk, begun in an earlier chunk
     double* partB;            // [nchunks][D]: the last segment, continued in a later chunk
-    uint32_t* fix_list;       // chunks where a segment that began in an earlier chunk ends
+    uint32_t* fix_list;       // [4 per entry]: chunk where a segment that began in an earlier chunk
+                              // ends, the chunk it began in, its segment number
     uint32_t* fix_count;      // entries of fix_list (cleared by the heads launch)
 };
 
@@ -477,11 +479,14 @@ __device__ __forceinline__ void store_partial(double* row, int64_t col, int64_t 
 // when that segment is not longer than L.  Only segments longer than L are then
 // cut by chunk boundaries (always at multiples of L); a chunk holds between 1
 // and 2L - 1 positions.
-__device__ __forceinline__ int64_t chunk_start(const SumParams& a, int64_t c) {
+// Also returns the segment number at c * L and that segment's start.
+__device__ __forceinline__ int64_t chunk_start(const SumParams& a, int64_t c, uint32_t& u, int64_t& s) {
     const int64_t x = c * a.L;
+    u = 0;
+    s = 0;
     if (x >= a.P) return a.P;
-    const uint32_t u = a.uid[x];
-    const int64_t s = a.seg_start[u];
+    u = a.uid[x];
+    s = a.seg_start[u];
     const int64_t e = a.seg_start[u + 1];
     return e - s > a.L ? x : s;
 }
@@ -502,8 +507,10 @@ __global__ __launch_bounds__(kCoalThreads) void coal_segsum(SumParams a) {
     const int slab = item - c * a.nslabs;
     const int64_t col = (int64_t)slab * kSlabCols + (int64_t)lane * kColsPerLane;
     const bool col_ok = col < a.D;
-    const int64_t k0 = chunk_start(a, c);
-    const int64_t k1 = chunk_start(a, (int64_t)c + 1);
+    uint32_t seg0, seg1;
+    int64_t start0, start1;
+    const int64_t k0 = chunk_start(a, c, seg0, start0);
+    const int64_t k1 = chunk_start(a, (int64_t)c + 1, seg1, start1);
     const UT* U = static_cast<const UT*>(a.U);
     const bool began_before = k0 > 0 && a.K[k0] == a.K[k0 - 1];
     const bool ends_after = k1 < a.P && a.K[k1] == a.K[k1 - 1];
@@ -596,7 +603,13 @@ __global__ __launch_bounds__(kCoalThreads) void coal_segsum(SumParams a) {
             }
         }
     }
-    if (ends_crossing && slab == 0 && lane == 0) a.fix_list[atomicAdd(a.fix_count, 1u)] = (uint32_t)c;
+    // (a chunk that begins inside a segment begins at c L, so seg0 and start0
+    // are that segment's number and start)
+    if (ends_crossing && slab == 0 && lane == 0) {
+        const uint32_t e = atomicAdd(a.fix_count, 1u);
+        *reinterpret_cast<uint4*>(a.fix_list + 4 * (int64_t)e) =
+            make_uint4((uint32_t)c, (uint32_t)(start0 / a.L), seg0, 0u);
+    }
 }
 
 // Segments that cross chunk boundaries: for each listed chunk (where such a
@@ -615,14 +628,14 @@ __global__ __launch_bounds__(kCoalThreads) void coal_fixup(SumParams a) {
     const int64_t items = (int64_t)(*a.fix_count) * nslabs;
     const int64_t wave0 = (int64_t)blockIdx.x * kCoalWaves + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     for (int64_t item = wave0; item < items; item += (int64_t)gridDim.x * kCoalWaves) {
-        const int c = (int)a.fix_list[item / nslabs];
+        const uint4 f = *reinterpret_cast<const uint4*>(a.fix_list + 4 * (item / nslabs));
+        const int c = (int)f.x;
+        const int c0 = (int)f.y;
+        const uint32_t u = f.z;
         const int slab = (int)(item % nslabs);
-        const int64_t k0 = (int64_t)c * a.L;
         const int64_t col = (int64_t)slab * kWave + lane;
         const bool ok = col < a.D;
         const int64_t colc = ok ? col : 0;
-        const uint32_t u = a.uid[k0];
-        const int c0 = (int)(a.seg_start[u] / a.L);
         double acc = a.partB[(int64_t)c0 * a.D + colc];
         for (int cc = c0 + 1; cc <= c; cc += kFixBatch) {
             double x[kFixBatch];
@@ -689,7 +702,7 @@ CoalPlan coal_plan(int64_t P, int64_t V, int64_t D) {
     const size_t nc = (size_t)(c.nchunks > 0 ? c.nchunks : 1);
     c.part_a = off; off = align256(off + nc * (size_t)D * 8);
     c.part_b = off; off = align256(off + nc * (size_t)D * 8);
-    c.fix_list = off; off = align256(off + nc * 4);
+    c.fix_list = off; off = align256(off + nc * 16);
     c.fix_count = off; off = align256(off + 4);
     c.total = off;
     return c;
