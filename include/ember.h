@@ -418,6 +418,18 @@ typedef struct {
 int ember_profile_enable(int enable);
 
 /*
+ * Bound of each grid-barrier wait of the one-launch sparse step
+ * (diagnostics, for testing its failure path): `ticks` of the GPU's 100 MHz
+ * real-time counter, for the steps enqueued after the call, process-wide;
+ * 0 restores the default (1e8 ticks, about one second).  A wait that runs
+ * out ends the launch normally and sets the timeout bit that
+ * ember_get_error reports as EMBER_ERR_DEVICE (the state is then unspecified
+ * until ember_init_state).  Returns EMBER_ERR_ARG for ticks < 0, else
+ * EMBER_OK.
+ */
+int ember_set_barrier_wait_ticks(int64_t ticks);
+
+/*
  * Streaming probe (diagnostics): reference rates of plain streaming kernels
  * over the same bytes as the passes above (not ceilings: the passes keep more
  * rows in flight per wavefront, and the apply pass finds part of G in the

@@ -4,6 +4,7 @@
 
 #include "ember.h"
 
+#include <atomic>
 #include <cmath>
 #include <mutex>
 #include <string>
@@ -112,6 +113,10 @@ int run_step(StepArgs& a, float lr, float beta2, float eps, int64_t t, int maxim
     return e == hipSuccess ? EMBER_OK : EMBER_ERR_HIP;
 }
 
+// Bound of a grid-barrier wait of the one-launch sparse step (real-time counter
+// ticks); 0: the default.  Set by ember_set_barrier_wait_ticks.
+std::atomic<int64_t> g_barrier_wait_ticks{0};
+
 void set_scalars(StepArgs& a, float lr, float beta2, float eps, int64_t t, int maximize) {
     const double b2 = (double)beta2;
     a.beta2 = beta2;
@@ -120,7 +125,8 @@ void set_scalars(StepArgs& a, float lr, float beta2, float eps, int64_t t, int m
     const double alpha_s = maximize ? (double)lr : -(double)lr;
     a.inv_alpha = lr > 0.0f ? 1.0 / alpha_s : 0.0;
     a.eps_over_alpha = lr > 0.0f ? (float)((double)eps / alpha_s) : 0.0f;
-    a.spin_ticks = ember::kOnchipSpinTicks;
+    const int64_t w = g_barrier_wait_ticks.load(std::memory_order_relaxed);
+    a.spin_ticks = w > 0 ? w : ember::kOnchipSpinTicks;
 }
 
 // LM-head step: the weight-gradient GEMM writes G and the statistics
@@ -736,6 +742,12 @@ int ember_stream_probe(int mode, void* dst, const void* a, const void* b, size_t
     const hipError_t e = timed("ember_stream_probe", stream,
                                [&] { return ember::launch_stream_probe(mode, dst, a, b, bytes, stream); });
     return e == hipSuccess ? EMBER_OK : EMBER_ERR_HIP;
+}
+
+int ember_set_barrier_wait_ticks(int64_t ticks) {
+    if (ticks < 0) return EMBER_ERR_ARG;
+    g_barrier_wait_ticks.store(ticks, std::memory_order_relaxed);
+    return EMBER_OK;
 }
 
 int ember_profile_enable(int enable) {

@@ -35,6 +35,7 @@ EXPORTED = ("ember_workspace_bytes", "ember_init_state", "ember_step_dense",
             "ember_rowonly_step_sparse_rows_devn", "ember_coalesce_workspace_bytes", "ember_coalesce_rows",
             "ember_lmhead_step", "ember_step_multi", "ember_get_error", "ember_strerror",
             "ember_profile_enable", "ember_profile_collect", "ember_stream_probe",
+            "ember_set_barrier_wait_ticks",
             "ember_step_sparse_rows_static")
 
 
@@ -92,6 +93,7 @@ def _load(path: str = _LIB_PATH) -> ctypes.CDLL:
     lib.ember_strerror.argtypes = [i32]
     lib.ember_strerror.restype = ctypes.c_char_p
     lib.ember_profile_enable.argtypes = [i32]
+    lib.ember_set_barrier_wait_ticks.argtypes = [ctypes.c_int64]
     lib.ember_profile_collect.argtypes = [ctypes.POINTER(_KernelStat), i32, ctypes.POINTER(i32)]
     lib.ember_stream_probe.argtypes = [i32, vp, vp, vp, sz, vp]
     lib.ember_step_sparse_rows_static.argtypes = [vp, i32, i64, vp, i32, i64, vp, i64, vp, vp, i64, i64, i64,
@@ -378,6 +380,12 @@ def ember_get_error(ws: torch.Tensor) -> int:
     st = ctypes.c_int(0)
     _check(LIB.ember_get_error(_ptr(ws), _stream(ws), ctypes.byref(st)), "ember_get_error")
     return st.value
+
+
+def ember_set_barrier_wait_ticks(ticks: int) -> None:
+    """Bound of the one-launch sparse step's grid-barrier waits in 100 MHz
+    ticks (diagnostics; 0 restores the default of about one second)."""
+    _check(LIB.ember_set_barrier_wait_ticks(int(ticks)), "ember_set_barrier_wait_ticks")
 
 
 def ember_profile_enable(enable: bool) -> None:

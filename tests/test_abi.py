@@ -395,3 +395,9 @@ def test_table_step_struct_matches_the_header(em):
         assert getattr(em.TableStep, pname).offset == off, name
         off += sz
     assert ctypes.sizeof(em.TableStep) == (off + 7) // 8 * 8
+
+
+def test_barrier_wait_bound_checks_its_argument(em):
+    assert em.LIB.ember_set_barrier_wait_ticks(-1) == em.EMBER_ERR_ARG
+    assert em.LIB.ember_set_barrier_wait_ticks(1000) == em.EMBER_OK
+    assert em.LIB.ember_set_barrier_wait_ticks(0) == em.EMBER_OK   # the default again
