@@ -204,11 +204,12 @@ int ember_step_sparse_rows_static(void* W, int w_dtype, int64_t ldw,
  * Several Ember steps in one call: the tables of a model (for example the
  * LM head, dense, and the input embedding, sparse rows) each take the step
  * Algorithm 1 defines for them (or the row-only step of Section 2.1), exactly
- * as the single-table entry points would, but the library enqueues three
- * launches in all for the canonical tables (one statistics pass, one finalize
- * pass, one apply pass over every table) instead of three per table, so the
- * tables share the chip and a small table costs its bytes instead of its
- * launch latency.  Each table's results are the same bits as its own
+ * as the single-table entry points would, but the canonical tables share
+ * three launches (one statistics pass, one finalize pass, one apply pass over
+ * every table) instead of three per table, so the tables share the chip and a
+ * small table costs its bytes instead of its launch latency; a sparse table
+ * whose rows fit on chip takes its one-launch step (that of
+ * ember_step_sparse_rows) ahead of them.  Each table's results are the same bits as its own
  * single-table call (ember_step_dense, ember_step_sparse_rows(_devn), or the
  * row-only entry points declared below).
  *

@@ -1,6 +1,8 @@
 // HIP kernels of the Ember step for gfx950 (MI355X).
 //
-// One step (Token Geometry, Algorithm 1) is three launches on one stream:
+// One dense step (Token Geometry, Algorithm 1) is three launches on one
+// stream (a sparse step whose rows fit on chip is one launch, ember_sparse_onchip,
+// further down; larger sparse batches take the same three):
 //   ember_stats          reads G once: per-row sums of g^2 and per-block
 //                        column sums of g^2 (per-lane registers, then a
 //                        fixed-order LDS combine of the block's 4 waves).  The

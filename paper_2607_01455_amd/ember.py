@@ -354,7 +354,8 @@ def table_step(W: torch.Tensor, G: torch.Tensor | None, r: torch.Tensor, c: torc
 
 def ember_step_multi(steps, stream_of: torch.Tensor) -> None:
     """Enqueue the steps of several tables (TableStep entries) on the current
-    stream of stream_of's device: three launches in all."""
+    stream of stream_of's device, in shared launches (a sparse table whose
+    rows fit on chip takes its one-launch step)."""
     arr = (TableStep * len(steps))(*steps)
     _check(LIB.ember_step_multi(arr, len(steps), _stream(stream_of)), "ember_step_multi")
 
