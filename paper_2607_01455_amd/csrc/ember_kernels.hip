@@ -1477,23 +1477,14 @@ __global__ __launch_bounds__(kOnchipThreads, 1) void ember_sparse_onchip(OnchipP
     __shared__ double dsum[kOnchipWaves];
     __shared__ int sh_ok, sh_err;
     __shared__ float sh_scale;
-    __shared__ unsigned sh_epoch;
 
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int b = blockIdx.x;
     const int64_t V = a.V, D = a.D;
-    if (threadIdx.x == 0) sh_epoch = *a.epoch;
-    __syncthreads();
-    // The error bits alternate between two words by launch, so block 0 can
-    // clear the next launch's word while this launch still reads its own.
-    const unsigned epoch = sh_epoch;
-    int* flag = (epoch & 1u) ? a.flag_odd : a.flag;
-
     // ---- phase 1: load the rows, row and column sums of g^2, row marks ----
     bool bad_count = false;
     const int64_t n = active_rows(a.n_dev, a.rows, bad_count);
-    if (bad_count && b == 0 && threadIdx.x == 0) atomicOr(flag, kFlagCount);
     int64_t r0, r1;
     row_range(n, NB, b, r0, r1);
     const int nloc = (int)(r1 - r0);
@@ -1541,6 +1532,12 @@ __global__ __launch_bounds__(kOnchipThreads, 1) void ember_sparse_onchip(OnchipP
 #pragma unroll
         for (int m = 0; m < M; ++m) buf_load<GT, EPC>(gb, goff[m], graw[u][m]);
     }
+    // Every wave reads the epoch itself, once its gradient loads are in flight
+    // (no wait and no block barrier in front of them).  The error bits
+    // alternate between two words by launch, so block 0 can clear the next
+    // launch's word while this launch still reads its own.
+    const unsigned epoch = __builtin_amdgcn_readfirstlane(*a.epoch);
+    int* flag = (epoch & 1u) ? a.flag_odd : a.flag;
     // Row marks (lane u of each slab-0 wave, unit u's row): a count per id,
     // read in phase 2 (0: untouched, 1: touched, more: a repeated id), so no
     // result has to come back here; and r of the row, loaded before the weight
@@ -1565,6 +1562,7 @@ __global__ __launch_bounds__(kOnchipThreads, 1) void ember_sparse_onchip(OnchipP
     }
     // every load is issued before the first wait, and no decode moves above them
     __builtin_amdgcn_sched_barrier(0);
+    if (bad_count && b == 0 && threadIdx.x == 0) atomicOr(flag, kFlagCount);
 
     float acc[M][EPC];
 #pragma unroll
