@@ -132,34 +132,48 @@ __global__ __launch_bounds__(1024) void coal_scan(const uint32_t* in, uint32_t* 
     }
 }
 
-// Exclusive scan of one value per thread over the block (256 threads).
+// Exclusive scan of one value per thread over the block (256 threads): an
+// inclusive scan inside each wavefront with lane shuffles, then the totals of
+// the lower wavefronts from LDS (two block barriers in all).  lds holds at
+// least kCoalWaves words.
 __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* lds, uint32_t* total) {
-    const int t = threadIdx.x;
-    lds[t] = v;
-    __syncthreads();
-    for (int off = 1; off < kCoalThreads; off <<= 1) {
-        const uint32_t x = t >= off ? lds[t - off] : 0u;
-        __syncthreads();
-        lds[t] += x;
-        __syncthreads();
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    uint32_t x = v;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const uint32_t y = __shfl_up(x, off, kWave);
+        if (lane >= off) x += y;
     }
-    const uint32_t incl = lds[t];
-    *total = lds[kCoalThreads - 1];
+    if (lane == kWave - 1) lds[wave] = x;
     __syncthreads();
-    return incl - v;
+    uint32_t before = 0, all = 0;
+#pragma unroll
+    for (int w = 0; w < kCoalWaves; ++w) {
+        const uint32_t c = lds[w];
+        before += w < wave ? c : 0u;
+        all += c;
+    }
+    *total = all;
+    __syncthreads();
+    return before + x - v;
 }
 
 // Stable scatter of one tile by the current digit.  Tile keys are taken in
-// position order (item j of thread t is key base + j * 256 + t); within each
-// group of 256 keys a key's rank among equal digits is the number of equal
-// digits in lower lanes of its wavefront (from one ballot per digit bit) plus
-// the counts of that digit in lower wavefronts and in earlier groups.
+// position order (item j of thread t is key base + j * 256 + t), in groups of
+// 64 keys (group j * kCoalWaves + w: item j of wavefront w).  A key's rank
+// among equal digits is the number of equal digits in lower lanes of its group
+// (from one ballot per digit bit) plus the count of that digit in earlier
+// groups: every group's digit counts are written first, then one prefix pass
+// per digit over the groups, so the whole ranking takes two block barriers.
+constexpr int kGroups = kCoalItems * kCoalWaves;   // groups of 64 keys in a tile
+
 __global__ __launch_bounds__(kCoalThreads) void coal_scatter(SortPass a) {
     __shared__ uint32_t off[kMaxBins];
-    __shared__ uint32_t run[kMaxBins];
-    __shared__ uint32_t wcnt[kCoalWaves][kMaxBins];
-    __shared__ uint32_t wexcl[kCoalWaves][kMaxBins];
-    __shared__ uint32_t scan_lds[kCoalThreads];
+    // [group][digit]: the group's count of the digit, then the count in the
+    // earlier groups of the tile (< kTile, so 16 bits)
+    __shared__ uint16_t cnt[kGroups * kMaxBins];
+    __shared__ uint32_t scan_lds[kCoalWaves];
     const int bins = 1 << a.bits;
     const int tile = blockIdx.x;
     const int t = threadIdx.x;
@@ -212,14 +226,15 @@ __global__ __launch_bounds__(kCoalThreads) void coal_scatter(SortPass a) {
             excl += tot[q];
         }
     }
-    for (int b = t; b < bins; b += kCoalThreads) {
-        run[b] = 0;
-#pragma unroll
-        for (int w = 0; w < kCoalWaves; ++w) wcnt[w][b] = 0;
+    {
+        // clear the counts, two 16-bit entries per word
+        uint32_t* c32 = reinterpret_cast<uint32_t*>(cnt);
+        for (int x = t; x < kGroups * bins / 2; x += kCoalThreads) c32[x] = 0u;
     }
     __syncthreads();
 
     const uint64_t below = lane == 0 ? 0ull : (~0ull >> (kWave - lane));
+    uint32_t rank[kCoalItems], dig[kCoalItems];
 #pragma unroll
     for (int j = 0; j < kCoalItems; ++j) {
         const int64_t i = base + (int64_t)j * kCoalThreads + t;
@@ -231,22 +246,27 @@ __global__ __launch_bounds__(kCoalThreads) void coal_scatter(SortPass a) {
             const uint64_t m = __ballot(bit);
             peers &= bit ? m : ~m;
         }
-        const uint32_t rank = (uint32_t)__popcll(peers & below);
-        if (valid && rank == 0) wcnt[wave][d] = (uint32_t)__popcll(peers);
-        __syncthreads();
-        for (int b = t; b < bins; b += kCoalThreads) {
-            uint32_t r = run[b];
+        rank[j] = (uint32_t)__popcll(peers & below);
+        dig[j] = d;
+        if (valid && rank[j] == 0) cnt[(j * kCoalWaves + wave) * bins + d] = (uint16_t)__popcll(peers);
+    }
+    __syncthreads();
+    // per digit: counts of the earlier groups, in position order
+    for (int b = t; b < bins; b += kCoalThreads) {
+        uint32_t r = 0;
 #pragma unroll
-            for (int w = 0; w < kCoalWaves; ++w) {
-                wexcl[w][b] = r;
-                r += wcnt[w][b];
-                wcnt[w][b] = 0;
-            }
-            run[b] = r;
+        for (int g = 0; g < kGroups; ++g) {
+            const uint32_t c = cnt[g * bins + b];
+            cnt[g * bins + b] = (uint16_t)r;
+            r += c;
         }
-        __syncthreads();
-        if (valid) {
-            const uint32_t dst = off[d] + wexcl[wave][d] + rank;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kCoalItems; ++j) {
+        const int64_t i = base + (int64_t)j * kCoalThreads + t;
+        if (i < a.P) {
+            const uint32_t dst = off[dig[j]] + cnt[(j * kCoalWaves + wave) * bins + dig[j]] + rank[j];
             a.keys_out[dst] = key[j];
             a.vals_out[dst] = val[j];
         }
