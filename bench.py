@@ -554,6 +554,14 @@ def main():
     if ember.ember_get_error(emb.ws) != ember.EMBER_OK:
         raise RuntimeError("sparse step reported an index error")
 
+    # --- timed region A2: each table's step alone, K steps back to back -------
+    # (no marker between steps; the sparse table's hot rows may still sit in
+    # the last-level cache from the step before, which region A1 rules out)
+    dense_alone_ms = whole_steps(lambda k: head.step(W_head, grads[k % n_grads]))
+    sparse_alone_ms = whole_steps(lambda k: emb.step_sparse_rows(W_emb, batches[k][1], batches[k][0]))
+    if ember.ember_get_error(emb.ws) != ember.EMBER_OK:
+        raise RuntimeError("sparse step reported an index error")
+
     dense_bytes = wl.algorithmic_bytes(V, D, 2, 2)
     n_rows = [int(b[0].numel()) for b in batches[Wm:Wm + K]]
     sparse_bytes = [wl.algorithmic_bytes(V, D, 2, 2, rows=n) for n in n_rows]
@@ -709,12 +717,16 @@ def main():
         "parts": {
             "dense_lmhead": {"workload": "LM head 128256 x 4096 bf16, dense step (three launches)",
                              "ms": round(dense_ms, 4), "bytes": dense_bytes,
+                             "ms_back_to_back": round(dense_alone_ms, 4),
                              "GBps": round(dense_bytes / (dense_ms * 1e-3) / 1e9, 1),
                              "pct_of_peak": round(100.0 * dense_bytes / (dense_ms * 1e-3) / 1e9 / PEAK_GBPS, 2),
                              "roofline": dense_roofline},
             "sparse_embedding": {"workload": "input embedding 128256 x 4096 bf16, sparse-row step of an "
                                              "8 x 2048-token Zipf(1.1) batch (one launch)",
                                  "ms": round(sparse_ms, 4), "bytes": int(sparse_step_bytes),
+                                 "ms_back_to_back": round(sparse_alone_ms, 4),
+                                 "pct_of_peak_back_to_back": round(100.0 * sparse_step_bytes / (sparse_alone_ms * 1e-3)
+                                                                   / 1e9 / PEAK_GBPS, 2),
                                  "GBps": round(sparse_step_bytes / (sparse_ms * 1e-3) / 1e9, 1),
                                  "pct_of_peak": round(100.0 * sparse_step_bytes / (sparse_ms * 1e-3) / 1e9
                                                       / PEAK_GBPS, 2),
