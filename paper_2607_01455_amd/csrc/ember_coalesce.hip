@@ -47,7 +47,10 @@ constexpr int kMaxBins = 1 << kMaxDigitBits;         // digits of up to 10 bits
 constexpr int kInBlockOffsetTiles = 64;              // up to this many tiles the
                                                      // scatter derives its own offsets
 constexpr int kRunRows = 16;                         // rows a wavefront holds at once
-constexpr int kMinChunkBatches = 2;                  // a chunk is at least this many batches
+constexpr int kMinChunkBatches = 3;                  // a chunk is at least this many batches
+                                                     // (fewer, longer chunks: at 16384 tokens and
+                                                     // D = 4096 every wavefront of the sums is then
+                                                     // resident at once, six per SIMD)
 constexpr int kMaxChunks = 4096;                     // bound on the chunks ...
 constexpr int64_t kMaxPartialElems = (int64_t)1 << 25; // ... and on chunks x D
 constexpr int kColsPerLane = 4;                      // columns per lane (4 or 8)
@@ -409,20 +412,36 @@ template <typename T> struct Cols {
     }
 };
 
-// float64 -> bf16, one round-to-nearest-even: round to fp32 with round-to-odd
-// (the truncation, with its last bit set when inexact), then to bf16 with
-// round-to-nearest-even; fp32 keeps 16 more bits than bf16, so the result is
-// the correctly rounded one (Boldo and Melquiond, "When double rounding is
-// odd", 2005).
+// float64 -> bf16, one round-to-nearest-even.  Rounding to fp32 (nearest-even)
+// and then to bf16 (nearest-even) gives the correctly rounded result except
+// where the fp32 value is a bf16 midpoint that x itself is not: fp32's grid
+// refines bf16's and holds every bf16 midpoint, so the first rounding never
+// crosses a midpoint, it can only land on one.  In that case (low 16 bits of
+// the fp32 value 0x8000, fp32 inexact) the side of the midpoint x lies on
+// decides; only then are float64 comparisons needed.
 __device__ __forceinline__ uint16_t f64_to_bf16(double x) {
     const float f = (float)x;
     const uint32_t b0 = __float_as_uint(f);
-    const bool inexact = (double)f != x;                        // also true for NaN
-    const uint32_t toward_zero = b0 - (fabs((double)f) > fabs(x) ? 1u : 0u);
-    const uint32_t b = inexact ? (toward_zero | 1u) : b0;     // round-to-odd fp32
-    const uint32_t rne = (b + 0x7FFFu + ((b >> 16) & 1u)) >> 16;
-    const bool nan = x != x;
-    return (uint16_t)(nan ? ((b0 >> 16) | 0x0040u) : rne);
+    uint32_t r = (b0 + 0x7FFFu + ((b0 >> 16) & 1u)) >> 16;
+    if ((b0 & 0xFFFFu) == 0x8000u) {
+        const double fd = (double)f;
+        if (fd != x) r = (b0 >> 16) + (fabs(x) > fabs(fd) ? 1u : 0u);
+    }
+    if (f != f) r = (b0 >> 16) | 0x0040u;   // NaN stays NaN (quiet)
+    return (uint16_t)r;
+}
+
+// fp32 bits of one input value as a float64 sum of that value alone gives them
+// back: 0 + (-0) = +0, and a NaN comes back quiet.
+__device__ __forceinline__ uint32_t one_row_f32(uint32_t w) {
+    if ((w & 0x7FFFFFFFu) > 0x7F800000u) return w | 0x00400000u;
+    return w == 0x80000000u ? 0u : w;
+}
+
+// fp32 bits -> bf16, nearest-even (a NaN stays a quiet NaN)
+__device__ __forceinline__ uint32_t f32_bits_to_bf16(uint32_t w) {
+    if ((w & 0x7FFFFFFFu) > 0x7F800000u) return (w >> 16) | 0x0040u;
+    return (w + 0x7FFFu + ((w >> 16) & 1u)) >> 16;
 }
 
 template <typename GT>
@@ -463,30 +482,59 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(void* row, int64_t by
     return __builtin_amdgcn_make_buffer_rsrc(row, 0, (int)bytes, kBufferWord3);
 }
 
+// One lane's columns of row u of G, already in G's format (kWords words).
 template <typename GT>
-__device__ __forceinline__ void buf_store_cols(void* G, int64_t ldg, uint32_t u, int col, int64_t D,
-                                               const double (&x)[kColsPerLane]) {
+__device__ __forceinline__ void buf_store_words(void* G, int64_t ldg, uint32_t u, int col, int64_t D,
+                                                const uint32_t (&w)[Cols<GT>::kWords]) {
     GT* row = static_cast<GT*>(G) + (int64_t)u * ldg;
     const __amdgpu_buffer_rsrc_t rs = row_rsrc(row, D * (int64_t)sizeof(GT));
     using v4 = decltype(__builtin_amdgcn_raw_buffer_load_b128(rs, 0, 0, 0));
     using v2 = decltype(__builtin_amdgcn_raw_buffer_load_b64(rs, 0, 0, 0));
-    if constexpr (sizeof(GT) == 4) {
+    constexpr int kW = Cols<GT>::kWords;
+    const int byte0 = col * (int)sizeof(GT);
+    if constexpr (kW % 4 == 0) {
 #pragma unroll
-        for (int g = 0; g < kColsPerLane; g += 4) {
-            const uint32_t w0 = __float_as_uint((float)x[g]), w1 = __float_as_uint((float)x[g + 1]);
-            const uint32_t w2 = __float_as_uint((float)x[g + 2]), w3 = __float_as_uint((float)x[g + 3]);
-            __builtin_amdgcn_raw_buffer_store_b128(v4{w0, w1, w2, w3}, rs, (col + g) * 4, 0, 0);
-        }
+        for (int g = 0; g < kW; g += 4)
+            __builtin_amdgcn_raw_buffer_store_b128(v4{w[g], w[g + 1], w[g + 2], w[g + 3]}, rs, byte0 + 4 * g, 0, 0);
     } else {
-        uint32_t w[kColsPerLane / 2];
-#pragma unroll
-        for (int e = 0; e < kColsPerLane / 2; ++e)
-            w[e] = (uint32_t)f64_to_bf16(x[2 * e]) | ((uint32_t)f64_to_bf16(x[2 * e + 1]) << 16);
-        if constexpr (kColsPerLane == 8)
-            __builtin_amdgcn_raw_buffer_store_b128(v4{w[0], w[1], w[2], w[3]}, rs, col * 2, 0, 0);
-        else
-            __builtin_amdgcn_raw_buffer_store_b64(v2{w[0], w[1]}, rs, col * 2, 0, 0);
+        static_assert(kW == 2, "4 bf16 columns per lane");
+        __builtin_amdgcn_raw_buffer_store_b64(v2{w[0], w[1]}, rs, byte0, 0, 0);
     }
+}
+
+// A finished float64 sum, rounded once to G's type.
+template <typename GT>
+__device__ __forceinline__ void buf_store_cols(void* G, int64_t ldg, uint32_t u, int col, int64_t D,
+                                               const double (&x)[kColsPerLane]) {
+    uint32_t w[Cols<GT>::kWords];
+#pragma unroll
+    for (int e = 0; e < Cols<GT>::kWords; ++e) {
+        if constexpr (sizeof(GT) == 4) w[e] = __float_as_uint((float)x[e]);
+        else w[e] = (uint32_t)f64_to_bf16(x[2 * e]) | ((uint32_t)f64_to_bf16(x[2 * e + 1]) << 16);
+    }
+    buf_store_words<GT>(G, ldg, u, col, D, w);
+}
+
+// A segment of one row: its sum is that row's value, which G's type holds
+// exactly when the types agree (else one rounding, fp32 -> bf16), so the
+// value is converted without float64 arithmetic; -0 and NaN come out as the
+// float64 sum gives them.
+template <typename UT, typename GT>
+__device__ __forceinline__ void buf_store_one_row(void* G, int64_t ldg, uint32_t u, int col, int64_t D,
+                                                  const typename Cols<UT>::raw& r) {
+    uint32_t f[kColsPerLane];   // fp32 bits per column
+#pragma unroll
+    for (int e = 0; e < kColsPerLane; ++e) {
+        if constexpr (sizeof(UT) == 4) f[e] = one_row_f32(r[e]);
+        else f[e] = one_row_f32((e & 1) ? (r[e / 2] & 0xFFFF0000u) : (r[e / 2] << 16));
+    }
+    uint32_t w[Cols<GT>::kWords];
+#pragma unroll
+    for (int e = 0; e < Cols<GT>::kWords; ++e) {
+        if constexpr (sizeof(GT) == 4) w[e] = f[e];
+        else w[e] = f32_bits_to_bf16(f[2 * e]) | (f32_bits_to_bf16(f[2 * e + 1]) << 16);
+    }
+    buf_store_words<GT>(G, ldg, u, col, D, w);
 }
 
 __device__ __forceinline__ void store_partial(double* row, int64_t col, int64_t D, const double (&x)[kColsPerLane]) {
@@ -511,7 +559,11 @@ __device__ __forceinline__ int64_t chunk_start(const SumParams& a, int64_t c, ui
     return e - s > a.L ? x : s;
 }
 
-// One wavefront per (chunk, 256-column slab); slabs of a chunk are adjacent.
+// One wavefront per (chunk, 256-column slab); slabs of a chunk are adjacent,
+// and chunks go to wavefronts in reverse order: the last chunks hold the rare
+// ids (a segment per row or two, so the most stores and roundings per row)
+// and start first, while the long segments of the frequent ids, which only
+// stream rows, fill the slots that free up.
 // kExact (D a multiple of 4): the wavefront loads kRunRows rows at a time into
 // registers (lanes past D read column 0 and store nothing), then walks them in
 // order; a row that starts a segment resets the sum, a row that ends one
@@ -522,9 +574,10 @@ __global__ __launch_bounds__(kCoalThreads) void coal_segsum(SumParams a) {
     using raw = typename Cols<UT>::raw;
     const int lane = threadIdx.x & (kWave - 1);
     const int item = blockIdx.x * kCoalWaves + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-    const int c = item / a.nslabs;
-    if (c >= a.nchunks) return;
-    const int slab = item - c * a.nslabs;
+    const int ci = item / a.nslabs;
+    if (ci >= a.nchunks) return;
+    const int slab = item - ci * a.nslabs;
+    const int c = a.nchunks - 1 - ci;
     const int64_t col = (int64_t)slab * kSlabCols + (int64_t)lane * kColsPerLane;
     const bool col_ok = col < a.D;
     uint32_t seg0, seg1;
@@ -589,6 +642,8 @@ __global__ __launch_bounds__(kCoalThreads) void coal_segsum(SumParams a) {
                         if (first || (chunk_end && ends_after)) {
                             store_partial((first ? a.partA : a.partB) + (int64_t)c * a.D, col, a.D, acc);
                             ends_crossing |= first && !(chunk_end && ends_after);
+                        } else if (run0 == k) {
+                            buf_store_one_row<UT, GT>(a.G, a.ldg, u, (int)col, a.D, rows[r]);
                         } else {
                             buf_store_cols<GT>(a.G, a.ldg, u, (int)col, a.D, acc);
                         }
