@@ -20,7 +20,7 @@ import torch
 
 import oracle
 from paper_2607_01455_amd import workloads as wl
-from parity_checks import DEV, as_f64 as _as_f64, check_coalesced_rows as check_rows, host_bits
+from parity_checks import DEV, as_f64 as _as_f64, bf16_values, check_coalesced_rows as check_rows, host_bits
 
 pytestmark = pytest.mark.gpu
 
@@ -79,6 +79,56 @@ def test_coalesce_padded_rows_and_rounding_ties(em):
     assert n_diff == 0
     got = host_bits(G)
     assert got[0, 0] == 0x3F80 and got[1, 0] == 0x3F81 and got[0, 1] == 0xBF80
+
+
+def _bits_tensor(bits: np.ndarray, dtype) -> torch.Tensor:
+    """uint16 bf16 bits or uint32 fp32 bits -> a device tensor of that dtype."""
+    if dtype == torch.bfloat16:
+        return torch.from_numpy(bits.astype(np.uint16).view(np.int16)).to(DEV).view(torch.bfloat16)
+    return torch.from_numpy(bits.astype(np.uint32).view(np.float32)).to(DEV)
+
+
+@pytest.mark.parametrize("ud", [torch.bfloat16, torch.float32])
+def test_coalesce_rounding_edges_and_one_row_segments(em, ud):
+    # the hand-derived segments of the oracle's pins (midpoints, overflow,
+    # -0, inf, subnormals), the rows of all ids interleaved; column j carries
+    # the row with its sign flipped for odd j; plus rows only an fp32 input
+    # has (one-row segments rounded once from fp32 to bf16) and a NaN
+    from test_oracle_coalesce_pins import BF16_EDGE_SEGMENTS
+    segs = [[b << 16 for b in rows] for rows, _ in BF16_EDGE_SEGMENTS]
+    if ud == torch.float32:
+        segs += [[0x3F808008], [0x3F808000], [0x3F818000], [0x00000001], [0x00008000], [0x00008001],
+                 [0x80000000], [0x3F808000, 0x00000000]]
+    segs += [[0x7FC10000]]
+    tok_h = np.concatenate([np.full(len(r), k, np.int64) for k, r in enumerate(segs)])
+    rows32 = np.concatenate([np.array(r, np.uint64) for r in segs]).astype(np.uint32)
+    perm = np.random.default_rng(9).permutation(tok_h.size)   # positions interleaved
+    tok_h, rows32 = tok_h[perm], rows32[perm]
+    D, V = 8, len(segs)
+    cols = np.stack([rows32 ^ (0x80000000 if j % 2 else 0) for j in range(D)], axis=1).astype(np.uint32)
+    bits = (cols >> 16).astype(np.uint16) if ud == torch.bfloat16 else cols
+    U = _bits_tensor(bits, ud)
+    for gd in (torch.bfloat16, torch.float32):
+        co = em.Coalescer(tok_h.size, V, D, dtype=gd, device=DEV)
+        idx, G = co(torch.from_numpy(tok_h).to(DEV), U)
+        st, idx_o, G_o = oracle.coalesce(tok_h, host_bits(U), V,
+                                         out_dtype=np.uint16 if gd == torch.bfloat16 else np.float32)
+        assert st == oracle.OK and np.array_equal(idx.cpu().numpy(), idx_o)
+        got, want = host_bits(G), G_o
+        if gd == torch.bfloat16:
+            got_v, want_v = bf16_values(got), bf16_values(want)
+        else:
+            got_v, want_v = got.astype(np.float64), want.astype(np.float64)
+        nan = np.isnan(want_v)
+        assert np.array_equal(np.isnan(got_v), nan), f"{ud}->{gd}: NaN positions differ"
+        gb = got.view(np.uint32) if got.dtype == np.float32 else got
+        wb = want.view(np.uint32) if want.dtype == np.float32 else want
+        bad = np.argwhere((gb != wb) & ~nan)
+        assert bad.size == 0, f"{ud}->{gd}: {len(bad)} elements differ, first {bad[:4].tolist()}: " \
+                              f"{[hex(int(gb[tuple(i)])) for i in bad[:4]]} vs {[hex(int(wb[tuple(i)])) for i in bad[:4]]}"
+        if gd == torch.bfloat16:
+            for k, (_, want_bits) in enumerate(BF16_EDGE_SEGMENTS):
+                assert int(got[k, 0]) == want_bits and int(got[k, 1]) == want_bits ^ 0x8000 or want_bits == 0
 
 
 def test_coalesce_index_errors_empty_batch_and_reuse(em):

@@ -115,6 +115,33 @@ def test_bf16_output_is_rounded_once_from_float64():
     assert np.float32(np.float64(1.0) + 2.0 ** -8 + 2.0 ** -30) == np.float32(1.0 + 2.0 ** -8)
 
 
+# (rows of one id, as bf16 bits; the bf16 bits of their once-rounded sum),
+# every expected value derived by hand from the bf16 grid
+BF16_EDGE_SEGMENTS = [
+    ([0x3F80, 0x3B80, 0x3080], 0x3F81),   # 1 + 2^-8 + 2^-30: just above the 1 / 1+2^-7 midpoint -> up
+    ([0x3F80, 0x3B80, 0xB080], 0x3F80),   # 1 + 2^-8 - 2^-30: just below it -> down
+    ([0x3F80, 0x3B80], 0x3F80),           # the midpoint itself -> the even neighbour 1
+    ([0x3F81, 0x3B80], 0x3F82),           # 1 + 2^-7 + 2^-8: midpoint, even neighbour above
+    ([0xBF80, 0xBB80, 0xB080], 0xBF81),   # the first three mirrored
+    ([0xBF80, 0xBB80, 0x3080], 0xBF80),
+    ([0x7F7F, 0x7F7F], 0x7F80),           # 2 x the largest finite value -> +inf
+    ([0x7F7F, 0x7B00], 0x7F80),           # largest + half its spacing: a tie, even side is 2^128 -> +inf
+    ([0x8000], 0x0000),                   # a row of -0 alone: 0 + (-0) = +0
+    ([0x7F80], 0x7F80),                   # +inf alone
+    ([0x0001], 0x0001),                   # the smallest subnormal alone
+    ([0xFF7F], 0xFF7F),                   # the most negative finite value alone
+    ([0x0001, 0x0001], 0x0002),           # subnormals add exactly
+]
+
+
+@pytest.mark.parametrize("rows,want", BF16_EDGE_SEGMENTS)
+def test_bf16_edge_segments_round_once(rows, want):
+    tok = np.zeros(len(rows), np.int64)
+    U = np.array(rows, np.uint16).reshape(-1, 1)
+    st, _, G = oracle.coalesce(tok, U, 1, out_dtype=np.uint16)
+    assert st == oracle.OK and int(G[0, 0]) == want
+
+
 def test_index_errors_and_empty_batch():
     U = np.ones((3, 2), np.float32)
     for bad in ([0, 5, 1], [0, -1, 1]):
