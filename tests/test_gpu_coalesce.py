@@ -151,6 +151,23 @@ def test_coalesce_index_errors_empty_batch_and_reuse(em):
     check_rows(host_bits(G), G_o, tok_h, _as_f64(host_bits(U)), "after error")
 
 
+@pytest.mark.parametrize("P", [65536, 65537, 70000])
+def test_coalesce_index_error_and_recovery_many_tiles(em, P):
+    # 64 sort tiles (offsets derived in the blocks) and more (separate scans):
+    # an id outside [0, V) in the last tile is reported, n = -1, and the same
+    # workspace then coalesces a valid batch
+    D, V = 8, 5000
+    rng = np.random.default_rng(P)
+    co = em.Coalescer(P, V, D, dtype=torch.bfloat16, device=DEV)
+    U = torch.randn(P, D, device=DEV).to(torch.bfloat16)
+    tok_h = rng.integers(0, V, P).astype(np.int64)
+    bad = tok_h.copy()
+    bad[P - 3] = V
+    em.ember_coalesce_rows(torch.from_numpy(bad).to(DEV), U, V, co.idx, co.G_rows, co.n_out, co.ws)
+    assert em.ember_get_error(co.ws) == em.EMBER_ERR_INDEX and int(co.n_out.item()) == -1
+    run_case(em, tok_h, U, V, torch.bfloat16, f"heads{P}")
+
+
 def test_coalesce_is_bitwise_reproducible(em):
     cfg = wl.Config("co_det", 128256, 512, torch.bfloat16, torch.bfloat16, 1, "sparse_zipf", batch_tokens=20000)
     tok, U = wl.make_token_batch(cfg, 1, seed=3, device=DEV)
