@@ -151,10 +151,15 @@ int ember_step_sparse_rows(void* W, int w_dtype, int64_t ldw,
  * memory, read when the step runs; max_rows (host) bounds it and sizes the
  * launches; G_rows and idx must hold max_rows rows.  A device count outside
  * [0, max_rows] is reported like an index error (EMBER_ERR_INDEX through
- * ember_get_error; W, r and c untouched).  With *n_idx_dev == max_rows the
- * result is the same, bit for bit, as ember_step_sparse_rows with n_idx =
- * max_rows; other counts partition the rows differently and agree within the
- * stated tolerances.  Everything else as for ember_step_sparse_rows.
+ * ember_get_error; W, r and c untouched).  The step takes the one-launch form
+ * of ember_step_sparse_rows whenever the count fits it: decided on the host
+ * when max_rows fits, else on the device from the count (the one-launch kernel
+ * runs first and, when it has taken the step, the three launches of the other
+ * form return at once).  With *n_idx_dev == max_rows, or a count that takes the
+ * one-launch form, the result is the same, bit for bit, as
+ * ember_step_sparse_rows with n_idx = that count; other counts partition the
+ * rows differently and agree within the stated tolerances.  Everything else as
+ * for ember_step_sparse_rows.
  */
 int ember_step_sparse_rows_devn(void* W, int w_dtype, int64_t ldw,
                                 const void* G_rows, int g_dtype, int64_t ldg,

@@ -103,7 +103,16 @@ int run_step(StepArgs& a, float lr, float beta2, float eps, int64_t t, int maxim
         });
         return e == hipSuccess ? EMBER_OK : EMBER_ERR_HIP;
     }
-    hipError_t e = timed("ember_stats", s, [&] { return ember::launch_stats(a, s); });
+    // A device-count step whose maximum does not fit may still hold few enough
+    // rows: the one-launch kernel reads the count and takes the step when it
+    // fits (marking that in the workspace), and the three launches below then
+    // return at once; otherwise they take it.
+    hipError_t e = hipSuccess;
+    if (a.n_dev != nullptr && ember::onchip_shape_fits(a)) {
+        a.taken = reinterpret_cast<int*>(a.ws + ember::ws_layout(a.V, a.D).taken);
+        e = timed("ember_sparse_onchip", s, [&] { return ember::launch_sparse_onchip(a, ember::onchip_space(a), s); });
+    }
+    if (e == hipSuccess) e = timed("ember_stats", s, [&] { return ember::launch_stats(a, s); });
     if (e == hipSuccess) e = timed("ember_finalize", s, [&] { return ember::launch_finalize(a, s); });
     // lr == 0 leaves every weight bit unchanged, so the dense step skips the
     // apply pass; the sparse apply pass also clears the index-error flag for the

@@ -321,6 +321,7 @@ struct StatsParams {
     int64_t V;
     int* slot;
     int* flag;
+    const int* taken;     // set: the one-launch kernel may have taken this step (then return)
 };
 
 // Sums N values per lane over the 64 lanes, N rows at once (reduce-scatter
@@ -527,6 +528,7 @@ __device__ __forceinline__ void stats_block(const StatsParams& a, unsigned blk, 
 template <typename GT, int M, int R, bool kSparse, bool kWide>
 __global__ __launch_bounds__(kBlock) void ember_stats(StatsParams a) {
     __shared__ float lds[kWaves][kWave * 16 / sizeof(GT)];
+    if (a.taken != nullptr && *a.taken != 0) return;
     stats_block<GT, M, R, kSparse, kWide>(a, blockIdx.x, lds);
 }
 
@@ -594,6 +596,7 @@ struct FinParams {
     float* scale;          // sqrt(1 / (bias s)) / alpha_s
     double inv_bias;
     double inv_alpha;
+    const int* taken;      // set: the one-launch kernel may have taken this step (then return)
 };
 
 // Run by the last block of the finalize pass, once every r, c and partial sum
@@ -674,6 +677,7 @@ __device__ __forceinline__ void finalize_block(const FinParams& a, int blk, int 
 template <bool kSparse>
 __global__ __launch_bounds__(kFinThreads) void ember_finalize(FinParams a) {
     __shared__ FinLds sh;
+    if (a.taken != nullptr && *a.taken != 0) return;
     finalize_block<kSparse>(a, (int)blockIdx.x, (int)gridDim.x, sh);
 }
 
@@ -780,6 +784,7 @@ struct ApplyParams {
     float eps_over_alpha; // eps / alpha_s
     const int* status;    // sparse only: skip when the statistics pass flagged idx
     int* flag;            // sparse only: cleared for the next step
+    const int* taken;     // set: the one-launch kernel may have taken this step (then return)
 };
 
 // Block `blk` of the `nblk` apply blocks of one table.
@@ -871,6 +876,7 @@ __device__ __forceinline__ void apply_block(const ApplyParams& a, unsigned blk, 
 
 template <typename GT, typename WT, int M, int R, bool kSparse>
 __global__ __launch_bounds__(kBlock) void ember_apply(ApplyParams a) {
+    if (a.taken != nullptr && *a.taken != 0) return;
     apply_block<GT, WT, M, R, kSparse>(a, blockIdx.x, gridDim.x);
 }
 
@@ -1388,6 +1394,9 @@ struct OnchipParams {
     float* qa;              // [D rounded up to 8]: column factors sqrt(c_j)
     float* cnew;            // [D]: the new c, stored in phase 3
     int64_t spin_ticks;     // bound of a barrier wait in real-time counter ticks
+    int* taken;             // device-count steps beyond the launch's row capacity: 1 when this
+                            // launch takes the step (the count fits), else 0 and nothing is done;
+                            // null when the host already knows the rows fit
 };
 
 __device__ __forceinline__ int ld_agent_i(const int* p) {
@@ -1485,6 +1494,13 @@ __global__ __launch_bounds__(kOnchipThreads, 1) void ember_sparse_onchip(OnchipP
     // ---- phase 1: load the rows, row and column sums of g^2, row marks ----
     bool bad_count = false;
     const int64_t n = active_rows(a.n_dev, a.rows, bad_count);
+    if (a.taken != nullptr) {
+        // the count decides (the same in every block): more rows per block than
+        // the waves hold and the three-launch form takes the step instead
+        const bool fits = (n + NB - 1) / NB <= (int64_t)a.q_lanes * U;
+        if (b == 0 && threadIdx.x == 0) *a.taken = fits ? 1 : 0;
+        if (!fits) return;
+    }
     int64_t r0, r1;
     row_range(n, NB, b, r0, r1);
     const int nloc = (int)(r1 - r0);
@@ -1959,7 +1975,8 @@ WsLayout ws_layout(int64_t V, int64_t D) {
     L.scale = off + 12;
     L.epoch = off + 16;
     L.oflag = off + 20;
-    off = align256(28);
+    L.taken = off + 28;
+    off = align256(32);
     L.arrive = off;
     off = align256(off + (size_t)kOnchipBlocks * kArriveStride * 4);
     L.slot = off;
@@ -2016,6 +2033,7 @@ static StatsParams stats_params(const StepArgs& a) {
     p.V = a.V;
     p.slot = reinterpret_cast<int*>(a.ws + L.slot);
     p.flag = reinterpret_cast<int*>(a.ws + L.flag);
+    p.taken = a.taken;
     return p;
 }
 
@@ -2056,6 +2074,7 @@ static FinParams finalize_params(const StepArgs& a) {
     p.scale = reinterpret_cast<float*>(a.ws + L.scale);
     p.inv_bias = a.inv_bias;
     p.inv_alpha = a.inv_alpha;
+    p.taken = a.taken;
     return p;
 }
 
@@ -2097,6 +2116,7 @@ static ApplyParams apply_params(const StepArgs& a) {
     p.eps_over_alpha = a.eps_over_alpha;
     p.status = reinterpret_cast<const int*>(a.ws + L.status);
     p.flag = reinterpret_cast<int*>(a.ws + L.flag);
+    p.taken = a.taken;
     return p;
 }
 
@@ -2160,14 +2180,19 @@ bool onchip_resident(int g_dtype, int w_dtype, int m) {
 
 } // namespace
 
-bool onchip_fits(const StepArgs& a) {
+bool onchip_shape_fits(const StepArgs& a) {
     if (!a.sparse || a.c == nullptr) return false;
     const ColPlan cp = col_plan(a.D, a.g_dtype);
     // whole 16-byte chunks only (rows are read through buffer resources)
     if (cp.nslab > kOnchipWaves || a.D % cp.epc != 0) return false;
-    const int64_t per_block = (a.rows + kOnchipBlocks - 1) / kOnchipBlocks;
-    if (per_block > (int64_t)(kOnchipWaves / cp.nslab) * onchip_units_for(a.g_dtype, a.w_dtype)) return false;
     return onchip_resident(a.g_dtype, a.w_dtype, cp.m);
+}
+
+bool onchip_fits(const StepArgs& a) {
+    if (!onchip_shape_fits(a)) return false;
+    const ColPlan cp = col_plan(a.D, a.g_dtype);
+    const int64_t per_block = (a.rows + kOnchipBlocks - 1) / kOnchipBlocks;
+    return per_block <= (int64_t)(kOnchipWaves / cp.nslab) * onchip_units_for(a.g_dtype, a.w_dtype);
 }
 
 OnchipSpace onchip_space(const StepArgs& a) {
@@ -2222,6 +2247,7 @@ hipError_t launch_sparse_onchip(const StepArgs& a, const OnchipSpace& sp, hipStr
     p.qa = reinterpret_cast<float*>(sp.base + sp.qa);
     p.cnew = reinterpret_cast<float*>(sp.base + sp.cnew);
     p.spin_ticks = a.spin_ticks;
+    p.taken = a.taken;
     // A plain launch: the residency check above (blocks per compute unit x
     // compute units >= kOnchipBlocks) is what the grid barriers rely on, and
     // their bounded waits turn a violation into EMBER_ERR_DEVICE instead of a

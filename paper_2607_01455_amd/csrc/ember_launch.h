@@ -98,6 +98,7 @@ struct WsLayout {
     size_t scale;   // float: sqrt(1 / (bias s)) / alpha_s of the last step
     size_t epoch;   // uint32: one-launch sparse steps taken (numbers their grid barriers)
     size_t oflag;   // int32[2]: error bits of the one-launch sparse steps, by epoch parity
+    size_t taken;   // int32: 1 when the one-launch kernel took the current device-count step
     size_t arrive;  // uint32[kOnchipBlocks * kArriveStride]: last barrier number of each block
     size_t slot;    // int32[V]: 1 + position in idx of a touched row, else 0
     size_t zero_end;// [0, zero_end) must be zero before the first step
@@ -123,6 +124,9 @@ struct StepArgs {
     bool sparse;        // sparse-row step: G holds `rows` rows mapped through idx
     const int64_t* idx;    // sparse steps: device array of `rows` row indices
     const int64_t* n_dev;  // sparse steps: row count in device memory (rows is then its maximum), or null
+    int* taken;         // device-count steps whose maximum is too large for the one-launch form: written
+                        // by that launch (1: it took the step, the three launches then return at once),
+                        // or null
     int64_t rows;       // V (dense) or n_idx (sparse)
     float* r;
     float* c;
@@ -152,6 +156,9 @@ constexpr int64_t kOnchipSpinTicks = 100000000;   // ~1 s: a barrier wait that l
 // True when the step's rows fit the launch (dtypes, slabs and row count) and
 // the current device keeps every block of it resident.
 bool onchip_fits(const StepArgs& a);
+// The same without the row count: the launch could take the step for a count
+// small enough (a device-count step decides on the device).
+bool onchip_shape_fits(const StepArgs& a);
 // Byte offsets (from base) of the regions the one-launch step uses.
 struct OnchipSpace {
     char* base;

@@ -93,6 +93,42 @@ def test_full_count_is_bitwise_the_host_count_step(em, row_only):
     _tables_equal(outs[0], outs[1])
 
 
+def test_count_decides_the_form_on_the_device(em):
+    # a maximum of 8192 rows, more than the one-launch form holds at D = 4096
+    # bf16 (20 rows per block, 5120 in all): a count that fits takes that form
+    # (marked in the workspace word after the status words), a larger one the
+    # three launches; the result is the host-count step's, bit for bit, where
+    # the partitions agree (a count that fits, or the maximum itself)
+    V, D, max_rows = 20000, 4096, 8192
+    cfg = wl.Config("devn_choice", V, D, torch.bfloat16, torch.bfloat16, 1, "sparse_zipf", batch_tokens=max_rows)
+    rng = np.random.default_rng(43)
+    W_dev = wl.make_weights(cfg, seed=43, device=DEV)
+    W_host = W_dev.clone()
+    A = em.EmberTable(V, D, device=DEV)
+    B = em.EmberTable(V, D, device=DEV)
+    g = torch.Generator(device=DEV).manual_seed(43)
+    counts = [3000, max_rows, 100, 5120, 0, max_rows, 5121]
+    for t, n in enumerate(counts, start=1):
+        print(f"device-count step t={t} n={n} max={max_rows}", flush=True)
+        ids = rng.permutation(V)[:max_rows].astype(np.int64)
+        idx = torch.from_numpy(ids).to(DEV)
+        Gr = (torch.randn(max_rows, D, generator=g, device=DEV) * 1e-3).to(torch.bfloat16)
+        n_dev = torch.tensor([n], dtype=torch.int64, device=DEV)
+        em.ember_step_sparse_rows_devn(W_dev, Gr, idx, n_dev, A.r, A.c, t, LR, B2, EPS, False, A.ws)
+        assert em.ember_get_error(A.ws) == em.EMBER_OK
+        taken = int(A.ws[28:32].view(torch.int32).item())
+        assert taken == (1 if n <= 5120 else 0), f"n={n}: taken={taken}"
+        em.ember_step_sparse_rows(W_host, Gr[:n], idx[:n], B.r, B.c, t, LR, B2, EPS, False, B.ws)
+        assert em.ember_get_error(B.ws) == em.EMBER_OK
+        if n <= 5120 or n == max_rows:
+            _tables_equal((W_dev, A.r, A.c), (W_host, B.r, B.c))
+        else:
+            # other partitions of the same rows: the same step up to rounding
+            assert torch.allclose(A.r, B.r, rtol=1e-5, atol=0)
+            assert torch.allclose(A.c, B.c, rtol=1e-5, atol=0)
+            assert torch.allclose(W_dev.float(), W_host.float(), rtol=1e-2, atol=1e-6)
+
+
 @pytest.mark.parametrize("row_only", [False, True])
 def test_bad_counts_and_coalescing_errors_leave_the_table_untouched(em, row_only):
     V, D = 1000, 128
