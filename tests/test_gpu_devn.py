@@ -218,3 +218,59 @@ def test_captured_steps_replay_bitwise(em, row_only):
         assert em.ember_get_error(te.ws) == em.EMBER_OK and em.ember_get_error(co.ws) == em.EMBER_OK
         _tables_equal((Wh, th.r, th.c), (Wh2, th2.r, th2.c))
         _tables_equal((We, te.r, te.c), (We2, te2.r, te2.c))
+
+
+def test_captured_count_choice_replays_bitwise(em):
+    """A captured device-count step whose maximum (8192 rows at D = 4096 bf16)
+    is beyond the one-launch form: each replay decides the form from the count
+    it finds (3000 and 100 rows fit, 8192 and 5121 do not) and must give the
+    bits of the same step run eagerly on a twin table."""
+    V, D, max_rows = 20000, 4096, 8192
+    cfg = wl.Config("g_choice", V, D, torch.bfloat16, torch.bfloat16, 1, "sparse_zipf", batch_tokens=max_rows)
+    W = wl.make_weights(cfg, seed=47, device=DEV)
+    W2 = W.clone()
+    A = em.EmberTable(V, D, device=DEV)
+    B = em.EmberTable(V, D, device=DEV)
+    idx_s = torch.empty(max_rows, dtype=torch.int64, device=DEV)
+    G_s = torch.empty(max_rows, D, dtype=torch.bfloat16, device=DEV)
+    n_s = torch.zeros(1, dtype=torch.int64, device=DEV)
+    rng = np.random.default_rng(47)
+    g = torch.Generator(device=DEV).manual_seed(47)
+    t_fixed = 3   # the step counter is a launch argument: a captured step keeps its t
+
+    def inputs(n):
+        idx = torch.from_numpy(rng.permutation(V)[:max_rows].astype(np.int64)).to(DEV)
+        G = (torch.randn(max_rows, D, generator=g, device=DEV) * 1e-3).to(torch.bfloat16)
+        return idx, G, torch.tensor([n], dtype=torch.int64, device=DEV)
+
+    def step(W_, T, idx, G, n):
+        em.ember_step_sparse_rows_devn(W_, G, idx, n, T.r, T.c, t_fixed, LR, B2, EPS, False, T.ws)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        idx0, G0, n0 = inputs(3000)
+        idx_s.copy_(idx0)
+        G_s.copy_(G0)
+        n_s.copy_(n0)
+        step(W, A, idx_s, G_s, n_s)
+        step(W2, B, idx0, G0, n0)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    _tables_equal((W, A.r, A.c), (W2, B.r, B.c))
+
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step(W, A, idx_s, G_s, n_s)
+    for n in (8192, 100, 5121, 3000, 8192):
+        print(f"graph replay with n={n}", flush=True)
+        idx, G, nd = inputs(n)
+        idx_s.copy_(idx)
+        G_s.copy_(G)
+        n_s.copy_(nd)
+        graph.replay()
+        step(W2, B, idx, G, nd)   # eager twin
+        torch.cuda.synchronize()
+        assert em.ember_get_error(A.ws) == em.EMBER_OK and em.ember_get_error(B.ws) == em.EMBER_OK
+        assert int(A.ws[28:32].view(torch.int32).item()) == (1 if n <= 5120 else 0)
+        _tables_equal((W, A.r, A.c), (W2, B.r, B.c))
