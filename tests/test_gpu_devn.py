@@ -127,6 +127,19 @@ def test_count_decides_the_form_on_the_device(em):
             assert torch.allclose(A.r, B.r, rtol=1e-5, atol=0)
             assert torch.allclose(A.c, B.c, rtol=1e-5, atol=0)
             assert torch.allclose(W_dev.float(), W_host.float(), rtol=1e-2, atol=1e-6)
+    # a count outside [0, max]: the one-launch kernel takes it as a refused
+    # step (the table is left alone, the index error reported), and the next
+    # valid count steps normally
+    before = (W_dev.clone(), A.r.clone(), A.c.clone())
+    for bad in (-1, max_rows + 1):
+        n_dev = torch.tensor([bad], dtype=torch.int64, device=DEV)
+        em.ember_step_sparse_rows_devn(W_dev, Gr, idx, n_dev, A.r, A.c, len(counts) + 1, LR, B2, EPS, False, A.ws)
+        assert em.ember_get_error(A.ws) == em.EMBER_ERR_INDEX
+        assert int(A.ws[28:32].view(torch.int32).item()) == 1
+        _tables_equal(before, (W_dev, A.r, A.c))
+    n_dev = torch.tensor([2000], dtype=torch.int64, device=DEV)
+    em.ember_step_sparse_rows_devn(W_dev, Gr, idx, n_dev, A.r, A.c, len(counts) + 1, LR, B2, EPS, False, A.ws)
+    assert em.ember_get_error(A.ws) == em.EMBER_OK
 
 
 @pytest.mark.parametrize("row_only", [False, True])
