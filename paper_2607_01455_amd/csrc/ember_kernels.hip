@@ -898,6 +898,12 @@ constexpr int kRowOnlyRows = 2;                          // rows in flight per b
 constexpr int kRowOnlyMaxWaves = 8;                      // waves per block
 constexpr int kRowOnlyRowsPerBlock = 16;                 // rows per block
 constexpr int kRowOnlyWaveRows = 2;                      // rows in flight per wave (one-wave rows)
+// The single-table sparse step of the one-wave kernel: one row per wave and
+// one row per wave of a block, so the few thousand rows of a batch are all in
+// flight at once (about half the registers, more waves per SIMD) instead of
+// taking two rounds of two rows per wave.
+constexpr int kRowOnlySparseRowsPerBlock = 4;
+constexpr int kRowOnlySparseWaveRows = 1;
 constexpr int kRowOnlyWaveChunks = 16 * kWave;           // longest row held by one wave, in chunks
 
 struct RowOnlyParams {
@@ -912,6 +918,7 @@ struct RowOnlyParams {
     int nslab;
     int64_t nb;            // row blocks
     int64_t nvb;           // row blocks + decay blocks (sparse)
+    int rows_per_block;    // gradient rows per row block
     const int64_t* idx;    // sparse only
     const int64_t* n_dev;  // sparse only: device row count, or null
     float* r;
@@ -942,8 +949,8 @@ __device__ __forceinline__ void rowonly_rows(const RowOnlyParams& a, int64_t nro
     const int nw = blockDim.x / kWave;
     const bool update = a.inv_alpha != 0.0f;
 
-    const int64_t r0 = vb * kRowOnlyRowsPerBlock;
-    const int64_t r1 = min(r0 + kRowOnlyRowsPerBlock, nrows);
+    const int64_t r0 = vb * a.rows_per_block;
+    const int64_t r1 = min(r0 + a.rows_per_block, nrows);
     const GT* G = static_cast<const GT*>(a.G);
     WT* W = static_cast<WT*>(a.W);
     const double invD = 1.0 / (double)a.D;
@@ -1113,13 +1120,13 @@ template <typename GT, typename WT, int C, bool kSparse, bool kExact, bool kRunt
 __device__ __forceinline__ void rowonly_wave_rows(const RowOnlyParams& a, int64_t nrows, int64_t vb,
                                                   bool sparse_rt = false) {
     constexpr int EPC = 16 / (int)sizeof(GT);
-    constexpr int R = kRowOnlyWaveRows;
+    constexpr int R = (kSparse && !kRuntime) ? kRowOnlySparseWaveRows : kRowOnlyWaveRows;
     constexpr int kWBytes = EPC * (int)sizeof(WT);   // bytes of W per chunk
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const bool update = a.inv_alpha != 0.0f;
-    const int64_t r0 = vb * kRowOnlyRowsPerBlock;
-    const int64_t r1 = min(r0 + kRowOnlyRowsPerBlock, nrows);
+    const int64_t r0 = vb * a.rows_per_block;
+    const int64_t r1 = min(r0 + a.rows_per_block, nrows);
     const GT* G = static_cast<const GT*>(a.G);
     WT* W = static_cast<WT*>(a.W);
     const double invD = 1.0 / (double)a.D;
@@ -2350,6 +2357,7 @@ static RowOnlyParams rowonly_params(const StepArgs& a) {
     p.total_chunks = cp.total_chunks;
     p.slab_chunks = cp.slab_chunks;
     p.nslab = cp.nslab;
+    p.rows_per_block = kRowOnlyRowsPerBlock;
     p.nb = (a.rows + kRowOnlyRowsPerBlock - 1) / kRowOnlyRowsPerBlock;
     p.idx = a.idx;
     p.n_dev = a.n_dev;
@@ -2384,10 +2392,15 @@ hipError_t launch_rowonly(const StepArgs& a, hipStream_t s) {
     const int spw = cp.nslab <= kRowOnlyMaxWaves ? 1 : 2;
     const int waves = resident ? (cp.nslab + spw - 1) / spw : kRowOnlyMaxWaves;
     if ((spw == 2 || !resident) && cp.m != 2) return hipErrorInvalidValue;
-    const RowOnlyParams p = rowonly_params(a);
+    RowOnlyParams p = rowonly_params(a);
+    const int c = rowonly_wave_chunks(a);
+    if (c > 0 && a.sparse) {
+        p.rows_per_block = kRowOnlySparseRowsPerBlock;
+        p.nb = (a.rows + p.rows_per_block - 1) / p.rows_per_block;
+        p.nvb = p.nb + (a.V + kDecayRows - 1) / kDecayRows;
+    }
     if (p.nvb == 0) return hipSuccess;
     const dim3 grid((unsigned)capped_blocks(p.nvb));
-    const int c = rowonly_wave_chunks(a);
     if (c > 0)
         return a.sparse ? rowonly_wave_dispatch_t<true>(p, a.g_dtype, a.w_dtype, c, grid, s)
                         : rowonly_wave_dispatch_t<false>(p, a.g_dtype, a.w_dtype, c, grid, s);
