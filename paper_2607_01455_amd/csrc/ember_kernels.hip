@@ -919,6 +919,7 @@ struct RowOnlyParams {
     int64_t nb;            // row blocks
     int64_t nvb;           // row blocks + decay blocks (sparse)
     int rows_per_block;    // gradient rows per row block
+    int* tgroups;          // sparse only: first-level completion counters
     const int64_t* idx;    // sparse only
     const int64_t* n_dev;  // sparse only: device row count, or null
     float* r;
@@ -1228,11 +1229,24 @@ __device__ __forceinline__ void rowonly_decay(const RowOnlyParams& a, int err, i
 
 // Every block of the sparse step has read the error bits before it counts
 // itself; the last one clears them for the next step.
-__device__ __forceinline__ void rowonly_clear_flag(const RowOnlyParams& a, int nblocks, int* last) {
-    if (block_ticket(a.ticket, nblocks, last) && threadIdx.x == 0) {
-        *a.flag = 0;
-        *a.ticket = 0;
-    }
+// The count has two levels, so the blocks' atomics do not all queue on one
+// address: block b counts itself in group b % kTicketGroups (counters
+// kTicketStride words apart), and the last block of each group counts the
+// group at the top counter (the ticket word).  Each last block resets the
+// counter it completed.
+__device__ __forceinline__ void rowonly_clear_flag(const RowOnlyParams& a, int blk, int nblocks) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x != 0) return;
+    const int g = blk % kTicketGroups;
+    const int members = (nblocks - g + kTicketGroups - 1) / kTicketGroups;
+    const int groups = nblocks < kTicketGroups ? nblocks : kTicketGroups;
+    int* gc = a.tgroups + g * kTicketStride;
+    if (__hip_atomic_fetch_add(gc, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != members - 1) return;
+    *gc = 0;
+    if (__hip_atomic_fetch_add(a.ticket, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != groups - 1) return;
+    *a.ticket = 0;
+    *a.flag = 0;
 }
 
 // Dense: blocks [0, nb) over the V rows.  Sparse: the same over the n gradient
@@ -1241,7 +1255,7 @@ __device__ __forceinline__ void rowonly_clear_flag(const RowOnlyParams& a, int n
 // Block `blk` of the `nblk` blocks of one table (kRuntime: dense or sparse is
 // the uniform flag sparse_rt, one body for both kinds in a multi-table launch).
 template <typename GT, typename WT, int C, bool kSparseArg, bool kExact, bool kRuntime = false>
-__device__ __forceinline__ void rowonly_wave_block(const RowOnlyParams& a, unsigned blk, unsigned nblk, int* last,
+__device__ __forceinline__ void rowonly_wave_block(const RowOnlyParams& a, unsigned blk, unsigned nblk,
                                                    bool sparse_rt = false) {
     const bool kSparse = kRuntime ? sparse_rt : kSparseArg;
     if (!kSparse) {
@@ -1258,21 +1272,19 @@ __device__ __forceinline__ void rowonly_wave_block(const RowOnlyParams& a, unsig
         if (vb >= a.nb) rowonly_decay(a, err, vb - a.nb);
         else if (!err) rowonly_wave_rows<GT, WT, C, true, kExact, kRuntime>(a, nrows, vb, true);
     }
-    rowonly_clear_flag(a, (int)nblk, last);
+    rowonly_clear_flag(a, (int)blk, (int)nblk);
 }
 
 template <typename GT, typename WT, int C, bool kSparse, bool kExact>
 __global__ __launch_bounds__(kBlock) void ember_rowonly_wave(RowOnlyParams a) {
-    __shared__ int last;
-    rowonly_wave_block<GT, WT, C, kSparse, kExact>(a, blockIdx.x, gridDim.x, &last);
+    rowonly_wave_block<GT, WT, C, kSparse, kExact>(a, blockIdx.x, gridDim.x);
 }
 
 template <typename GT, typename WT, int C, bool kExact>
 __global__ __launch_bounds__(kBlock) void ember_rowonly_wave_multi(MultiParams<RowOnlyParams> g) {
-    __shared__ int last;
     const int k = multi_table(g.first, g.ntab);
     const RowOnlyParams p = g.p[k];
-    rowonly_wave_block<GT, WT, C, false, kExact, true>(p, blockIdx.x - g.first[k], g.first[k + 1] - g.first[k], &last,
+    rowonly_wave_block<GT, WT, C, false, kExact, true>(p, blockIdx.x - g.first[k], g.first[k + 1] - g.first[k],
                                                        g.sparse[k] != 0);
 }
 
@@ -1281,7 +1293,6 @@ template <typename GT, typename WT, int M, int S, bool kSparse, bool kResident>
 __global__ __launch_bounds__(kRowOnlyMaxWaves * kWave) void ember_rowonly(RowOnlyParams a) {
     __shared__ float part[kRowOnlyMaxWaves][kRowOnlyRows];
     __shared__ float rn_lds[kRowOnlyRows];
-    __shared__ int last;
     if (!kSparse) {
         if (blockIdx.x == 0 && threadIdx.x == 0) *a.status &= kFlagTimeout;
         for (int64_t vb = blockIdx.x; vb < a.nb; vb += gridDim.x)
@@ -1296,7 +1307,7 @@ __global__ __launch_bounds__(kRowOnlyMaxWaves * kWave) void ember_rowonly(RowOnl
         if (vb >= a.nb) rowonly_decay(a, err, vb - a.nb);
         else if (!err) rowonly_rows<GT, WT, M, S, true, kResident>(a, nrows, vb, part, rn_lds);
     }
-    rowonly_clear_flag(a, (int)gridDim.x, &last);
+    rowonly_clear_flag(a, (int)blockIdx.x, (int)gridDim.x);
 }
 
 // Sparse row-only step, first launch: validates idx and marks the touched rows
@@ -1986,6 +1997,8 @@ WsLayout ws_layout(int64_t V, int64_t D) {
     off = align256(32);
     L.arrive = off;
     off = align256(off + (size_t)kOnchipBlocks * kArriveStride * 4);
+    L.tgroups = off;
+    off = align256(off + (size_t)kTicketGroups * kTicketStride * 4);
     L.slot = off;
     off = align256(off + (size_t)V * 4);
     L.zero_end = off;
@@ -2371,6 +2384,7 @@ static RowOnlyParams rowonly_params(const StepArgs& a) {
     p.slot = reinterpret_cast<int*>(a.ws + L.slot);
     p.flag = reinterpret_cast<int*>(a.ws + L.flag);
     p.ticket = reinterpret_cast<int*>(a.ws + L.ticket);
+    p.tgroups = reinterpret_cast<int*>(a.ws + L.tgroups);
     p.status = reinterpret_cast<int*>(a.ws + L.status);
     const int64_t ndecay = a.sparse ? (a.V + kDecayRows - 1) / kDecayRows : 0;
     p.nvb = p.nb + ndecay;

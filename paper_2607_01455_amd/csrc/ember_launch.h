@@ -32,6 +32,8 @@ constexpr int kRowsPerBlockMin = 8; // fewer rows than this per block: fewer blo
 constexpr int kVRowsPerThread = 1; // rows per thread in the r pass of finalize
 constexpr int kFinCols = 64;        // columns per column block of finalize (16, 32 or 64)
 constexpr int kDecayRows = 1024;    // rows per decay block of the row-only sparse step
+constexpr int kTicketGroups = 16;   // first-level completion counters of the row-only sparse step ...
+constexpr int kTicketStride = 64;   // ... this many words (256 bytes) apart
 constexpr int64_t kMaxGridBlocks = (int64_t)1 << 20;  // launched blocks per kernel at most
 int64_t capped_blocks(int64_t blocks);
 
@@ -100,6 +102,8 @@ struct WsLayout {
     size_t oflag;   // int32[2]: error bits of the one-launch sparse steps, by epoch parity
     size_t taken;   // int32: 1 when the one-launch kernel took the current device-count step
     size_t arrive;  // uint32[kOnchipBlocks * kArriveStride]: last barrier number of each block
+    size_t tgroups; // int32[kTicketGroups * kTicketStride]: first-level completion counters of the
+                    // row-only sparse step
     size_t slot;    // int32[V]: 1 + position in idx of a touched row, else 0
     size_t zero_end;// [0, zero_end) must be zero before the first step
     size_t qa;      // float[D rounded up to 8]: column factors sqrt(c_j)
