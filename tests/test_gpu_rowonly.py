@@ -236,6 +236,37 @@ def test_rowonly_sparse_index_errors_leave_everything_untouched(em, bad):
     assert em.ember_get_error(tab.ws) == em.EMBER_OK
 
 
+def test_rowonly_sparse_error_and_recovery_with_many_blocks(em):
+    # ~1000 row blocks plus the decay blocks: every block counts itself in one
+    # of the completion counters before the last one clears the error bits;
+    # an index error, then valid steps, repeated, must each report correctly
+    cfg = wl.Config("ro_err_big", 20000, 1024, torch.bfloat16, torch.bfloat16, 1, "sparse_zipf",
+                    batch_tokens=4000)
+    W = wl.make_weights(cfg, seed=12, device=DEV)
+    tab = em.EmberTable(cfg.V, cfg.D, device=DEV, row_only=True)
+    twin_W = W.clone()
+    twin = em.EmberTable(cfg.V, cfg.D, device=DEV, row_only=True)
+    rng = np.random.default_rng(12)
+    g = torch.Generator(device=DEV).manual_seed(12)
+    for t in range(1, 4):
+        n = 4000
+        ids = rng.permutation(cfg.V)[:n].astype(np.int64)
+        Gr = (torch.randn(n, cfg.D, generator=g, device=DEV) * 1e-3).to(torch.bfloat16)
+        bad = ids.copy()
+        bad[n - 1] = bad[0]                      # a repeated id in the last block
+        before = (host_bits(W), tab.r.cpu().numpy())
+        em.ember_rowonly_step_sparse_rows(W, Gr, torch.from_numpy(bad).to(DEV), tab.r, t, LR, B2, EPS, False, tab.ws)
+        assert em.ember_get_error(tab.ws) == em.EMBER_ERR_INDEX
+        assert np.array_equal(host_bits(W), before[0]) and np.array_equal(tab.r.cpu().numpy(), before[1])
+        idx = torch.from_numpy(ids).to(DEV)
+        em.ember_rowonly_step_sparse_rows(W, Gr, idx, tab.r, t, LR, B2, EPS, False, tab.ws)
+        assert em.ember_get_error(tab.ws) == em.EMBER_OK
+        # the twin takes only the valid steps: the same bits
+        em.ember_rowonly_step_sparse_rows(twin_W, Gr, idx, twin.r, t, LR, B2, EPS, False, twin.ws)
+        assert em.ember_get_error(twin.ws) == em.EMBER_OK
+        assert torch.equal(W.view(torch.int16), twin_W.view(torch.int16)) and torch.equal(tab.r, twin.r)
+
+
 def test_rowonly_bitwise_reproducible_and_table_binding(em):
     cfg = wl.Config("ro_det", 20000, 1024, torch.bfloat16, torch.bfloat16, 2, "sparse_zipf",
                     batch_tokens=4000)
